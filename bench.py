@@ -1,0 +1,183 @@
+"""Decode-attention throughput on one MI355X at the Llama-3.1-8B 128K workload.
+
+One step = starkv_append of one new token per sequence from bf16 hidden states
+(down-projection + quantize/pack) followed by starkv_decode_attn over the whole
+context (split pass + combine pass), on one layer's cache.  Five layer caches
+(> 1 GB together) are used in rotation so the 256 MB last-level cache cannot
+serve the latent stream.  Inputs are seeded synthetic arrays of the workload's
+shape, resident in HBM before timing starts.
+
+Prints one JSON line; per-kernel times are measured with HIP events on the
+stream the kernels run on.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, inp, sample_ctx: int):
+    """The fp64 oracle on one sequence (all heads) over the first sample_ctx tokens, scaled
+    linearly to the full context."""
+    from oracle import oracle as O
+    cfg = O.make_cfg(1, w.n_q_heads, w.n_kv_heads, w.head_dim, sample_ctx, inp.key_rank,
+                     w.value_rank, w.qmode, w.rope_theta)
+    cache = O.new_cache(cfg)
+    O.append(cfg, cache, np.ascontiguousarray(inp.latents[:1, :sample_ctx]), [0])
+    t0 = time.perf_counter()
+    _, threads = O.decode_attn(cfg, cache, np.ascontiguousarray(inp.q[:1]), True, inp.Bk,
+                               inp.Bv, np.array([sample_ctx], np.int32))
+    dt = time.perf_counter() - t0
+    full = dt * (w.ctx / sample_ctx)            # seconds for one decode token at full context
+    return {"value": 1.0 / full, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": (f"1 sequence x {w.n_q_heads} query heads over the first {sample_ctx} of "
+                       f"{w.ctx} tokens took {dt:.2f} s; scaled linearly in context length")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="c3")
+    ap.add_argument("--layers", type=int, default=5)
+    ap.add_argument("--cpu-sample-ctx", type=int, default=32768)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(decode attention shards by batch or context; see the design notes).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_08382_amd import starkv as S
+    from paper_2606_08382_amd import synth
+    from paper_2606_08382_amd.device import Layer, to_dev
+
+    w = synth.WORKLOADS[args.workload]
+    torch.cuda.set_device(0)
+    log(f"generating {w.name}")
+    inp = synth.generate(w, with_hidden=w.d_model > 0, n_hidden_tokens=1)
+    B, L = w.batch, w.ctx
+    layers = []
+    lat_chunk = 16384
+    for li in range(args.layers):
+        layer = Layer(B, w.n_q_heads, w.n_kv_heads, w.head_dim, L, inp.key_rank, w.value_rank,
+                      w.qmode, w.rope_theta, w.q_dtype, w.out_dtype, d_model=w.d_model)
+        pos = torch.zeros(B, dtype=torch.int32, device="cuda")
+        for t0 in range(0, L, lat_chunk):
+            chunk = to_dev(np.ascontiguousarray(inp.latents[:, t0:t0 + lat_chunk]))
+            # the caches are filled through a latent-input plan with the same layout
+            S.starkv_append(_fill_plan(layer, w, inp), layer.cache, chunk, None, pos + t0,
+                            chunk.shape[1], None, 0)
+        layers.append(layer)
+        log(f"layer {li} filled ({S.starkv_cache_bytes(layer.plan) / 1e6:.1f} MB)")
+    torch.cuda.synchronize()
+    q = to_dev(inp.q)
+    Bk, Bv = to_dev(inp.Bk), to_dev(inp.Bv)
+    ctx = to_dev(inp.ctx_len)
+    x = to_dev(inp.x) if inp.x is not None else None
+    A = to_dev(inp.A) if inp.A is not None else None
+    pos_new = to_dev((inp.ctx_len - 1).astype(np.int32))
+    stream = torch.cuda.current_stream()
+    n_ev = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(n_ev)]
+
+    def step(i, events=None):
+        layer = layers[i % len(layers)]
+        if events:
+            events[0].record(stream)
+        if x is not None:
+            layer.append(x, pos_new, A_all=A)
+        if events:
+            events[1].record(stream)
+        S.starkv_decode_split(layer.plan, layer.cache, q, Bk, ctx, L, layer.dec_ws)
+        if events:
+            events[2].record(stream)
+        S.starkv_decode_combine(layer.plan, Bv, ctx, L, layer.out, layer.dec_ws)
+        if events:
+            events[3].record(stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i, ev[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    t_app = np.array([e[0].elapsed_time(e[1]) for e in ev])
+    t_split = np.array([e[1].elapsed_time(e[2]) for e in ev])
+    t_comb = np.array([e[2].elapsed_time(e[3]) for e in ev])
+    ms_step = wall * 1e3 / args.steps
+    tokens = int(inp.ctx_len.sum())
+    layout = S.starkv_cache_layout(layers[0].plan)
+    per_token = (sum(layout.key_row_bytes[g] + 4 * layout.key_groups[g]
+                     for g in range(w.n_kv_heads))
+                 + layout.value_row_bytes + 4 * layout.value_groups)
+    alg_bytes = per_token * tokens
+    split_s = float(t_split.mean()) / 1e3
+    achieved = alg_bytes / split_s / 1e9
+    log(f"append {t_app.mean() * 1e3:.1f} us  split {t_split.mean() * 1e3:.1f} us "
+        f"(median {np.median(t_split) * 1e3:.1f})  combine {t_comb.mean() * 1e3:.1f} us  "
+        f"wall/step {ms_step * 1e3:.1f} us")
+    result = {
+        "metric": "decode-attention tokens/s at 128K ctx; achieved HBM GB/s vs peak",
+        "value": B / (ms_step / 1e3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": B, "ctx": L, "q_heads": w.n_q_heads,
+                   "kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
+                   "key_ranks": inp.key_rank, "value_rank": w.value_rank,
+                   "cache": "int8/int4 mixed, 32-channel groups", "layers_rotated": args.layers,
+                   "append": f"{w.append_tokens} token/seq from bf16 hidden {w.d_model}"},
+        "kernels_us": {"append": float(t_app.mean() * 1e3), "decode_split": float(t_split.mean() * 1e3),
+                       "decode_combine": float(t_comb.mean() * 1e3)},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "decode_split", "alg_bytes_per_launch": alg_bytes,
+                     "bytes_per_token": per_token},
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
+        result["cpu_baseline"] = cpu_baseline(w, inp, min(args.cpu_sample_ctx, L))
+    print(json.dumps(result), flush=True)
+
+
+_fill_plans = {}
+
+
+def _fill_plan(layer, w, inp):
+    """A plan with the layer's cache layout taking fp16 latents directly (d_model = 0), used to
+    fill the caches before timing."""
+    from paper_2606_08382_amd import starkv as S
+    key = id(layer)
+    if key not in _fill_plans:
+        cfg = S.make_config(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.ctx, inp.key_rank,
+                            w.value_rank, w.qmode, w.rope_theta, d_model=0,
+                            q_dtype=w.q_dtype, out_dtype=w.out_dtype)
+        _fill_plans[key] = S.starkv_plan_create(cfg)
+    return _fill_plans[key]
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,222 @@
+/*
+ * starkv.h -- decode attention read directly from a low-rank, quantized KV cache
+ * (STAR-KV), for AMD Instinct MI355X (gfx950).
+ *
+ * The method (paper sections in brackets):
+ *   keys    K = (x . (Sigma V)_K,g) . U_K,g^T   one latent of rank r_g per KV head
+ *           (head-wise decomposition)                               [Sec. 3.2, 4.3.3]
+ *   values  V = (x . (Sigma V)_V) . U_V^T       one latent of rank r_v shared by all
+ *           heads of the layer (joint decomposition)                [Sec. 3.2, 4.3.3]
+ *   cache   the latents, quantized per token: an outlier block of leading
+ *           channels at 8 bits and an inlier block at 4 bits        [Sec. 4.4, Eq. Z-hat]
+ *   decode  keys are rebuilt from the latents, rotated with RoPE at their
+ *           position (RoPE blocks absorbing U_K into W_Q)           [Sec. 3.3]
+ *           and scored against q with a softmax over the context    [Sec. 3.1];
+ *           values are reordered: the probabilities weight the shared latent
+ *           V' and U_V is applied once per query head               [Sec. 3.3]
+ *           (the fused key and value kernels and the stacked p.V' GEMM of
+ *           App. A.6, "Operation Fusion" and "Attention with GEMM").
+ * The block-wise Hadamard rotation of Sec. 4.4 is fused offline into the
+ * factors; this library takes the factors as given.
+ *
+ * Conventions for every entry point:
+ *   - The caller owns all device memory (cache, q, factors, outputs, workspace)
+ *     and the plan's lifetime.  The library never allocates or frees device
+ *     memory and never synchronizes.
+ *   - Device work is enqueued on the given HIP stream and is complete when the
+ *     stream is.  Pointers documented as "device" must be device-accessible.
+ *   - Argument errors are reported synchronously, before anything is launched.
+ *     A failed launch returns STARKV_ERR_HIP.  No C++ exception crosses this
+ *     interface and nothing aborts.  starkv_last_error() gives a detail string
+ *     for the calling thread's last failure.
+ *   - Calls that write the same cache rows, or share a workspace, race if they
+ *     overlap on different streams.
+ */
+#ifndef STARKV_H
+#define STARKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* starkv_stream_t;   /* a hipStream_t; NULL = default stream */
+
+typedef enum {
+  STARKV_OK = 0,
+  STARKV_ERR_INVALID_ARG = 1,   /* null/ill-formed argument, inconsistent sizes */
+  STARKV_ERR_UNSUPPORTED = 2,   /* well-formed but outside what the kernels implement */
+  STARKV_ERR_CAPACITY = 3,      /* a length beyond the cache capacity */
+  STARKV_ERR_WORKSPACE = 4,     /* workspace missing or smaller than required */
+  STARKV_ERR_ALIGNMENT = 5,     /* a device pointer not aligned as documented */
+  STARKV_ERR_HIP = 6            /* the HIP runtime reported an error */
+} starkv_status;
+
+/* Cache precision (Sec. 4.4; bit widths per this library's formats):
+ *   F16     latents stored as fp16, no quantization;
+ *   INT4    every channel 4-bit;
+ *   MIX8_4  the leading r_out = 8*ceil(r/32) channels (about 25 %, the outlier
+ *           block; the latent channels are ordered by singular value) at 8 bits,
+ *           the remaining channels (inlier block) at 4 bits. */
+typedef enum { STARKV_Q_F16 = 0, STARKV_Q_INT4 = 1, STARKV_Q_MIX8_4 = 2 } starkv_qmode;
+
+typedef enum { STARKV_DT_F16 = 0, STARKV_DT_BF16 = 1 } starkv_dtype;
+
+#define STARKV_MAX_KV_HEADS 16
+#define STARKV_MAX_Q_HEADS 64
+
+typedef struct {
+  int32_t batch;          /* sequences B */
+  int32_t n_q_heads;      /* H_q, a multiple of n_kv_heads, <= 64 */
+  int32_t n_kv_heads;     /* H_kv <= 16; query head i reads KV head floor(i*H_kv/H_q) */
+  int32_t head_dim;       /* d: 64 or 128 */
+  int32_t capacity;       /* rows per sequence in the cache, >= 1 */
+  const int32_t* key_rank;/* host array [H_kv]: r_g, multiples of 16 in [16, d] (copied) */
+  int32_t value_rank;     /* r_v: a multiple of 16 in [16, min(H_kv*d, 1024)] */
+  int32_t qmode;          /* starkv_qmode */
+  int32_t group_size;     /* quantization group, must be 32 */
+  double  rope_theta;     /* RoPE base, > 1 */
+  int32_t d_model;        /* hidden size for starkv_append's down-projection; 0 = latents given */
+  int32_t q_dtype;        /* starkv_dtype of q */
+  int32_t out_dtype;      /* starkv_dtype of the attention output */
+  int32_t x_dtype;        /* starkv_dtype of hidden states (when d_model > 0) */
+} starkv_config;
+
+typedef struct starkv_plan starkv_plan;   /* opaque, immutable after creation */
+
+/* ------------------------------------------------------------------------------
+ * Cache format.  All integers little-endian, fp16 as IEEE binary16.
+ * Rows (token positions) per sequence are padded to Cp = ceil(capacity/256)*256.
+ * The cache is a sequence of planes, each starting on a 256-byte boundary, in
+ * this order: for g = 0..H_kv-1 {key code plane g, key meta plane g}, then the
+ * value code plane, then the value meta plane.  Meta planes of F16 caches are
+ * empty.
+ *
+ * A latent block of rank r (key head g: r = r_g; values: r = r_v) has regions:
+ * F16: one region, 16-bit values.  INT4: one 4-bit region.  MIX8_4: 8-bit
+ * channels [0, r_out), 4-bit channels [r_out, r).  Each quantized region is split
+ * into groups of 32 channels from the region start (the last may be shorter);
+ * groups are numbered 8-bit first.  Per token and group: z = min over the
+ * group's fp16 values, s = the smallest fp16 >= (max - min)/(2^b - 1) (s = 0 when
+ * max == min), code = round-half-even((x - z)/s) clamped to [0, 2^b - 1]
+ * (evaluated in fp64, which is exact for these operands); decode x-hat = z + code*s.
+ * Row bytes: F16 2r; INT4 r/2; MIX8_4 r_out + (r - r_out)/2.
+ *
+ * Keys, head g, sequence b, token t: 16-token block k = t/16, tau = t%16, at
+ *   plane + (b*Cp/16 + k) * 16*row_bytes.  Inside a block the channels go in
+ *   chunks of 8 (chunk c = channels 8c..8c+7); chunk c holds its 16 tokens
+ *   back to back, chunk_bytes each (16 F16, 8 for 8-bit, 4 for 4-bit chunks),
+ *   8-bit chunks first.  Within a chunk: F16 channel w at 2w; 8-bit channel w at
+ *   byte w; 4-bit channel w at byte w/2, low nibble for even w.
+ *   Key meta: per 16-token block, per group, 16 (s, z) fp16 pairs (4 B per token).
+ * Values, sequence b, token t: 32-token block k = t/32 at
+ *   plane + (b*Cp/32 + k) * 32*row_bytes.  A block's tokens form four chunks q of
+ *   eight slots: with u = t%32, q = (u%16)/4 and slot = 4*(u/16) + u%4 (so chunk q
+ *   holds tokens 4q..4q+3 and 16+4q..16+4q+3).  For each chunk q and channel c the
+ *   eight slots are stored together: F16 16 B (slot at 2*slot), 8-bit 8 B (slot at
+ *   byte slot), 4-bit one 32-bit word (slot 2k in bits 4k..4k+3, slot 2k+1 in bits
+ *   16+4k..16+4k+3, k = 0..3).  The
+ *   8-bit region (all q, then all channels) precedes the 4-bit region; within a
+ *   region the order is [q][channel][slots].
+ *   Value meta: per 32-token block, per group g, per chunk q: the 8 slots' s
+ *   (16 B) then their z (16 B), at ((g*4 + q)*32) inside the block's meta.
+ * ---------------------------------------------------------------------------- */
+typedef struct {
+  int64_t total_bytes;
+  int32_t padded_capacity;                       /* Cp */
+  int32_t sum_key_rank;                          /* sum of r_g */
+  int64_t key_code_offset[STARKV_MAX_KV_HEADS];
+  int64_t key_meta_offset[STARKV_MAX_KV_HEADS];
+  int32_t key_row_bytes[STARKV_MAX_KV_HEADS];
+  int32_t key_groups[STARKV_MAX_KV_HEADS];
+  int32_t key_outlier_channels[STARKV_MAX_KV_HEADS];
+  int64_t value_code_offset;
+  int64_t value_meta_offset;
+  int32_t value_row_bytes;
+  int32_t value_groups;
+  int32_t value_outlier_channels;
+} starkv_layout;
+
+/* Validates cfg and builds a plan (host memory owned by the library).
+ * Errors: INVALID_ARG (null, non-positive sizes, ranks not multiples of 16, ...),
+ * UNSUPPORTED (head_dim not 64/128, group_size != 32, too many heads, ...). */
+starkv_status starkv_plan_create(const starkv_config* cfg, starkv_plan** out);
+void          starkv_plan_destroy(starkv_plan* plan);
+
+/* Bytes of device memory the caller allocates for one cache (one layer). */
+size_t        starkv_cache_bytes(const starkv_plan* plan);
+starkv_status starkv_cache_layout(const starkv_plan* plan, starkv_layout* out);
+
+/* Workspace sizes (bytes).  Append: the fp16 latents of the new tokens plus, when
+ * d_model > 0, the down-projection's fp32 partial sums.  Decode: the split
+ * partials, for contexts up to max_ctx. */
+size_t        starkv_append_workspace_bytes(const starkv_plan* plan, int32_t n_new);
+size_t        starkv_decode_workspace_bytes(const starkv_plan* plan, int32_t max_ctx);
+
+/* starkv_append -- write n_new new tokens of every sequence into the cache.
+ * Down-projection (Sec. 3.2) then per-token quantization (Sec. 4.4).
+ *   cache        device, starkv_cache_bytes(plan) bytes, 256-byte aligned.
+ *   x_or_latents device.  d_model > 0: hidden states [B][n_new][d_model] in x_dtype;
+ *                the latents x.A_all are accumulated in fp32 and rounded to fp16
+ *                (left in ws: [B][n_new][sum_r + r_v] fp16 at offset 0).
+ *                d_model == 0: fp16 latents [B][n_new][sum_r + r_v] (key heads in
+ *                order, then the value latent).  2-byte aligned.
+ *   A_all        device bf16 [d_model][sum_r + r_v] (column block per key head, then
+ *                values); NULL when d_model == 0.
+ *   pos_dev      device int32 [B]: row of the first new token of each sequence;
+ *                rows pos[b] .. pos[b]+n_new-1 are written.  Rows outside
+ *                [0, capacity) are not written.  The caller advances its lengths.
+ *   n_new        >= 1.
+ *   ws           device workspace of starkv_append_workspace_bytes(plan, n_new)
+ *                bytes, 256-byte aligned.
+ * Errors: INVALID_ARG, WORKSPACE, ALIGNMENT, HIP. */
+starkv_status starkv_append(const starkv_plan* plan, void* cache, const void* x_or_latents,
+                            const void* A_all, const int32_t* pos_dev, int32_t n_new,
+                            void* ws, size_t ws_bytes, starkv_stream_t stream);
+
+/* starkv_decode_attn -- one decode step of attention for every sequence.
+ *   cache        device, as written by starkv_append.
+ *   q            device [B][H_q][d] in q_dtype, already rotated (RoPE) for the
+ *                current position; 16-byte aligned.
+ *   B_k          device fp16 [sum_r][d]: U_K,g^T of head g at rows
+ *                sum_{g'<g} r_g' .. +r_g (the key up-projection, Sec. 3.2).
+ *   B_v          device fp16 [r_v][H_kv*d]: U_V^T; query head i uses columns
+ *                g*d .. g*d+d-1 of its KV head g.
+ *   ctx_len_dev  device int32 [B]: sequence b attends to rows [0, ctx_len[b]);
+ *                key t is rotated by RoPE at position t.  Values are clamped to
+ *                [0, max_ctx]; 0 gives a zero output.
+ *   max_ctx      host upper bound of ctx_len, 1 <= max_ctx <= capacity.
+ *   out          device [B][H_q][d] in out_dtype, 16-byte aligned.
+ *   ws           device, starkv_decode_workspace_bytes(plan, max_ctx) bytes,
+ *                256-byte aligned.
+ * Errors: INVALID_ARG, CAPACITY (max_ctx > capacity), WORKSPACE, ALIGNMENT, HIP. */
+starkv_status starkv_decode_attn(const starkv_plan* plan, const void* cache, const void* q,
+                                 const void* B_k, const void* B_v, const int32_t* ctx_len_dev,
+                                 int32_t max_ctx, void* out, void* ws, size_t ws_bytes,
+                                 starkv_stream_t stream);
+
+/* The two launches of starkv_decode_attn, exposed separately so that each can be
+ * timed on its own: the split pass (keys, scores, softmax state and value
+ * latents per context split, written to ws) and the combine pass (merge of the
+ * splits and the value up-projection into out).  Same arguments and errors. */
+starkv_status starkv_decode_split(const starkv_plan* plan, const void* cache, const void* q,
+                                  const void* B_k, const int32_t* ctx_len_dev, int32_t max_ctx,
+                                  void* ws, size_t ws_bytes, starkv_stream_t stream);
+starkv_status starkv_decode_combine(const starkv_plan* plan, const void* B_v,
+                                    const int32_t* ctx_len_dev, int32_t max_ctx, void* out,
+                                    void* ws, size_t ws_bytes, starkv_stream_t stream);
+
+/* Number of context splits used for max_ctx (tokens per split =
+ * starkv_decode_split_tokens); informative. */
+int32_t       starkv_decode_splits(const starkv_plan* plan, int32_t max_ctx);
+int32_t       starkv_decode_split_tokens(const starkv_plan* plan, int32_t max_ctx);
+
+const char*   starkv_status_string(starkv_status status);
+const char*   starkv_last_error(void);          /* thread-local, never NULL */
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* STARKV_H */

@@ -217,8 +217,10 @@ static int64_t value_code_at(const orc_cfg* cfg, int b, int t, int c, int* nib) 
   if (cfg->qmode == ORC_Q_F16) return base + ((int64_t)kq * r + c) * 16 + slot * 2;
   int ro = orc_outlier_channels(cfg->qmode, r);
   if (c < ro) return base + ((int64_t)kq * ro + c) * 8 + slot;
-  *nib = slot % 2;
-  return base + 32 * ro + ((int64_t)kq * (r - ro) + (c - ro)) * 4 + slot / 2;
+  /* in a 4-bit chunk word, slot 2k sits in nibble k and slot 2k+1 in nibble k+4 */
+  int p = (slot % 2 == 0) ? slot / 2 : slot / 2 + 4;
+  *nib = p % 2;
+  return base + 32 * ro + ((int64_t)kq * (r - ro) + (c - ro)) * 4 + p / 2;
 }
 
 /* Value meta: per 32-token block, group and chunk, the 8 scales of the chunk's
@@ -278,10 +280,23 @@ static void store_block(const orc_cfg* cfg, uint8_t* cache, int g, int b, int t,
   }
 }
 
-int orc_append(const orc_cfg* cfg, uint8_t* cache, const uint16_t* latents,
-               const int32_t* pos, int n_new) {
+typedef struct {
+  const orc_cfg* cfg;
+  uint8_t* cache;
+  const uint16_t* latents;
+  const int32_t* pos;
+  int n_new, b;
+} append_job;
+
+static void* append_one_sequence(void* arg) {
+  append_job* J = (append_job*)arg;
+  const orc_cfg* cfg = J->cfg;
   int width = sum_key_rank(cfg) + cfg->value_rank;
-  for (int b = 0; b < cfg->batch; ++b) {
+  int b = J->b, n_new = J->n_new;
+  const int32_t* pos = J->pos;
+  const uint16_t* latents = J->latents;
+  uint8_t* cache = J->cache;
+  {
     for (int j = 0; j < n_new; ++j) {
       int t = pos[b] + j;
       if (t < 0 || t >= cfg->capacity) continue;   /* rows outside the cache are dropped */
@@ -294,6 +309,21 @@ int orc_append(const orc_cfg* cfg, uint8_t* cache, const uint16_t* latents,
       store_block(cfg, cache, -1, b, t, x + off);
     }
   }
+  return NULL;
+}
+
+/* Sequences own disjoint cache rows, so they are written by one thread each. */
+int orc_append(const orc_cfg* cfg, uint8_t* cache, const uint16_t* latents,
+               const int32_t* pos, int n_new) {
+  append_job jobs[1024];
+  pthread_t th[1024];
+  int nb = cfg->batch < 1024 ? cfg->batch : 1024;
+  for (int b = 0; b < nb; ++b) {
+    append_job J = {cfg, cache, latents, pos, n_new, b};
+    jobs[b] = J;
+    pthread_create(&th[b], NULL, append_one_sequence, &jobs[b]);
+  }
+  for (int b = 0; b < nb; ++b) pthread_join(th[b], NULL);
   return 0;
 }
 

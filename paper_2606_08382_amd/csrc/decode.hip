@@ -1,0 +1,753 @@
+// Decode attention read from the low-rank, quantized cache (gfx950).
+//
+// decode_split: one workgroup per (context split, sequence, KV-head group).
+//   Four waves each take 32 tokens per step (two 16-token subtiles).  For every
+//   KV head of the group a wave
+//     - dequantizes the key latents of its tokens into MFMA operands (registers),
+//     - rebuilds the keys with v_mfma_f32_16x16x32_f16 against the head's
+//       up-projection block held in LDS as MFMA fragments (Sec. 3.2, 4.3.3),
+//     - rotates them with RoPE at their absolute positions in fp32 (Sec. 3.3),
+//     - scores them against the group's query heads with a second MFMA whose
+//       k-index is the head dimension (Sec. 3.1).
+//   The rows of the score tile are the 16 tokens and the columns are query
+//   heads: each KV head only fills its own columns, so up to 16 query heads
+//   share one tile.  The online softmax keeps one running maximum per query
+//   head for the whole workgroup (maxima exchanged through LDS), so the
+//   probabilities of all waves can be stacked into one matrix and multiplied
+//   with the shared value latent V' as one MFMA GEMM, each wave owning a slice
+//   of V' channels (the reordered value path of Sec. 3.3 and the stacked
+//   p.V' GEMM of App. A.6).  The split's softmax state and value-latent
+//   accumulator go to the workspace.
+// decode_combine: merges the splits (log-sum-exp weights) and applies the value
+//   up-projection U_V once per query head (Sec. 3.3), casting to the output type.
+#include <hip/hip_runtime.h>
+
+#include "starkv_internal.h"
+
+namespace starkv {
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ f4 mfma16(h8 a, h8 b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ h2 as_h2(uint32_t u) { return __builtin_bit_cast(h2, u); }
+__device__ __forceinline__ uint32_t as_u32(h2 h) { return __builtin_bit_cast(uint32_t, h); }
+
+// A pair of 8-bit or 4-bit codes placed in the low mantissa bits of fp16 1024:
+// the fp16 value is 1024 + code exactly.  Subtracting 1024 is exact; the fma
+// with (s, z) rounds once.
+__device__ __forceinline__ uint32_t deq_pair(uint32_t magic_pair, h2 s, h2 z) {
+  h2 c = as_h2(magic_pair) - (h2){(_Float16)1024.0f, (_Float16)1024.0f};
+  return as_u32(__builtin_elementwise_fma(c, s, z));
+}
+
+// 4-bit word: element pairs (nibble k, nibble k+4), k = 0..3.
+__device__ __forceinline__ u4 deq_int4(uint32_t w, h2 s0, h2 z0, h2 s1, h2 z1, h2 s2, h2 z2,
+                                       h2 s3, h2 z3) {
+  u4 r;
+  r.x = deq_pair(((w >> 0) & 0x000F000Fu) | 0x64006400u, s0, z0);
+  r.y = deq_pair(((w >> 4) & 0x000F000Fu) | 0x64006400u, s1, z1);
+  r.z = deq_pair(((w >> 8) & 0x000F000Fu) | 0x64006400u, s2, z2);
+  r.w = deq_pair(((w >> 12) & 0x000F000Fu) | 0x64006400u, s3, z3);
+  return r;
+}
+
+// 8-bit chunk (bytes 0..7): element pairs (byte 2k, byte 2k+1).
+__device__ __forceinline__ uint32_t bytes01(uint32_t d) {
+  return (d & 0xFFu) | ((d & 0xFF00u) << 8) | 0x64006400u;
+}
+__device__ __forceinline__ uint32_t bytes23(uint32_t d) {
+  return ((d >> 16) & 0xFFu) | ((d >> 8) & 0xFF0000u) | 0x64006400u;
+}
+__device__ __forceinline__ u4 deq_int8(u2 d, h2 s0, h2 z0, h2 s1, h2 z1, h2 s2, h2 z2, h2 s3,
+                                       h2 z3) {
+  u4 r;
+  r.x = deq_pair(bytes01(d.x), s0, z0);
+  r.y = deq_pair(bytes23(d.x), s1, z1);
+  r.z = deq_pair(bytes01(d.y), s2, z2);
+  r.w = deq_pair(bytes23(d.y), s3, z3);
+  return r;
+}
+
+__device__ __forceinline__ float wave_max16(float v) {
+  v = fmaxf(v, __shfl_xor(v, 16));
+  v = fmaxf(v, __shfl_xor(v, 32));
+  return v;
+}
+__device__ __forceinline__ float wave_sum16(float v) {
+  v += __shfl_xor(v, 16);
+  v += __shfl_xor(v, 32);
+  return v;
+}
+
+__device__ __forceinline__ float2 cmul(float2 a, float2 b) {
+  return make_float2(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x);
+}
+
+__device__ __forceinline__ _Float16 load_q(const void* q, int64_t idx, int bf16) {
+  uint16_t u = static_cast<const uint16_t*>(q)[idx];
+  if (bf16) {
+    float f = __uint_as_float(static_cast<uint32_t>(u) << 16);
+    return (_Float16)f;
+  }
+  return __builtin_bit_cast(_Float16, u);
+}
+
+// LDS layout of the split kernel (byte offsets); identical on the host.
+struct SplitLds {
+  int frag, qc, red, alpha, loop, raw, vmeta, pbuf, rope, total;
+};
+
+__host__ __device__ inline SplitLds split_lds(int frags, int nql, int head_dim, int ct,
+                                             int raw_bytes, int v_ng) {
+  SplitLds L;
+  L.frag = 0;
+  L.qc = frags * 1024;
+  L.red = L.qc + ((nql * head_dim * 2 + 16 + 15) / 16) * 16;
+  L.alpha = L.red + kWaves * ct * 16 * 4;
+  L.loop = L.alpha + ct * 16 * 4;
+  L.raw = L.loop;
+  L.vmeta = L.raw + kWaves * raw_bytes;
+  L.pbuf = L.vmeta + 4 * v_ng * 128;
+  int loop_end = L.pbuf + kWaves * ct * 1024;
+  L.rope = L.loop;   // RoPE tables (prologue only) alias the loop area
+  int rope_end = L.rope + (64 + 64 + 16 * 64 + 8 * 64) * 8;
+  L.total = loop_end > rope_end ? loop_end : rope_end;
+  return L;
+}
+
+constexpr int kMaxLoads = 8;   // 16-byte key-staging loads per lane per step
+constexpr int kMaxVMeta = 3;   // 16-byte value-meta loads per thread per step
+
+template <int D, int QM, int CT, int NTW>
+__global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams p) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  constexpr int NKBS = D / 32;   // score k-blocks (head dimension / 32)
+  constexpr int NF = 4 * NKBS;   // RoPE frequencies held per lane
+  constexpr int HALF = D / 2;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
+  const int col = lane & 15, quad = lane >> 4;
+  const int split = blockIdx.x, b = blockIdx.y, hg = blockIdx.z;
+  const int g0 = p.hg_first[hg], g1 = p.hg_first[hg + 1];
+  const int G = p.group_q;
+  const int nql = (g1 - g0) * G;
+  const int q0 = g0 * G;
+
+  int L = p.ctx_len[b];
+  L = L < 0 ? 0 : (L > p.max_ctx ? p.max_ctx : L);
+  const int t_begin = split * p.split_len;
+  if (t_begin >= L) return;
+  const int t_end = min(t_begin + p.split_len, L);
+  const int n_steps = (t_end - t_begin + kStepTokens - 1) / kStepTokens;
+
+  const int raw_bytes = p.hg_raw_bytes[hg];
+  const SplitLds LL = split_lds(p.hg_frags[hg], nql, D, CT, raw_bytes, p.v_ng);
+  h8* frag = reinterpret_cast<h8*>(smem + LL.frag);
+  _Float16* qc = reinterpret_cast<_Float16*>(smem + LL.qc);
+  float* red = reinterpret_cast<float*>(smem + LL.red);
+  float* alpha_s = reinterpret_cast<float*>(smem + LL.alpha);
+  uint8_t* raw = smem + LL.raw + w * raw_bytes;
+  uint8_t* vmeta = smem + LL.vmeta;
+  h8* pbuf = reinterpret_cast<h8*>(smem + LL.pbuf);
+  float2* rope_base = reinterpret_cast<float2*>(smem + LL.rope);   // [64]
+  float2* rope_step = rope_base + 64;                               // [64]
+  float2* rope_col = rope_step + 64;                                // [16][64]
+  float2* rope_ws = rope_col + 16 * 64;                             // [8][64]
+
+  // ---------------------------------------------------------------- prologue
+  // Zero the up-projection fragments (rank padding must read as 0).
+  {
+    u4* f = reinterpret_cast<u4*>(smem + LL.frag);
+    const int n = p.hg_frags[hg] * 64;
+    for (int i = tid; i < n; i += kThreads) f[i] = (u4){0, 0, 0, 0};
+  }
+  // RoPE angle tables: rotation by t*omega_j composed as
+  // base(t_begin) * step-of-wave(32w + 16s) * within-subtile(col).
+  {
+    const double l2t = p.log2_theta;
+    for (int i = tid; i < HALF; i += kThreads) {
+      const double om = exp2(-(2.0 * i / D) * l2t);
+      double a = (double)t_begin * om;
+      a -= 6.283185307179586476925286766559 * floor(a * 0.15915494309189533576888376337251);
+      double sa, ca;
+      sincos(a, &sa, &ca);
+      rope_base[i] = make_float2((float)ca, (float)sa);
+      float ss, cs;
+      sincosf((float)(kStepTokens * om), &ss, &cs);
+      rope_step[i] = make_float2(cs, ss);
+    }
+    for (int i = tid; i < 16 * HALF; i += kThreads) {
+      const int c = i / HALF, j = i % HALF;
+      const float om = (float)exp2(-(2.0 * j / D) * l2t);
+      float ss, cs;
+      sincosf((float)c * om, &ss, &cs);
+      rope_col[c * 64 + j] = make_float2(cs, ss);
+    }
+    for (int i = tid; i < 8 * HALF; i += kThreads) {
+      const int k = i / HALF, j = i % HALF;
+      const double om = exp2(-(2.0 * j / D) * l2t);
+      float ss, cs;
+      sincosf((float)(16.0 * k * om), &ss, &cs);
+      rope_ws[k * 64 + j] = make_float2(cs, ss);
+    }
+  }
+  // Query heads of the group, fp16, permuted so that lane (col, quad) of score
+  // k-block kbs reads one 16-byte vector: element 2e = q[j], 2e+1 = q[j + D/2],
+  // j = 16*kbs + 4*quad + e.  A zero vector follows for lanes whose column does
+  // not belong to the KV head being scored.
+  {
+    const int n = nql * D;
+    for (int i = tid; i < n / 2; i += kThreads) {
+      const int il = i / HALF, r = i % HALF;          // r = kbs*16 + quad*4 + e
+      const int kbs = r / 16, qd = (r / 4) % 4, e = r % 4;
+      const int j = 16 * kbs + 4 * qd + e;
+      const int64_t src = ((int64_t)b * p.n_q + q0 + il) * D;
+      _Float16* dst = qc + il * D + (kbs * 4 + qd) * 8 + 2 * e;
+      dst[0] = load_q(p.q, src + j, p.q_bf16);
+      dst[1] = load_q(p.q, src + j + HALF, p.q_bf16);
+    }
+    if (tid < 8) qc[n + tid] = (_Float16)0.0f;
+  }
+  __syncthreads();
+  // Up-projection fragments.  Fragment (head, m-tile mt, k-block kb), lane
+  // (jj, kq): 8 halves = B_k[row][16*mt + jj] for the 8 channels of chunk
+  // 4*kb + kq, ordered as the key operand delivers them (4-bit chunks pair
+  // channels (k, k+4); 8-bit and fp16 chunks are in order).
+  for (int gg = g0; gg < g1; ++gg) {
+    const KHeadInfo& kh = p.kh[gg];
+    const int nvec = kh.rank * (D / 8);
+    for (int i = tid; i < nvec; i += kThreads) {
+      const int row = i / (D / 8), j8 = i % (D / 8);
+      const u4 v = *reinterpret_cast<const u4*>(p.bk + (int64_t)(kh.bk_row + row) * D + 8 * j8);
+      const _Float16* hv = reinterpret_cast<const _Float16*>(&v);
+      const int c = row / 8, wi = row % 8;
+      const int kb = c / 4, kq = c % 4;
+      int e = wi;
+      if (QM != STARKV_Q_F16 && c >= kh.n8) e = (wi < 4) ? 2 * wi : 2 * (wi - 4) + 1;
+      for (int u = 0; u < 8; ++u) {
+        const int j = 8 * j8 + u;
+        const int mt = j / 16, jj = j % 16;
+        _Float16* f = reinterpret_cast<_Float16*>(frag + (kh.frag_base + mt * kh.nkb + kb) * 64 +
+                                                  jj + 16 * kq);
+        f[e] = hv[u];
+      }
+    }
+  }
+  // Per-lane rotations for its two subtiles: angles (t_begin + 32w + 16s + col) * omega_j.
+  float2 cs[2][NF];
+  float2 rot[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int j = 16 * (f / 4) + 4 * quad + (f % 4);
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+      cs[s][f] = cmul(cmul(rope_base[j], rope_ws[(2 * w + s) * 64 + j]), rope_col[col * 64 + j]);
+    rot[f] = rope_step[j];
+  }
+  __syncthreads();   // RoPE tables are dead from here on (the loop area reuses them)
+
+  // ---------------------------------------------------------------- prefetch setup
+  // Key staging: the wave's 32 tokens of every key head of the group, codes then
+  // meta per head, as one contiguous LDS area filled by flat 16-byte loads.
+  const uint8_t* ld_ptr[kMaxLoads];
+  int ld_stride[kMaxLoads];
+  {
+    const int64_t blk16 = (int64_t)b * (p.cap_pad / 16) + (t_begin + 32 * w) / 16;
+#pragma unroll
+    for (int i = 0; i < kMaxLoads; ++i) {
+      const int off = (i * 64 + lane) * 16;
+      ld_ptr[i] = nullptr;
+      ld_stride[i] = 0;
+      if (off < raw_bytes) {
+        for (int gg = g0; gg < g1; ++gg) {
+          const KHeadInfo& kh = p.kh[gg];
+          const int ncode = 32 * kh.row_bytes, nmeta = 2 * kh.ngroups * 64;
+          if (off >= kh.raw_code && off < kh.raw_code + ncode) {
+            ld_ptr[i] = p.cache + kh.code_off + blk16 * 16 * kh.row_bytes + (off - kh.raw_code);
+            ld_stride[i] = (kStepTokens / 16) * 16 * kh.row_bytes;
+          } else if (nmeta > 0 && off >= kh.raw_meta && off < kh.raw_meta + nmeta) {
+            ld_ptr[i] = p.cache + kh.meta_off + blk16 * kh.ngroups * 64 + (off - kh.raw_meta);
+            ld_stride[i] = (kStepTokens / 16) * kh.ngroups * 64;
+          }
+        }
+      }
+    }
+  }
+  u4 kraw[kMaxLoads];
+  auto load_k = [&](int step) {
+#pragma unroll
+    for (int i = 0; i < kMaxLoads; ++i)
+      if (ld_ptr[i]) kraw[i] = *reinterpret_cast<const u4*>(ld_ptr[i] + (int64_t)step * ld_stride[i]);
+  };
+  // Value codes of this wave's channel tiles for the four 32-token blocks of a step.
+  constexpr int VW = (QM == STARKV_Q_F16) ? 4 : ((QM == STARKV_Q_MIX8_4) ? 2 : 1);
+  const int NT = p.rv / 16;
+  const int v_ri = p.rv - p.v_ro;
+  uint32_t vraw[4][NTW][VW];
+  const int64_t vblk0 = (int64_t)b * (p.cap_pad / 32) + t_begin / 32;
+  auto load_v = [&](int step) {
+#pragma unroll
+    for (int ww = 0; ww < 4; ++ww) {
+      const uint8_t* blk = p.cache + p.v_code_off +
+                           (vblk0 + (int64_t)step * 4 + ww) * 32 * p.v_row_bytes;
+#pragma unroll
+      for (int t = 0; t < NTW; ++t) {
+        const int nt = w * NTW + t;
+        if (nt < NT) {
+          const int rho = 16 * nt + col;
+          if (QM == STARKV_Q_F16) {
+            const u4 v = *reinterpret_cast<const u4*>(blk + ((int64_t)quad * p.rv + rho) * 16);
+            vraw[ww][t][0] = v.x; vraw[ww][t][1 % VW] = v.y;
+            vraw[ww][t][2 % VW] = v.z; vraw[ww][t][3 % VW] = v.w;
+          } else if (rho < p.v_ro) {
+            const u2 v = *reinterpret_cast<const u2*>(blk + ((int64_t)quad * p.v_ro + rho) * 8);
+            vraw[ww][t][0] = v.x; vraw[ww][t][(VW - 1) & 1] = v.y;
+          } else {
+            vraw[ww][t][0] = *reinterpret_cast<const uint32_t*>(
+                blk + 32 * p.v_ro + ((int64_t)quad * v_ri + (rho - p.v_ro)) * 4);
+          }
+        }
+      }
+    }
+  };
+  u4 vm[kMaxVMeta];
+  const int vmeta_bytes = 4 * p.v_ng * 128;
+  auto load_vm = [&](int step) {
+    const uint8_t* src = p.cache + p.v_meta_off + (vblk0 + (int64_t)step * 4) * p.v_ng * 128;
+#pragma unroll
+    for (int i = 0; i < kMaxVMeta; ++i) {
+      const int off = (i * kThreads + tid) * 16;
+      if (off < vmeta_bytes) vm[i] = *reinterpret_cast<const u4*>(src + off);
+    }
+  };
+
+  // ---------------------------------------------------------------- main loop
+  float m_run[CT], l_part[CT];
+  f4 acc_v[CT][NTW];
+#pragma unroll
+  for (int c = 0; c < CT; ++c) {
+    m_run[c] = -INFINITY;
+    l_part[c] = 0.0f;
+#pragma unroll
+    for (int t = 0; t < NTW; ++t) acc_v[c][t] = (f4){0, 0, 0, 0};
+  }
+  const float sc = p.score_scale;
+
+  load_k(0);
+  load_v(0);
+  if (QM != STARKV_Q_F16) load_vm(0);
+
+  for (int step = 0; step < n_steps; ++step) {
+    const int t_step = t_begin + step * kStepTokens;
+    const int tw = t_step + 32 * w;
+    // stage this step's key bytes, then prefetch the next step's
+#pragma unroll
+    for (int i = 0; i < kMaxLoads; ++i)
+      if (ld_ptr[i]) *reinterpret_cast<u4*>(raw + (i * 64 + lane) * 16) = kraw[i];
+    if (step + 1 < n_steps) load_k(step + 1);
+    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): staging visible to this wave
+
+    // ------------------------------------------ keys: reconstruct, rotate, score
+    f4 acc_s[2][CT];
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int c = 0; c < CT; ++c) acc_s[s][c] = (f4){0, 0, 0, 0};
+
+    for (int gg = g0; gg < g1; ++gg) {
+      const KHeadInfo& kh = p.kh[gg];
+      const int gl = gg - g0;
+      // key operand: lane (tau = col, kq = quad) holds chunk 4*kb + quad of token
+      // tw + 16*s + col
+      h8 xop[2][NKBS];
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+#pragma unroll
+        for (int kb = 0; kb < NKBS; ++kb) {
+          u4 v = (u4){0, 0, 0, 0};
+          const int c = 4 * kb + quad;
+          if (kb < kh.nkb && 8 * c < kh.rank) {
+            const uint8_t* cb = raw + kh.raw_code + s * 16 * kh.row_bytes;
+            if (QM == STARKV_Q_F16) {
+              v = *reinterpret_cast<const u4*>(cb + c * 256 + col * 16);
+            } else {
+              int gi;
+              if (c < kh.n8) gi = (8 * c) / 32;
+              else gi = kh.ng8 + (8 * (c - kh.n8)) / 32;
+              const uint32_t mz = *reinterpret_cast<const uint32_t*>(
+                  raw + kh.raw_meta + (s * kh.ngroups + gi) * 64 + col * 4);
+              const h2 sv = as_h2((mz & 0xFFFFu) * 0x10001u);
+              const h2 zv = as_h2((mz >> 16) * 0x10001u);
+              if (c < kh.n8) {
+                const u2 d = *reinterpret_cast<const u2*>(cb + c * 128 + col * 8);
+                v = deq_int8(d, sv, zv, sv, zv, sv, zv, sv, zv);
+              } else {
+                const uint32_t d = *reinterpret_cast<const uint32_t*>(
+                    cb + kh.n8 * 128 + (c - kh.n8) * 64 + col * 4);
+                v = deq_int4(d, sv, zv, sv, zv, sv, zv, sv, zv);
+              }
+            }
+          }
+          xop[s][kb] = __builtin_bit_cast(h8, v);
+        }
+      }
+      // score tile and column range of this KV head's query heads
+      const int ct_g = (gl * G) / 16;
+      const int c_lo = (gl * G) % 16;
+      const bool mine = col >= c_lo && col < c_lo + G;
+      const int il = ct_g * 16 + col;   // local query head of this lane's column
+#pragma unroll
+      for (int kbs = 0; kbs < NKBS; ++kbs) {
+        f4 k_lo[2], k_hi[2];
+#pragma unroll
+        for (int s = 0; s < 2; ++s) { k_lo[s] = (f4){0, 0, 0, 0}; k_hi[s] = (f4){0, 0, 0, 0}; }
+#pragma unroll
+        for (int kb = 0; kb < NKBS; ++kb) {
+          if (kb < kh.nkb) {
+            const h8 a_lo = frag[(kh.frag_base + kbs * kh.nkb + kb) * 64 + lane];
+            const h8 a_hi = frag[(kh.frag_base + (kbs + NKBS) * kh.nkb + kb) * 64 + lane];
+#pragma unroll
+            for (int s = 0; s < 2; ++s) {
+              k_lo[s] = mfma16(a_lo, xop[s][kb], k_lo[s]);
+              k_hi[s] = mfma16(a_hi, xop[s][kb], k_hi[s]);
+            }
+          }
+        }
+        // lane (tau = col, quad) holds k[j] and k[j + D/2] for j = 16*kbs + 4*quad + e
+        const h8 qf = *reinterpret_cast<const h8*>(
+            qc + (mine ? (il * D + (kbs * 4 + quad) * 8) : nql * D));
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+          u4 kr;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float2 r = cs[s][4 * kbs + e];
+            const float a = k_lo[s][e], bb = k_hi[s][e];
+            const float ra = a * r.x - bb * r.y;
+            const float rb = bb * r.x + a * r.y;
+            kr[e] = as_u32((h2){(_Float16)ra, (_Float16)rb});
+          }
+          const h8 kop = __builtin_bit_cast(h8, kr);
+#pragma unroll
+          for (int c = 0; c < CT; ++c)
+            if (c == ct_g) acc_s[s][c] = mfma16(kop, qf, acc_s[s][c]);
+        }
+      }
+    }
+    // advance the rotations by one step
+#pragma unroll
+    for (int f = 0; f < NF; ++f) {
+      cs[0][f] = cmul(cs[0][f], rot[f]);
+      cs[1][f] = cmul(cs[1][f], rot[f]);
+    }
+
+    // ------------------------------------------ online softmax (log2 domain)
+    float x[CT][2][4];
+    float mx[CT];
+#pragma unroll
+    for (int c = 0; c < CT; ++c) {
+      mx[c] = -INFINITY;
+#pragma unroll
+      for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int t = tw + 16 * s + 4 * quad + e;
+          const float v = (t < t_end) ? acc_s[s][c][e] * sc : -INFINITY;
+          x[c][s][e] = v;
+          mx[c] = fmaxf(mx[c], v);
+        }
+      mx[c] = wave_max16(mx[c]);
+      if (quad == 0) red[(w * CT + c) * 16 + col] = mx[c];
+    }
+    __syncthreads();   // (1) tile maxima visible; previous step's value phase done
+    if (QM != STARKV_Q_F16) {
+#pragma unroll
+      for (int i = 0; i < kMaxVMeta; ++i) {
+        const int off = (i * kThreads + tid) * 16;
+        if (off < vmeta_bytes) *reinterpret_cast<u4*>(vmeta + off) = vm[i];
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < CT; ++c) {
+      float mn = m_run[c];
+#pragma unroll
+      for (int ww = 0; ww < kWaves; ++ww) mn = fmaxf(mn, red[(ww * CT + c) * 16 + col]);
+      const float al = exp2f(m_run[c] - mn);   // m_run = -inf on the first step: 0
+      m_run[c] = mn;
+      u4 pk;
+      float ls = 0.0f;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const _Float16 p0 = (_Float16)exp2f(x[c][k / 2][2 * (k % 2)] - mn);
+        const _Float16 p1 = (_Float16)exp2f(x[c][k / 2][2 * (k % 2) + 1] - mn);
+        ls += (float)p0 + (float)p1;
+        pk[k] = as_u32((h2){p0, p1});
+      }
+      l_part[c] = l_part[c] * al + ls;
+      pbuf[(w * CT + c) * 64 + lane] = __builtin_bit_cast(h8, pk);
+      if (w == 0 && quad == 0) alpha_s[c * 16 + col] = al;
+    }
+    __syncthreads();   // (2) probabilities, rescale factors and value meta visible
+
+    // ------------------------------------------ values: acc += P . V'
+#pragma unroll
+    for (int c = 0; c < CT; ++c) {
+      const f4 al = *reinterpret_cast<const f4*>(alpha_s + c * 16 + 4 * quad);
+#pragma unroll
+      for (int t = 0; t < NTW; ++t) acc_v[c][t] *= al;
+    }
+    const bool full = (t_step + kStepTokens <= t_end);
+#pragma unroll
+    for (int ww = 0; ww < 4; ++ww) {
+      h8 pa[CT];
+#pragma unroll
+      for (int c = 0; c < CT; ++c) pa[c] = pbuf[(ww * CT + c) * 64 + lane];
+      // slots 2k, 2k+1 of this lane's chunk: tokens
+      //   k < 2: 4*quad + 2k + {0,1};  k >= 2: 16 + 4*quad + 2(k-2) + {0,1}
+      u4 vmask = (u4){0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
+      if (!full) {
+        const int tb = t_step + 32 * ww;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int t0 = tb + (k < 2 ? 4 * quad + 2 * k : 16 + 4 * quad + 2 * (k - 2));
+          vmask[k] = (t0 < t_end ? 0x0000FFFFu : 0u) | (t0 + 1 < t_end ? 0xFFFF0000u : 0u);
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < NTW; ++t) {
+        const int nt = w * NTW + t;
+        if (nt < NT) {
+          const int rho = 16 * nt + col;
+          u4 v;
+          if (QM == STARKV_Q_F16) {
+            v = (u4){vraw[ww][t][0], vraw[ww][t][1 % VW], vraw[ww][t][2 % VW],
+                     vraw[ww][t][3 % VW]};
+          } else {
+            const int gi = rho < p.v_ro ? rho / 32 : p.v_ng8 + (rho - p.v_ro) / 32;
+            const uint8_t* mb = vmeta + ((ww * p.v_ng + gi) * 4 + quad) * 32;
+            const u4 sv = *reinterpret_cast<const u4*>(mb);
+            const u4 zv = *reinterpret_cast<const u4*>(mb + 16);
+            if (rho < p.v_ro) {
+              v = deq_int8((u2){vraw[ww][t][0], vraw[ww][t][(VW - 1) & 1]}, as_h2(sv.x),
+                           as_h2(zv.x), as_h2(sv.y), as_h2(zv.y), as_h2(sv.z), as_h2(zv.z),
+                           as_h2(sv.w), as_h2(zv.w));
+            } else {
+              v = deq_int4(vraw[ww][t][0], as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y),
+                           as_h2(sv.z), as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
+            }
+          }
+          v &= vmask;
+          const h8 vop = __builtin_bit_cast(h8, v);
+#pragma unroll
+          for (int c = 0; c < CT; ++c) acc_v[c][t] = mfma16(pa[c], vop, acc_v[c][t]);
+        }
+      }
+    }
+    if (step + 1 < n_steps) {
+      load_v(step + 1);
+      if (QM != STARKV_Q_F16) load_vm(step + 1);
+    }
+  }
+
+  // ---------------------------------------------------------------- partials
+#pragma unroll
+  for (int c = 0; c < CT; ++c) {
+    const float l = wave_sum16(l_part[c]);
+    if (quad == 0) red[(w * CT + c) * 16 + col] = l;
+  }
+  __syncthreads();
+  const int64_t pbase = ((int64_t)b * p.n_split + split) * p.n_q;
+  if (w == 0 && quad == 0) {
+#pragma unroll
+    for (int c = 0; c < CT; ++c) {
+      const int il = c * 16 + col;
+      if (il < nql) {
+        float lt = 0.0f;
+#pragma unroll
+        for (int ww = 0; ww < kWaves; ++ww) lt += red[(ww * CT + c) * 16 + col];
+        float* dst = p.part + (pbase + q0 + il) * p.part_stride + p.rv;
+        dst[0] = m_run[c];
+        dst[1] = lt;
+      }
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < CT; ++c)
+#pragma unroll
+    for (int t = 0; t < NTW; ++t) {
+      const int nt = w * NTW + t;
+      if (nt < NT) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int il = c * 16 + 4 * quad + e;
+          if (il < nql) p.part[(pbase + q0 + il) * p.part_stride + 16 * nt + col] = acc_v[c][t][e];
+        }
+      }
+    }
+}
+
+// ---------------------------------------------------------------------- combine
+#ifdef SK_COMMON
+__global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
+  extern __shared__ __align__(16) float sm[];
+  float* a = sm;                 // [rv]
+  float* wts = sm + p.rv;        // [n_split]
+  float* red = wts + p.n_split;  // [256]
+  const int i = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  const int D = p.head_dim;
+  const int g = (int)(((int64_t)i * p.n_kv) / p.n_q);
+  int L = p.ctx_len[b];
+  L = L < 0 ? 0 : (L > p.max_ctx ? p.max_ctx : L);
+  uint16_t* out = static_cast<uint16_t*>(p.out) + ((int64_t)b * p.n_q + i) * D;
+  if (L == 0) {
+    for (int j = tid; j < D; j += 256) out[j] = 0;
+    return;
+  }
+  const int ns = (L + p.split_len - 1) / p.split_len;
+  const float* part = p.part + ((int64_t)b * p.n_split * p.n_q + i) * p.part_stride;
+  const int64_t sstride = (int64_t)p.n_q * p.part_stride;
+  // global maximum of the split maxima
+  float m = -INFINITY;
+  for (int s = tid; s < ns; s += 256) m = fmaxf(m, part[s * sstride + p.rv]);
+  red[tid] = m;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (tid < o) red[tid] = fmaxf(red[tid], red[tid + o]);
+    __syncthreads();
+  }
+  const float M = red[0];
+  __syncthreads();
+  float lsum = 0.0f;
+  for (int s = tid; s < ns; s += 256) {
+    const float wv = exp2f(part[s * sstride + p.rv] - M);
+    wts[s] = wv;
+    lsum += wv * part[s * sstride + p.rv + 1];
+  }
+  red[tid] = lsum;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (tid < o) red[tid] += red[tid + o];
+    __syncthreads();
+  }
+  const float inv_l = 1.0f / red[0];
+  for (int r = tid; r < p.rv; r += 256) {
+    float acc = 0.0f;
+    for (int s = 0; s < ns; ++s) acc += wts[s] * part[s * sstride + r];
+    a[r] = acc * inv_l;
+  }
+  __syncthreads();
+  // o = a . U_V^T restricted to KV head g's d columns (Sec. 3.3 reordering)
+  const int nq4 = 256 / D;   // threads per output element
+  const int j = tid % D, part_id = tid / D;
+  float acc = 0.0f;
+  for (int r = part_id; r < p.rv; r += nq4)
+    acc += a[r] * (float)__builtin_bit_cast(_Float16, p.bv[(int64_t)r * p.n_kv * D + g * D + j]);
+  __syncthreads();
+  red[tid] = acc;
+  __syncthreads();
+  if (tid < D) {
+    float o = 0.0f;
+    for (int k = 0; k < nq4; ++k) o += red[k * D + tid];
+    uint16_t bits;
+    if (p.out_bf16) {
+      const uint32_t u = __float_as_uint(o);
+      bits = (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+      if ((u & 0x7F800000u) == 0x7F800000u) bits = (uint16_t)(u >> 16) | ((u & 0xFFFFu) ? 0x40 : 0);
+    } else {
+      bits = __builtin_bit_cast(uint16_t, (_Float16)o);
+    }
+    out[tid] = bits;
+  }
+}
+#endif  // SK_COMMON
+
+// ---------------------------------------------------------------------- launchers
+// The file is compiled once per (head_dim, cache precision) with SK_D and SK_QM
+// set, producing the split-kernel instances for that pair, and once with
+// SK_COMMON for the combine kernel and the dispatcher.
+#if defined(SK_D) && defined(SK_QM)
+template <int D, int QM, int CT, int NTW>
+static int launch_split_t(const DecodeParams& p, size_t lds, hipStream_t st) {
+  auto k = decode_split_kernel<D, QM, CT, NTW>;
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return (int)e;
+    attr = true;
+  }
+  dim3 grid(p.n_split, p.batch, p.n_hg);
+  hipLaunchKernelGGL(k, grid, dim3(kThreads), lds, st, p);
+  return (int)hipGetLastError();
+}
+
+template <int D, int QM, int CT>
+static int dispatch_ntw(const DecodeParams& p, int ntw, size_t lds, hipStream_t st) {
+  switch (ntw) {
+    case 1: return launch_split_t<D, QM, CT, 1>(p, lds, st);
+    case 2: return launch_split_t<D, QM, CT, 2>(p, lds, st);
+    case 4: return launch_split_t<D, QM, CT, 4>(p, lds, st);
+    case 8:
+      if (CT <= 2) return launch_split_t<D, QM, CT, 8>(p, lds, st);
+      break;
+  }
+  return (int)hipErrorInvalidValue;
+}
+
+#define SK_CAT2(a, b, c) launch_split_d##a##_q##b
+#define SK_NAME(a, b) SK_CAT2(a, b, _)
+int SK_NAME(SK_D, SK_QM)(const DecodeParams& p, int ct, int ntw, size_t lds, hipStream_t st) {
+  switch (ct) {
+    case 1: return dispatch_ntw<SK_D, SK_QM, 1>(p, ntw, lds, st);
+    case 2: return dispatch_ntw<SK_D, SK_QM, 2>(p, ntw, lds, st);
+    case 4: return dispatch_ntw<SK_D, SK_QM, 4>(p, ntw, lds, st);
+  }
+  return (int)hipErrorInvalidValue;
+}
+#endif
+
+#ifdef SK_COMMON
+#define SK_DECL(a, b) \
+  int launch_split_d##a##_q##b(const DecodeParams& p, int ct, int ntw, size_t lds, hipStream_t st);
+SK_DECL(64, 0) SK_DECL(64, 1) SK_DECL(64, 2) SK_DECL(128, 0) SK_DECL(128, 1) SK_DECL(128, 2)
+
+int split_lds_bytes(int frags, int nql, int head_dim, int ct, int raw_bytes, int v_ng) {
+  return split_lds(frags, nql, head_dim, ct, raw_bytes, v_ng).total;
+}
+
+int launch_decode_split_ntw(const DecodeParams& p, int head_dim, int qmode, int ct, int ntw,
+                            size_t lds, void* stream) {
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (head_dim == 128) {
+    switch (qmode) {
+      case STARKV_Q_F16: return launch_split_d128_q0(p, ct, ntw, lds, st);
+      case STARKV_Q_INT4: return launch_split_d128_q1(p, ct, ntw, lds, st);
+      case STARKV_Q_MIX8_4: return launch_split_d128_q2(p, ct, ntw, lds, st);
+    }
+  } else if (head_dim == 64) {
+    switch (qmode) {
+      case STARKV_Q_F16: return launch_split_d64_q0(p, ct, ntw, lds, st);
+      case STARKV_Q_INT4: return launch_split_d64_q1(p, ct, ntw, lds, st);
+      case STARKV_Q_MIX8_4: return launch_split_d64_q2(p, ct, ntw, lds, st);
+    }
+  }
+  return (int)hipErrorInvalidValue;
+}
+
+int launch_decode_combine(const CombineParams& p, void* stream) {
+  const size_t lds = (size_t)(p.rv + p.n_split + 256) * sizeof(float);
+  dim3 grid(p.n_q, p.batch);
+  hipLaunchKernelGGL(decode_combine_kernel, grid, dim3(256), lds,
+                     static_cast<hipStream_t>(stream), p);
+  return (int)hipGetLastError();
+}
+#endif
+
+}  // namespace starkv

@@ -1,0 +1,493 @@
+// Host side of the C ABI: plan creation and validation, cache layout, workspace
+// sizing and kernel launches.  No device allocation, no synchronization.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "starkv.h"
+#include "starkv_internal.h"
+
+using namespace starkv;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+starkv_status fail(starkv_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+starkv_status fail(starkv_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+int64_t align256(int64_t x) { return (x + 255) / 256 * 256; }
+
+int outlier_channels(int qmode, int r) { return qmode == STARKV_Q_MIX8_4 ? 8 * ((r + 31) / 32) : 0; }
+
+int n_groups(int qmode, int r) {
+  if (qmode == STARKV_Q_F16) return 0;
+  const int ro = outlier_channels(qmode, r);
+  return (ro + 31) / 32 + (r - ro + 31) / 32;
+}
+
+int row_bytes(int qmode, int r) {
+  if (qmode == STARKV_Q_F16) return 2 * r;
+  const int ro = outlier_channels(qmode, r);
+  return ro + (r - ro) / 2;
+}
+
+constexpr int kLdsLimit = 160 * 1024;
+
+}  // namespace
+
+struct starkv_plan {
+  starkv_config cfg;
+  int32_t key_rank[STARKV_MAX_KV_HEADS];
+  starkv_layout layout;
+  int32_t width;          // sum_r + r_v
+  // decode kernel shape
+  int32_t ct, ntw, n_hg;
+  int32_t hg_first[STARKV_MAX_KV_HEADS + 1];
+  int32_t hg_frags[STARKV_MAX_KV_HEADS];
+  int32_t hg_raw[STARKV_MAX_KV_HEADS];
+  KHeadInfo kh[STARKV_MAX_KV_HEADS];
+  int32_t lds_bytes;
+};
+
+extern "C" {
+
+const char* starkv_status_string(starkv_status s) {
+  switch (s) {
+    case STARKV_OK: return "ok";
+    case STARKV_ERR_INVALID_ARG: return "invalid argument";
+    case STARKV_ERR_UNSUPPORTED: return "unsupported configuration";
+    case STARKV_ERR_CAPACITY: return "length beyond cache capacity";
+    case STARKV_ERR_WORKSPACE: return "workspace missing or too small";
+    case STARKV_ERR_ALIGNMENT: return "misaligned pointer";
+    case STARKV_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* starkv_last_error(void) { return g_last_error.c_str(); }
+
+starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
+  if (!out) return fail(STARKV_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (!c) return fail(STARKV_ERR_INVALID_ARG, "config is NULL");
+  if (c->batch < 1) return fail(STARKV_ERR_INVALID_ARG, "batch %d < 1", c->batch);
+  if (c->n_kv_heads < 1 || c->n_q_heads < 1)
+    return fail(STARKV_ERR_INVALID_ARG, "head counts must be positive");
+  if (c->n_q_heads % c->n_kv_heads)
+    return fail(STARKV_ERR_INVALID_ARG, "n_q_heads %d not a multiple of n_kv_heads %d",
+                c->n_q_heads, c->n_kv_heads);
+  if (c->head_dim < 2 || c->head_dim % 2) return fail(STARKV_ERR_INVALID_ARG, "head_dim must be even");
+  if (c->capacity < 1) return fail(STARKV_ERR_INVALID_ARG, "capacity %d < 1", c->capacity);
+  if (!c->key_rank) return fail(STARKV_ERR_INVALID_ARG, "key_rank is NULL");
+  if (c->qmode < STARKV_Q_F16 || c->qmode > STARKV_Q_MIX8_4)
+    return fail(STARKV_ERR_INVALID_ARG, "qmode %d", c->qmode);
+  if (!(c->rope_theta > 1.0) || !std::isfinite(c->rope_theta))
+    return fail(STARKV_ERR_INVALID_ARG, "rope_theta must be finite and > 1");
+  if (c->d_model < 0) return fail(STARKV_ERR_INVALID_ARG, "d_model < 0");
+  for (int dt : {c->q_dtype, c->out_dtype, c->x_dtype})
+    if (dt != STARKV_DT_F16 && dt != STARKV_DT_BF16) return fail(STARKV_ERR_INVALID_ARG, "dtype %d", dt);
+  if (c->n_kv_heads > STARKV_MAX_KV_HEADS)
+    return fail(STARKV_ERR_UNSUPPORTED, "n_kv_heads %d > %d", c->n_kv_heads, STARKV_MAX_KV_HEADS);
+  if (c->n_q_heads > STARKV_MAX_Q_HEADS)
+    return fail(STARKV_ERR_UNSUPPORTED, "n_q_heads %d > %d", c->n_q_heads, STARKV_MAX_Q_HEADS);
+  const int G = c->n_q_heads / c->n_kv_heads;
+  if (G > 16 || 16 % G) return fail(STARKV_ERR_UNSUPPORTED, "query heads per KV head %d not in {1,2,4,8,16}", G);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(STARKV_ERR_UNSUPPORTED, "head_dim %d not 64 or 128", c->head_dim);
+  if (c->group_size != 32) return fail(STARKV_ERR_UNSUPPORTED, "group_size %d != 32", c->group_size);
+  if (c->capacity > (1 << 24)) return fail(STARKV_ERR_UNSUPPORTED, "capacity %d > 2^24", c->capacity);
+  const int D = c->head_dim;
+  int sum_r = 0;
+  for (int g = 0; g < c->n_kv_heads; ++g) {
+    const int r = c->key_rank[g];
+    if (r < 16 || r > D || r % 16)
+      return fail(STARKV_ERR_INVALID_ARG, "key_rank[%d] = %d: need a multiple of 16 in [16, %d]", g, r, D);
+    sum_r += r;
+  }
+  const int rv = c->value_rank;
+  if (rv < 16 || rv % 16 || rv > c->n_kv_heads * D)
+    return fail(STARKV_ERR_INVALID_ARG, "value_rank %d: need a multiple of 16 in [16, %d]", rv,
+                c->n_kv_heads * D);
+  if (rv > 1024) return fail(STARKV_ERR_UNSUPPORTED, "value_rank %d > 1024", rv);
+  if (n_groups(c->qmode, rv) > 24) return fail(STARKV_ERR_UNSUPPORTED, "value_rank %d: too many groups", rv);
+  if (c->d_model > 0) {
+    if (c->x_dtype != STARKV_DT_BF16) return fail(STARKV_ERR_UNSUPPORTED, "hidden states must be bf16");
+    if (c->d_model % 8) return fail(STARKV_ERR_UNSUPPORTED, "d_model %d not a multiple of 8", c->d_model);
+  }
+
+  starkv_plan* P = new (std::nothrow) starkv_plan();
+  if (!P) return fail(STARKV_ERR_INVALID_ARG, "out of host memory");
+  P->cfg = *c;
+  for (int g = 0; g < c->n_kv_heads; ++g) P->key_rank[g] = c->key_rank[g];
+  P->cfg.key_rank = P->key_rank;
+  P->width = sum_r + rv;
+
+  // ---- layout
+  starkv_layout& L = P->layout;
+  std::memset(&L, 0, sizeof(L));
+  const int64_t Cp = ((int64_t)c->capacity + 255) / 256 * 256;
+  const int64_t rows = (int64_t)c->batch * Cp;
+  L.padded_capacity = (int32_t)Cp;
+  L.sum_key_rank = sum_r;
+  int64_t off = 0;
+  for (int g = 0; g < c->n_kv_heads; ++g) {
+    const int r = c->key_rank[g];
+    L.key_row_bytes[g] = row_bytes(c->qmode, r);
+    L.key_groups[g] = n_groups(c->qmode, r);
+    L.key_outlier_channels[g] = outlier_channels(c->qmode, r);
+    L.key_code_offset[g] = off;
+    off = align256(off + rows * L.key_row_bytes[g]);
+    L.key_meta_offset[g] = off;
+    off = align256(off + rows * 4 * L.key_groups[g]);
+  }
+  L.value_row_bytes = row_bytes(c->qmode, rv);
+  L.value_groups = n_groups(c->qmode, rv);
+  L.value_outlier_channels = outlier_channels(c->qmode, rv);
+  L.value_code_offset = off;
+  off = align256(off + rows * L.value_row_bytes);
+  L.value_meta_offset = off;
+  off = align256(off + rows * 4 * L.value_groups);
+  L.total_bytes = off;
+
+  // ---- decode kernel shape: head groups whose up-projection fragments and
+  // key staging fit the workgroup's LDS
+  const int NT = rv / 16;
+  int ntw = (NT + kWaves - 1) / kWaves;
+  ntw = ntw <= 1 ? 1 : ntw <= 2 ? 2 : ntw <= 4 ? 4 : 8;
+  P->ntw = ntw;
+  int bk_row = 0;
+  for (int g = 0; g < c->n_kv_heads; ++g) {
+    KHeadInfo& k = P->kh[g];
+    k.code_off = L.key_code_offset[g];
+    k.meta_off = L.key_meta_offset[g];
+    k.rank = c->key_rank[g];
+    k.nkb = (k.rank + 31) / 32;
+    k.n8 = L.key_outlier_channels[g] / 8;
+    k.ng8 = (L.key_outlier_channels[g] + 31) / 32;
+    k.ngroups = L.key_groups[g];
+    k.row_bytes = L.key_row_bytes[g];
+    k.bk_row = bk_row;
+    bk_row += k.rank;
+  }
+  auto group_fits = [&](int g_first, int g_last, int ct, int* frags_out, int* raw_out) {
+    int frags = 0, raw = 0;
+    for (int g = g_first; g < g_last; ++g) {
+      frags += (D / 16) * P->kh[g].nkb;
+      raw += 32 * P->kh[g].row_bytes + 2 * P->kh[g].ngroups * 64;
+    }
+    *frags_out = frags;
+    *raw_out = raw;
+    const int nql = (g_last - g_first) * G;
+    if (nql > 16 * ct) return false;
+    if (raw > 8 * 64 * 16) return false;   // kMaxLoads 16-byte loads per lane
+    return split_lds_bytes(frags, nql, D, ct, raw, L.value_groups) <= kLdsLimit;
+  };
+  int best_ct = -1;
+  for (int ct : {1, 2, 4}) {
+    if (ct == 4 && ntw > 4) break;
+    // greedy contiguous grouping at this tile count
+    int n_hg = 0, g = 0;
+    bool ok = true;
+    int first[STARKV_MAX_KV_HEADS + 1];
+    while (g < c->n_kv_heads) {
+      int e = g + 1, fr, rw;
+      if (!group_fits(g, e, ct, &fr, &rw)) { ok = false; break; }
+      while (e < c->n_kv_heads && group_fits(g, e + 1, ct, &fr, &rw)) ++e;
+      first[n_hg++] = g;
+      g = e;
+    }
+    if (!ok) continue;
+    first[n_hg] = c->n_kv_heads;
+    if (best_ct < 0 || n_hg < P->n_hg) {
+      best_ct = ct;
+      P->n_hg = n_hg;
+      std::memcpy(P->hg_first, first, sizeof(int) * (n_hg + 1));
+    }
+    if (n_hg == 1) break;
+  }
+  if (best_ct < 0) {
+    delete P;
+    return fail(STARKV_ERR_UNSUPPORTED, "no workgroup shape fits the ranks in LDS");
+  }
+  P->ct = best_ct;
+  P->lds_bytes = 0;
+  for (int h = 0; h < P->n_hg; ++h) {
+    int fr, rw;
+    group_fits(P->hg_first[h], P->hg_first[h + 1], P->ct, &fr, &rw);
+    P->hg_frags[h] = fr;
+    P->hg_raw[h] = rw;
+    int fb = 0, ro = 0;
+    for (int g = P->hg_first[h]; g < P->hg_first[h + 1]; ++g) {
+      KHeadInfo& k = P->kh[g];
+      k.frag_base = fb;
+      fb += (D / 16) * k.nkb;
+      k.raw_code = ro;
+      ro += 32 * k.row_bytes;
+      k.raw_meta = ro;
+      ro += 2 * k.ngroups * 64;
+    }
+    const int nql = (P->hg_first[h + 1] - P->hg_first[h]) * G;
+    const int lds = split_lds_bytes(fr, nql, D, P->ct, rw, L.value_groups);
+    if (lds > P->lds_bytes) P->lds_bytes = lds;
+  }
+  *out = P;
+  g_last_error.clear();
+  return STARKV_OK;
+}
+
+void starkv_plan_destroy(starkv_plan* plan) { delete plan; }
+
+size_t starkv_cache_bytes(const starkv_plan* plan) {
+  return plan ? (size_t)plan->layout.total_bytes : 0;
+}
+
+starkv_status starkv_cache_layout(const starkv_plan* plan, starkv_layout* out) {
+  if (!plan || !out) return fail(STARKV_ERR_INVALID_ARG, "NULL argument");
+  *out = plan->layout;
+  return STARKV_OK;
+}
+
+// ---------------------------------------------------------------- decode sizing
+
+int32_t starkv_decode_split_tokens(const starkv_plan* P, int32_t max_ctx) {
+  if (!P || max_ctx < 1) return 0;
+  // enough splits to give every compute unit a workgroup
+  const int64_t wgs_per_split = (int64_t)P->cfg.batch * P->n_hg;
+  int64_t splits = (256 + wgs_per_split - 1) / wgs_per_split;
+  int64_t len = ((int64_t)max_ctx + splits - 1) / splits;
+  len = (len + kStepTokens - 1) / kStepTokens * kStepTokens;
+  if (len < kStepTokens) len = kStepTokens;
+  if (len > 8192) len = 8192;
+  return (int32_t)len;
+}
+
+int32_t starkv_decode_splits(const starkv_plan* P, int32_t max_ctx) {
+  const int32_t len = starkv_decode_split_tokens(P, max_ctx);
+  if (len <= 0) return 0;
+  return (max_ctx + len - 1) / len;
+}
+
+static int part_stride(const starkv_plan* P) { return P->cfg.value_rank + 4; }
+
+size_t starkv_decode_workspace_bytes(const starkv_plan* P, int32_t max_ctx) {
+  if (!P || max_ctx < 1) return 0;
+  const int64_t ns = starkv_decode_splits(P, max_ctx);
+  return (size_t)align256((int64_t)P->cfg.batch * ns * P->cfg.n_q_heads * part_stride(P) * 4);
+}
+
+static starkv_status check_common(const starkv_plan* P, int32_t max_ctx, size_t ws_bytes,
+                                  const void* ws) {
+  if (!P) return fail(STARKV_ERR_INVALID_ARG, "plan is NULL");
+  if (max_ctx < 1) return fail(STARKV_ERR_INVALID_ARG, "max_ctx %d < 1", max_ctx);
+  if (max_ctx > P->cfg.capacity)
+    return fail(STARKV_ERR_CAPACITY, "max_ctx %d > capacity %d", max_ctx, P->cfg.capacity);
+  const size_t need = starkv_decode_workspace_bytes(P, max_ctx);
+  if (!ws || ws_bytes < need)
+    return fail(STARKV_ERR_WORKSPACE, "decode workspace %zu bytes < %zu", ws_bytes, need);
+  if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(STARKV_ERR_ALIGNMENT, "ws not 256-byte aligned");
+  return STARKV_OK;
+}
+
+static starkv_status hip_status(int e, const char* what) {
+  if (e != hipSuccess) return fail(STARKV_ERR_HIP, "%s: %s", what, hipGetErrorString((hipError_t)e));
+  return STARKV_OK;
+}
+
+starkv_status starkv_decode_split(const starkv_plan* P, const void* cache, const void* q,
+                                  const void* B_k, const int32_t* ctx_len_dev, int32_t max_ctx,
+                                  void* ws, size_t ws_bytes, starkv_stream_t stream) {
+  starkv_status st = check_common(P, max_ctx, ws_bytes, ws);
+  if (st != STARKV_OK) return st;
+  if (!cache || !q || !B_k || !ctx_len_dev) return fail(STARKV_ERR_INVALID_ARG, "NULL device pointer");
+  if (reinterpret_cast<uintptr_t>(cache) % 256) return fail(STARKV_ERR_ALIGNMENT, "cache not 256-byte aligned");
+  if (reinterpret_cast<uintptr_t>(q) % 16) return fail(STARKV_ERR_ALIGNMENT, "q not 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(B_k) % 16) return fail(STARKV_ERR_ALIGNMENT, "B_k not 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(ctx_len_dev) % 4) return fail(STARKV_ERR_ALIGNMENT, "ctx_len not 4-byte aligned");
+  const starkv_config& c = P->cfg;
+  DecodeParams p;
+  std::memset(&p, 0, sizeof(p));
+  p.cache = static_cast<const uint8_t*>(cache);
+  p.q = q;
+  p.bk = static_cast<const uint16_t*>(B_k);
+  p.ctx_len = ctx_len_dev;
+  p.part = static_cast<float*>(ws);
+  p.batch = c.batch;
+  p.n_q = c.n_q_heads;
+  p.n_kv = c.n_kv_heads;
+  p.group_q = c.n_q_heads / c.n_kv_heads;
+  p.cap_pad = P->layout.padded_capacity;
+  p.max_ctx = max_ctx;
+  p.split_len = starkv_decode_split_tokens(P, max_ctx);
+  p.n_split = starkv_decode_splits(P, max_ctx);
+  p.q_bf16 = c.q_dtype == STARKV_DT_BF16;
+  p.score_scale = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
+  p.log2_theta = std::log2(c.rope_theta);
+  p.v_code_off = P->layout.value_code_offset;
+  p.v_meta_off = P->layout.value_meta_offset;
+  p.rv = c.value_rank;
+  p.v_ro = P->layout.value_outlier_channels;
+  p.v_ng8 = (p.v_ro + 31) / 32;
+  p.v_ng = P->layout.value_groups;
+  p.v_row_bytes = P->layout.value_row_bytes;
+  p.part_stride = part_stride(P);
+  p.n_hg = P->n_hg;
+  std::memcpy(p.hg_first, P->hg_first, sizeof(p.hg_first));
+  std::memcpy(p.hg_frags, P->hg_frags, sizeof(p.hg_frags));
+  std::memcpy(p.hg_raw_bytes, P->hg_raw, sizeof(p.hg_raw_bytes));
+  std::memcpy(p.kh, P->kh, sizeof(p.kh));
+  const int e = launch_decode_split_ntw(p, c.head_dim, c.qmode, P->ct, P->ntw, P->lds_bytes,
+                                        static_cast<void*>(stream));
+  return hip_status(e, "decode_split launch");
+}
+
+starkv_status starkv_decode_combine(const starkv_plan* P, const void* B_v,
+                                    const int32_t* ctx_len_dev, int32_t max_ctx, void* out,
+                                    void* ws, size_t ws_bytes, starkv_stream_t stream) {
+  starkv_status st = check_common(P, max_ctx, ws_bytes, ws);
+  if (st != STARKV_OK) return st;
+  if (!B_v || !ctx_len_dev || !out) return fail(STARKV_ERR_INVALID_ARG, "NULL device pointer");
+  if (reinterpret_cast<uintptr_t>(out) % 16) return fail(STARKV_ERR_ALIGNMENT, "out not 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(B_v) % 2) return fail(STARKV_ERR_ALIGNMENT, "B_v not 2-byte aligned");
+  const starkv_config& c = P->cfg;
+  CombineParams p;
+  p.part = static_cast<const float*>(ws);
+  p.bv = static_cast<const uint16_t*>(B_v);
+  p.ctx_len = ctx_len_dev;
+  p.out = out;
+  p.batch = c.batch;
+  p.n_q = c.n_q_heads;
+  p.n_kv = c.n_kv_heads;
+  p.head_dim = c.head_dim;
+  p.rv = c.value_rank;
+  p.max_ctx = max_ctx;
+  p.split_len = starkv_decode_split_tokens(P, max_ctx);
+  p.n_split = starkv_decode_splits(P, max_ctx);
+  p.part_stride = part_stride(P);
+  p.out_bf16 = c.out_dtype == STARKV_DT_BF16;
+  return hip_status(launch_decode_combine(p, static_cast<void*>(stream)), "decode_combine launch");
+}
+
+starkv_status starkv_decode_attn(const starkv_plan* P, const void* cache, const void* q,
+                                 const void* B_k, const void* B_v, const int32_t* ctx_len_dev,
+                                 int32_t max_ctx, void* out, void* ws, size_t ws_bytes,
+                                 starkv_stream_t stream) {
+  if (!B_v || !out) return fail(STARKV_ERR_INVALID_ARG, "NULL device pointer");
+  starkv_status st = starkv_decode_split(P, cache, q, B_k, ctx_len_dev, max_ctx, ws, ws_bytes, stream);
+  if (st != STARKV_OK) return st;
+  return starkv_decode_combine(P, B_v, ctx_len_dev, max_ctx, out, ws, ws_bytes, stream);
+}
+
+// ---------------------------------------------------------------- append
+
+static void downproj_shape(const starkv_plan* P, int32_t n_new, int* k_split, int* k_chunk) {
+  const int M = P->cfg.batch * n_new, N = P->width, K = P->cfg.d_model;
+  const int tiles = ((M + 63) / 64) * ((N + 63) / 64);
+  int ks = 256 / tiles;
+  if (ks < 1) ks = 1;
+  int chunk = (K + ks - 1) / ks;
+  chunk = (chunk + 31) / 32 * 32;
+  if (chunk < 32) chunk = 32;
+  *k_chunk = chunk;
+  *k_split = (K + chunk - 1) / chunk;
+}
+
+size_t starkv_append_workspace_bytes(const starkv_plan* P, int32_t n_new) {
+  if (!P || n_new < 1 || P->cfg.d_model == 0) return 0;
+  int ks, kc;
+  downproj_shape(P, n_new, &ks, &kc);
+  const int64_t mn = (int64_t)P->cfg.batch * n_new * P->width;
+  return (size_t)(align256(mn * 2) + align256((int64_t)ks * mn * 4));
+}
+
+starkv_status starkv_append(const starkv_plan* P, void* cache, const void* x_or_latents,
+                            const void* A_all, const int32_t* pos_dev, int32_t n_new, void* ws,
+                            size_t ws_bytes, starkv_stream_t stream) {
+  if (!P) return fail(STARKV_ERR_INVALID_ARG, "plan is NULL");
+  if (n_new < 1) return fail(STARKV_ERR_INVALID_ARG, "n_new %d < 1", n_new);
+  if (!cache || !x_or_latents || !pos_dev) return fail(STARKV_ERR_INVALID_ARG, "NULL device pointer");
+  const starkv_config& c = P->cfg;
+  if (c.d_model > 0 && !A_all) return fail(STARKV_ERR_INVALID_ARG, "A_all is NULL with d_model > 0");
+  if (reinterpret_cast<uintptr_t>(cache) % 256) return fail(STARKV_ERR_ALIGNMENT, "cache not 256-byte aligned");
+  if (reinterpret_cast<uintptr_t>(pos_dev) % 4) return fail(STARKV_ERR_ALIGNMENT, "pos not 4-byte aligned");
+  const size_t need = starkv_append_workspace_bytes(P, n_new);
+  if (need > 0 && (!ws || ws_bytes < need))
+    return fail(STARKV_ERR_WORKSPACE, "append workspace %zu bytes < %zu", ws_bytes, need);
+  if (need > 0 && reinterpret_cast<uintptr_t>(ws) % 256)
+    return fail(STARKV_ERR_ALIGNMENT, "ws not 256-byte aligned");
+  if ((int64_t)c.batch * n_new > (1 << 24)) return fail(STARKV_ERR_UNSUPPORTED, "too many new tokens");
+  const uint16_t* lat = static_cast<const uint16_t*>(x_or_latents);
+  if (c.d_model > 0) {
+    if (reinterpret_cast<uintptr_t>(x_or_latents) % 16)
+      return fail(STARKV_ERR_ALIGNMENT, "x not 16-byte aligned");
+    if (reinterpret_cast<uintptr_t>(A_all) % 2) return fail(STARKV_ERR_ALIGNMENT, "A_all not 2-byte aligned");
+    int ks, kc;
+    downproj_shape(P, n_new, &ks, &kc);
+    const int64_t mn = (int64_t)c.batch * n_new * P->width;
+    DownprojParams d;
+    d.x = static_cast<const uint16_t*>(x_or_latents);
+    d.a = static_cast<const uint16_t*>(A_all);
+    d.lat = static_cast<uint16_t*>(ws);
+    d.partial = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + align256(mn * 2));
+    d.m = c.batch * n_new;
+    d.n = P->width;
+    d.k = c.d_model;
+    d.k_split = ks;
+    d.k_chunk = kc;
+    d.x_bf16 = 1;
+    starkv_status st = hip_status(launch_downproj(d, static_cast<void*>(stream)), "downproj launch");
+    if (st != STARKV_OK) return st;
+    lat = d.lat;
+  } else if (reinterpret_cast<uintptr_t>(x_or_latents) % 2) {
+    return fail(STARKV_ERR_ALIGNMENT, "latents not 2-byte aligned");
+  }
+  AppendParams a;
+  std::memset(&a, 0, sizeof(a));
+  a.cache = static_cast<uint8_t*>(cache);
+  a.lat = lat;
+  a.pos = pos_dev;
+  a.batch = c.batch;
+  a.n_new = n_new;
+  a.width = P->width;
+  a.capacity = c.capacity;
+  a.cap_pad = P->layout.padded_capacity;
+  a.qmode = c.qmode;
+  a.n_kv = c.n_kv_heads;
+  int lo = 0;
+  a.n_items = 0;
+  for (int bl = 0; bl <= c.n_kv_heads; ++bl) {
+    const bool v = bl == c.n_kv_heads;
+    const int r = v ? c.value_rank : c.key_rank[bl];
+    a.rank[bl] = r;
+    a.lat_off[bl] = lo;
+    lo += r;
+    a.ro[bl] = v ? P->layout.value_outlier_channels : P->layout.key_outlier_channels[bl];
+    a.ng[bl] = v ? P->layout.value_groups : P->layout.key_groups[bl];
+    a.row_bytes[bl] = v ? P->layout.value_row_bytes : P->layout.key_row_bytes[bl];
+    a.code_off[bl] = v ? P->layout.value_code_offset : P->layout.key_code_offset[bl];
+    a.meta_off[bl] = v ? P->layout.value_meta_offset : P->layout.key_meta_offset[bl];
+    const int items = c.qmode == STARKV_Q_F16 ? (r + 31) / 32 : a.ng[bl];
+    for (int i = 0; i < items; ++i) {
+      if (a.n_items >= 128) return fail(STARKV_ERR_UNSUPPORTED, "too many quantization groups");
+      a.item_block[a.n_items] = bl;
+      a.item_group[a.n_items] = i;
+      ++a.n_items;
+    }
+  }
+  return hip_status(launch_append_pack(a, static_cast<void*>(stream)), "append pack launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,103 @@
+// Internal interface between the host library (starkv_host.cpp) and the HIP
+// kernels (decode.hip, append.hip).  Not part of the public ABI.
+#pragma once
+#include <stdint.h>
+
+#include "starkv.h"
+
+namespace starkv {
+
+constexpr int kWaves = 4;                 // waves per decode workgroup
+constexpr int kThreads = 64 * kWaves;
+constexpr int kWaveTokens = 32;           // tokens per wave per step (two 16-token subtiles)
+constexpr int kStepTokens = kWaves * kWaveTokens;
+constexpr int kMaxSeg = 2 * STARKV_MAX_KV_HEADS;
+
+// One key head as seen by the split kernel (all offsets in bytes).
+struct KHeadInfo {
+  int64_t code_off;      // key code plane
+  int64_t meta_off;      // key meta plane
+  int32_t rank;
+  int32_t nkb;           // 32-channel k-blocks: ceil(rank/32)
+  int32_t n8;            // 8-bit chunks (8 channels each)
+  int32_t ng8;           // 8-bit groups
+  int32_t ngroups;
+  int32_t row_bytes;
+  int32_t bk_row;        // first row of this head in B_k
+  int32_t frag_base;     // first 1 KiB up-projection fragment of this head in LDS
+  int32_t raw_code;      // offset of this head's codes in a wave's LDS staging area
+  int32_t raw_meta;      // offset of this head's meta in a wave's LDS staging area
+};
+
+struct DecodeParams {
+  const uint8_t* cache;
+  const void* q;
+  const uint16_t* bk;
+  const int32_t* ctx_len;
+  float* part;                 // split partials
+  int32_t batch, n_q, n_kv, group_q;   // group_q = H_q / H_kv
+  int32_t cap_pad;             // Cp
+  int32_t max_ctx, split_len, n_split;
+  int32_t q_bf16;
+  float score_scale;           // log2(e)/sqrt(d)
+  double log2_theta;
+  // values
+  int64_t v_code_off, v_meta_off;
+  int32_t rv, v_ro, v_ng8, v_ng, v_row_bytes;
+  int32_t part_stride;         // floats per (b, split, query head)
+  // head groups (blockIdx.z)
+  int32_t n_hg;
+  int32_t hg_first[STARKV_MAX_KV_HEADS + 1];
+  int32_t hg_frags[STARKV_MAX_KV_HEADS];     // fragments used by the group
+  int32_t hg_raw_bytes[STARKV_MAX_KV_HEADS]; // per-wave staging bytes used by the group
+  KHeadInfo kh[STARKV_MAX_KV_HEADS];
+};
+
+struct CombineParams {
+  const float* part;
+  const uint16_t* bv;
+  const int32_t* ctx_len;
+  void* out;
+  int32_t batch, n_q, n_kv, head_dim, rv;
+  int32_t max_ctx, split_len, n_split, part_stride;
+  int32_t out_bf16;
+};
+
+struct AppendParams {
+  uint8_t* cache;
+  const uint16_t* lat;         // fp16 latents [B][n_new][width]
+  const int32_t* pos;
+  int32_t batch, n_new, width, capacity, cap_pad, qmode;
+  int32_t n_kv;
+  // per block: 0..n_kv-1 key heads, n_kv = values
+  int32_t rank[STARKV_MAX_KV_HEADS + 1];
+  int32_t lat_off[STARKV_MAX_KV_HEADS + 1];
+  int32_t ro[STARKV_MAX_KV_HEADS + 1];
+  int32_t ng[STARKV_MAX_KV_HEADS + 1];
+  int32_t row_bytes[STARKV_MAX_KV_HEADS + 1];
+  int64_t code_off[STARKV_MAX_KV_HEADS + 1];
+  int64_t meta_off[STARKV_MAX_KV_HEADS + 1];
+  // work items per token: (block, group) pairs
+  int32_t n_items;
+  int32_t item_block[128];
+  int32_t item_group[128];
+};
+
+struct DownprojParams {
+  const uint16_t* x;           // [M][K] bf16 or fp16
+  const uint16_t* a;           // [K][N] bf16
+  float* partial;              // [ksplit][M][N]
+  uint16_t* lat;               // [M][N] fp16
+  int32_t m, n, k, k_split, k_chunk;
+  int32_t x_bf16;
+};
+
+// launchers (return hipError_t as int)
+int split_lds_bytes(int frags, int nql, int head_dim, int ct, int raw_bytes, int v_ng);
+int launch_decode_split_ntw(const DecodeParams& p, int head_dim, int qmode, int ct, int ntw,
+                            size_t lds_bytes, void* stream);
+int launch_decode_combine(const CombineParams& p, void* stream);
+int launch_append_pack(const AppendParams& p, void* stream);
+int launch_downproj(const DownprojParams& p, void* stream);
+
+}  // namespace starkv

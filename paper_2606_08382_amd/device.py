@@ -1,0 +1,73 @@
+"""Device-memory plumbing around the C ABI: one layer's cache, factors and workspaces.
+
+PyTorch provides device memory and the stream; every computation runs in the
+library's HIP kernels.
+"""
+from __future__ import annotations
+
+from typing import Optional
+
+import numpy as np
+
+from . import starkv as S
+
+
+def to_dev(bits: np.ndarray, device="cuda"):
+    """uint16 / int32 / uint8 numpy array -> device tensor with the same bytes."""
+    import torch
+    a = np.ascontiguousarray(bits)
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(a.copy()).to(device)
+
+
+class Layer:
+    """Plan + cache + workspaces of one attention layer."""
+
+    def __init__(self, batch, n_q_heads, n_kv_heads, head_dim, capacity, key_rank, value_rank,
+                 qmode, rope_theta, q_dtype, out_dtype, d_model=0, device="cuda",
+                 max_ctx: Optional[int] = None):
+        import torch
+        self.cfg = S.make_config(batch, n_q_heads, n_kv_heads, head_dim, capacity, key_rank,
+                                 value_rank, qmode, rope_theta, d_model=d_model,
+                                 q_dtype=q_dtype, out_dtype=out_dtype)
+        self.plan = S.starkv_plan_create(self.cfg)
+        self.device = device
+        self.batch, self.n_q, self.head_dim = batch, n_q_heads, head_dim
+        self.capacity = capacity
+        self.out_dtype = out_dtype
+        self.cache = torch.zeros(S.starkv_cache_bytes(self.plan), dtype=torch.uint8, device=device)
+        self.max_ctx = capacity if max_ctx is None else max_ctx
+        self.dec_ws = torch.empty(max(S.starkv_decode_workspace_bytes(self.plan, self.max_ctx), 256),
+                                  dtype=torch.uint8, device=device)
+        self.app_ws = None
+        self.out = torch.empty((batch, n_q_heads, head_dim), dtype=torch.int16, device=device)
+
+    def _app_ws(self, n_new: int):
+        import torch
+        need = S.starkv_append_workspace_bytes(self.plan, n_new)
+        if need == 0:
+            return None
+        if self.app_ws is None or self.app_ws.numel() < need:
+            self.app_ws = torch.empty(need, dtype=torch.uint8, device=self.device)
+        return self.app_ws
+
+    def append(self, x_or_latents, pos, A_all=None, stream=None):
+        n_new = int(x_or_latents.shape[1])
+        ws = self._app_ws(n_new)
+        S.starkv_append(self.plan, self.cache, x_or_latents, A_all, pos, n_new, ws, stream=stream)
+
+    def decode(self, q, B_k, B_v, ctx_len, max_ctx: Optional[int] = None, out=None, stream=None):
+        mc = self.max_ctx if max_ctx is None else max_ctx
+        out = self.out if out is None else out
+        S.starkv_decode_attn(self.plan, self.cache, q, B_k, B_v, ctx_len, mc, out, self.dec_ws,
+                             stream=stream)
+        return out
+
+    def out_float(self, out=None):
+        """Output bit patterns -> float64 numpy."""
+        import torch
+        o = (self.out if out is None else out).cpu()
+        if self.out_dtype == S.DT_BF16:
+            return o.view(torch.bfloat16).to(torch.float64).numpy()
+        return o.view(torch.float16).to(torch.float64).numpy()

@@ -1,0 +1,176 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle on the same inputs.
+
+Bit-exact: packed cache bytes (codes, scales, zeros, positions) for identical
+fp16 latents.  Floating point: attention outputs within 2e-3 + 1e-3 |oracle|
+elementwise and 1 % of the output's max magnitude.
+"""
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2606_08382_amd import synth
+
+from _helpers import assert_close, oracle_cfg, say, small
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _layer(w, inp, capacity=None, d_model=0, max_ctx=None):
+    from paper_2606_08382_amd.device import Layer
+    return Layer(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim,
+                 w.ctx if capacity is None else capacity, inp.key_rank, w.value_rank, w.qmode,
+                 w.rope_theta, w.q_dtype, w.out_dtype, d_model=d_model, max_ctx=max_ctx)
+
+
+def _dev(a):
+    from paper_2606_08382_amd.device import to_dev
+    return to_dev(a)
+
+
+def _run_case(w, inp, capacity=None, max_ctx=None, ctx_len=None):
+    """Append all latents at row 0, compare bytes, decode, compare outputs."""
+    say(f"case {w.name} B={w.batch} ctx={w.ctx} ranks={inp.key_rank} qmode={w.qmode}")
+    layer = _layer(w, inp, capacity, max_ctx=max_ctx)
+    pos = torch.zeros(w.batch, dtype=torch.int32, device="cuda")
+    layer.append(_dev(inp.latents), pos)
+    ctx = inp.ctx_len if ctx_len is None else np.asarray(ctx_len, np.int32)
+    out = layer.decode(_dev(inp.q), _dev(inp.Bk), _dev(inp.Bv), _dev(ctx))
+    torch.cuda.synchronize()
+    cfg = oracle_cfg(w, inp, capacity)
+    cache = O.new_cache(cfg)
+    O.append(cfg, cache, inp.latents, [0] * w.batch)
+    got_cache = layer.cache.cpu().numpy()
+    diff = np.nonzero(got_cache != cache)[0]
+    assert diff.size == 0, f"{diff.size} cache bytes differ, first at {diff[:6]}"
+    mc = layer.max_ctx if max_ctx is None else max_ctx
+    ref, _ = O.decode_attn(cfg, cache, inp.q, w.q_dtype == synth.DT_BF16, inp.Bk, inp.Bv,
+                           np.minimum(ctx, mc))
+    got = layer.out_float()
+    e, s = assert_close(got, ref, w.name)
+    say(f"  max err {e:.3e}  max |o| {s:.3e}")
+    return layer, got, ref
+
+
+@pytest.mark.parametrize("name,ctx,batch", [("c1", 1024, None), ("c1", 1000, None),
+                                            ("c2", 700, 2), ("c3", 1100, 2), ("c3", 129, 1),
+                                            ("c5", 600, 2)])
+@pytest.mark.parametrize("peaked", [False, True])
+def test_decode_matches_oracle(name, ctx, batch, peaked):
+    w = small(name, ctx, batch)
+    inp = synth.generate(w, peaked=peaked)
+    _run_case(w, inp)
+
+
+def test_ragged_lengths_and_partial_splits():
+    w = small("c4", ctx=900, batch=6, ragged=(1, 900))
+    inp = synth.generate(w)
+    inp.ctx_len[:3] = [1, 128, 257]
+    _run_case(w, inp)
+
+
+def test_zero_length_and_clamped_lengths():
+    w = small("c3", ctx=600, batch=3)
+    inp = synth.generate(w)
+    layer, got, ref = _run_case(w, inp, ctx_len=[0, 600, 5], max_ctx=600)
+    assert np.all(got[0] == 0.0)
+    # lengths above max_ctx are clamped to max_ctx
+    w2 = small("c3", ctx=600, batch=3)
+    _run_case(w2, inp, capacity=1000, max_ctx=400, ctx_len=[999, 400, 17])
+
+
+def test_decode_is_deterministic():
+    w = small("c3", ctx=800, batch=2)
+    inp = synth.generate(w)
+    layer, got, _ = _run_case(w, inp)
+    o1 = layer.out.clone()
+    for _ in range(3):
+        layer.decode(_dev(inp.q), _dev(inp.Bk), _dev(inp.Bv), _dev(inp.ctx_len))
+        torch.cuda.synchronize()
+        assert torch.equal(layer.out, o1)
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3"])
+def test_incremental_appends_bit_exact(name):
+    """Appends of 1, 3, 37, ... tokens at unaligned rows rewrite only their rows."""
+    w = small(name, ctx=300, batch=2)
+    inp = synth.generate(w)
+    say(f"incremental {w.name}")
+    layer = _layer(w, inp)
+    cfg = oracle_cfg(w, inp)
+    cache = O.new_cache(cfg)
+    start = 0
+    for n in [1, 3, 37, 1, 64, 5, 100, 1, 2, 30, 56]:
+        n = min(n, w.ctx - start)
+        if n <= 0:
+            break
+        chunk = np.ascontiguousarray(inp.latents[:, start:start + n])
+        pos = np.array([start, start], np.int32)
+        layer.append(_dev(chunk), _dev(pos))
+        O.append(cfg, cache, chunk, pos)
+        start += n
+    torch.cuda.synchronize()
+    got = layer.cache.cpu().numpy()
+    diff = np.nonzero(got != cache)[0]
+    assert diff.size == 0, f"{diff.size} bytes differ, first at {diff[:6]}"
+    # different positions per sequence, rows past capacity dropped
+    pos = np.array([w.ctx - 2, 7], np.int32)
+    chunk = np.ascontiguousarray(inp.latents[:, :5])
+    layer.append(_dev(chunk), _dev(pos))
+    O.append(cfg, cache, chunk, pos)
+    torch.cuda.synchronize()
+    assert np.array_equal(layer.cache.cpu().numpy(), cache)
+
+
+@pytest.mark.parametrize("name,n_new,d_model", [("c4", 1, 4096), ("c3", 1, 4096), ("c5", 96, 1024)])
+def test_append_from_hidden_states(name, n_new, d_model):
+    """Down-projection then quantization: latents within 1 fp16 ulp of the oracle's fp64
+    product; codes bit-exact when the oracle re-quantizes the GPU's fp16 latents."""
+    w = small(name, ctx=256, batch=min(synth.WORKLOADS[name].batch, 4))
+    w = w.with_(d_model=d_model)
+    inp = synth.generate(w, with_hidden=True, n_hidden_tokens=n_new)
+    say(f"hidden {w.name} n_new={n_new} d_model={d_model}")
+    layer = _layer(w, inp, d_model=d_model)
+    pos = np.array([3 + 11 * b for b in range(w.batch)], np.int32)
+    layer.append(_dev(inp.x), _dev(pos), A_all=_dev(inp.A))
+    torch.cuda.synchronize()
+    width = sum(inp.key_rank) + w.value_rank
+    lat_gpu = layer.app_ws[: w.batch * n_new * width * 2].cpu().numpy().view(np.uint16)
+    lat_gpu = lat_gpu.reshape(w.batch, n_new, width)
+    cfg = oracle_cfg(w, inp, d_model=d_model)
+    lat_ref, z64 = O.downproj(cfg, inp.x, True, inp.A)
+    g = lat_gpu.reshape(-1, width).view(np.float16).astype(np.float64)
+    r = lat_ref.view(np.float16).astype(np.float64)
+    ulp = np.abs(np.spacing(r.astype(np.float16)).astype(np.float64))
+    assert np.all(np.abs(g - r) <= ulp), f"max diff {np.abs(g - r).max()}"
+    cache = O.new_cache(cfg)
+    O.append(cfg, cache, lat_gpu, pos)
+    assert np.array_equal(layer.cache.cpu().numpy(), cache)
+
+
+def test_full_size_128k_sampled_heads():
+    """The 128K workload at full size in the benchmark's launch configuration: the whole packed
+    cache bit-exact, and sampled query heads (one per KV head, across the batch) within
+    tolerance."""
+    w = synth.WORKLOADS["c3"]
+    inp = synth.generate(w)
+    say(f"full size {w.name}")
+    layer = _layer(w, inp)
+    pos = torch.zeros(w.batch, dtype=torch.int32, device="cuda")
+    for b0 in range(0, w.ctx, 32768):          # append in four chunks
+        chunk = np.ascontiguousarray(inp.latents[:, b0:b0 + 32768])
+        layer.append(_dev(chunk), pos + b0)
+    out = layer.decode(_dev(inp.q), _dev(inp.Bk), _dev(inp.Bv), _dev(inp.ctx_len))
+    torch.cuda.synchronize()
+    cfg = oracle_cfg(w, inp)
+    cache = O.new_cache(cfg)
+    O.append(cfg, cache, inp.latents, [0] * w.batch)
+    got_cache = layer.cache.cpu().numpy()
+    assert np.array_equal(got_cache, cache)
+    sel = [(0, 5), (3, 30)]                     # query heads of KV heads 1 and 7
+    ref, _ = O.decode_attn(cfg, cache, inp.q, True, inp.Bk, inp.Bv, inp.ctx_len, sel=sel)
+    got = layer.out_float()
+    for (b, i) in sel:
+        e, s = assert_close(got[b, i], ref[b, i], f"b={b} head={i}")
+    say(f"  sampled heads ok, last max err {e:.3e} |o| {s:.3e}")
