@@ -117,9 +117,8 @@ typedef struct starkv_plan starkv_plan;   /* opaque, immutable after creation */
  *   holds tokens 4q..4q+3 and 16+4q..16+4q+3).  For each chunk q and channel c the
  *   eight slots are stored together: F16 16 B (slot at 2*slot), 8-bit 8 B (slot at
  *   byte slot), 4-bit one 32-bit word (slot 2k in bits 4k..4k+3, slot 2k+1 in bits
- *   16+4k..16+4k+3, k = 0..3).  The
- *   8-bit region (all q, then all channels) precedes the 4-bit region; within a
- *   region the order is [q][channel][slots].
+ *   16+4k..16+4k+3, k = 0..3).  The 8-bit region precedes the 4-bit region;
+ *   within a region the order is [channel][q][slots].
  *   Value meta: per 32-token block, per group g, per chunk q: the 8 slots' s
  *   (16 B) then their z (16 B), at ((g*4 + q)*32) inside the block's meta.
  * ---------------------------------------------------------------------------- */

@@ -199,7 +199,8 @@ static int64_t key_meta_at(const orc_cfg* cfg, int g, int b, int t, int gi, int6
 }
 
 /* Value code of channel c at token t.  A 32-token block is split into four
- * 8-token chunks k: tokens 4k..4k+3 and 16+4k..16+4k+3; slot 0..3 and 4..7. */
+ * 8-token chunks k: tokens 4k..4k+3 and 16+4k..16+4k+3; slot 0..3 and 4..7.
+ * Within a precision region the order is [channel][chunk][slots]. */
 static void value_slot(int t, int* kq, int* slot) {
   int tau = t % 32, sub = tau / 16, rem = tau % 16;
   *kq = rem / 4;
@@ -214,13 +215,13 @@ static int64_t value_code_at(const orc_cfg* cfg, int b, int t, int c, int* nib) 
   int kq, slot;
   value_slot(t, &kq, &slot);
   *nib = 0;
-  if (cfg->qmode == ORC_Q_F16) return base + ((int64_t)kq * r + c) * 16 + slot * 2;
+  if (cfg->qmode == ORC_Q_F16) return base + ((int64_t)c * 4 + kq) * 16 + slot * 2;
   int ro = orc_outlier_channels(cfg->qmode, r);
-  if (c < ro) return base + ((int64_t)kq * ro + c) * 8 + slot;
+  if (c < ro) return base + ((int64_t)c * 4 + kq) * 8 + slot;
   /* in a 4-bit chunk word, slot 2k sits in nibble k and slot 2k+1 in nibble k+4 */
   int p = (slot % 2 == 0) ? slot / 2 : slot / 2 + 4;
   *nib = p % 2;
-  return base + 32 * ro + ((int64_t)kq * (r - ro) + (c - ro)) * 4 + p / 2;
+  return base + 32 * ro + ((int64_t)(c - ro) * 4 + kq) * 4 + p / 2;
 }
 
 /* Value meta: per 32-token block, group and chunk, the 8 scales of the chunk's

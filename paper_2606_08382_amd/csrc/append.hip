@@ -146,7 +146,7 @@ __global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
       if (bits == 16) {
         for (int i = 0; i < n; ++i) {
           const int c = c0 + i;
-          *reinterpret_cast<uint16_t*>(vblock + ((int64_t)kq * r + c) * 16 + slot * 2) = x[i];
+          *reinterpret_cast<uint16_t*>(vblock + ((int64_t)c * 4 + kq) * 16 + slot * 2) = x[i];
         }
         continue;
       }
@@ -154,13 +154,13 @@ __global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
       if (bits == 8) {
         for (int i = 0; i < n; ++i) {
           const int c = c0 + i;
-          vblock[((int64_t)kq * ro + c) * 8 + slot] = (uint8_t)group_code(g, x[i]);
+          vblock[((int64_t)c * 4 + kq) * 8 + slot] = (uint8_t)group_code(g, x[i]);
         }
       } else {
         if (!have_words) {
           for (int i = 0; i < n; ++i)
             words[i] = *reinterpret_cast<const uint32_t*>(
-                vblock + 32 * ro + ((int64_t)kq * ri + (c0 - ro + i)) * 4);
+                vblock + 32 * ro + ((int64_t)(c0 - ro + i) * 4 + kq) * 4);
           have_words = true;
         }
         // slot 2k -> bits 4k..4k+3, slot 2k+1 -> bits 16+4k..16+4k+3
@@ -176,7 +176,7 @@ __global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
   }
   if (have_words) {
     for (int i = 0; i < n; ++i)
-      *reinterpret_cast<uint32_t*>(vblock + 32 * ro + ((int64_t)kq * ri + (c0 - ro + i)) * 4) =
+      *reinterpret_cast<uint32_t*>(vblock + 32 * ro + ((int64_t)(c0 - ro + i) * 4 + kq) * 4) =
           words[i];
   }
 }

@@ -101,44 +101,189 @@ __device__ __forceinline__ _Float16 load_q(const void* q, int64_t idx, int bf16)
 
 // LDS layout of the split kernel (byte offsets); identical on the host.
 struct SplitLds {
-  int frag, qc, red, alpha, loop, raw, vmeta, pbuf, rope, total;
+  int frag, qc, red, alpha, flag, rot, loop, raw, vcode, vmeta, pbuf, rope, total;
 };
 
+// vcode_bytes: value codes of one step (kStepTokens tokens), a multiple of 16.
 __host__ __device__ inline SplitLds split_lds(int frags, int nql, int head_dim, int ct,
-                                             int raw_bytes, int v_ng) {
+                                             int raw_bytes, int v_ng, int vcode_bytes) {
   SplitLds L;
   L.frag = 0;
   L.qc = frags * 1024;
-  L.red = L.qc + ((nql * head_dim * 2 + 16 + 15) / 16) * 16;
-  L.alpha = L.red + kWaves * ct * 16 * 4;
-  L.loop = L.alpha + ct * 16 * 4;
+  L.red = L.qc + ((nql * (head_dim + 8) * 2 + 16 + 15) / 16) * 16;
+  L.alpha = L.red + kTokenGroups * ct * 16 * 4;
+  L.flag = L.alpha + ct * 16 * 4;
+  L.rot = L.flag + 16;
+  L.loop = L.rot + 64 * 8;
   L.raw = L.loop;
-  L.vmeta = L.raw + kWaves * raw_bytes;
+  L.vcode = L.raw + kWaves * raw_bytes;
+  L.vmeta = L.vcode + vcode_bytes;
   L.pbuf = L.vmeta + 4 * v_ng * 128;
-  int loop_end = L.pbuf + kWaves * ct * 1024;
+  int loop_end = L.pbuf + kTokenGroups * ct * 1024;
   L.rope = L.loop;   // RoPE tables (prologue only) alias the loop area
-  int rope_end = L.rope + (64 + 64 + 16 * 64 + 8 * 64) * 8;
+  int rope_end = L.rope + (64 + 16 * 64 + 8 * 64) * 8;
   L.total = loop_end > rope_end ? loop_end : rope_end;
   return L;
 }
 
-constexpr int kMaxLoads = 8;   // 16-byte key-staging loads per lane per step
-constexpr int kMaxVMeta = 3;   // 16-byte value-meta loads per thread per step
+// Asynchronous copy of n_bytes (a multiple of 16) from global memory into LDS by
+// the whole workgroup, 16 bytes per lane, without passing through registers.
+// Completion is tracked by vmcnt.
+__device__ __forceinline__ void copy_to_lds(uint8_t* lds, const uint8_t* src, int n_bytes,
+                                            int w, int lane) {
+  for (int base = w * 1024; base < n_bytes; base += kWaves * 1024) {
+    if (base + lane * 16 < n_bytes)
+      __builtin_amdgcn_global_load_lds(src + base + lane * 16, lds + base, 16, 0, 0);
+  }
+}
 
+__device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel) {
+  return __builtin_amdgcn_perm(hi, lo, sel);
+}
+
+// 8-bit codes d (bytes b0..b3) -> fp16 pairs (1024+b0, 1024+b1) and (1024+b2, 1024+b3)
+__device__ __forceinline__ u4 deq_int8p(u2 d, h2 s0, h2 z0, h2 s1, h2 z1, h2 s2, h2 z2, h2 s3,
+                                        h2 z3) {
+  u4 r;
+  r.x = deq_pair(perm(0x64646464u, d.x, 0x05010400u), s0, z0);
+  r.y = deq_pair(perm(0x64646464u, d.x, 0x05030402u), s1, z1);
+  r.z = deq_pair(perm(0x64646464u, d.y, 0x05010400u), s2, z2);
+  r.w = deq_pair(perm(0x64646464u, d.y, 0x05030402u), s3, z3);
+  return r;
+}
+
+// One KV head with KB k-blocks for the wave's 32 tokens: dequantize the key
+// latents from the LDS staging area into MFMA operands, rebuild the keys
+// (16 rows of the head dimension per MFMA, both halves of every RoPE pair),
+// rotate, and accumulate the scores of the head's query heads.  The
+// reconstruction of score k-block kbs+1 is issued before the rotation of
+// kbs so the matrix cores and the vector ALUs overlap.
+template <int D, int QM, int CTH, int KB>
+__device__ __forceinline__ void key_head(const KHeadInfo& kh, const uint8_t* raw, const h8* frag,
+                                         const _Float16* qc, int qzero, int gl, int ct0, int G,
+                                         int lane, int col, int quad,
+                                         const float2 (&cs)[2][4 * (D / 32)],
+                                         f4 (&acc_s)[2][CTH]) {
+  constexpr int NKBS = D / 32;
+  constexpr int QS = D + 8;                  // padded query row (halves)
+  const uint8_t* rc = raw + kh.raw_code;
+  const uint8_t* rm = raw + kh.raw_meta;
+  const int rb16 = 16 * kh.row_bytes;        // bytes of one 16-token block
+  // all LDS reads of the head first, then the dequantization
+  u2 code[2][KB];
+  uint32_t meta[2][KB];
+  u4 cf[2][KB];
+  bool valid[KB], is8[KB];
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb) {
+    const int c = 4 * kb + quad;
+    valid[kb] = (kb < KB - 1) || (8 * c < kh.rank);
+    if (QM == STARKV_Q_F16) {
+      const int off = valid[kb] ? kb * 1024 + lane * 16 : 0;
+#pragma unroll
+      for (int s = 0; s < 2; ++s) cf[s][kb] = *reinterpret_cast<const u4*>(rc + s * rb16 + off);
+    } else {
+      is8[kb] = c < kh.n8;
+      int off = is8[kb] ? kb * 512 + lane * 8 : kh.n8 * 64 + kb * 256 + lane * 4;
+      int gi = is8[kb] ? 0 : kh.ng8 + (c - kh.n8) / 4;
+      if (!valid[kb]) { off = 0; gi = 0; }
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        meta[s][kb] = *reinterpret_cast<const uint32_t*>(rm + (s * kh.ngroups + gi) * 64 + col * 4);
+        code[s][kb] = *reinterpret_cast<const u2*>(rc + s * rb16 + off);
+      }
+    }
+  }
+  h8 xop[2][KB];
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      u4 v;
+      if (QM == STARKV_Q_F16) {
+        v = cf[s][kb];
+      } else {
+        const uint32_t mz = meta[s][kb];
+        const h2 sv = as_h2(perm(mz, mz, 0x01000100u));
+        const h2 zv = as_h2(perm(mz, mz, 0x03020302u));
+        if (QM == STARKV_Q_MIX8_4 && is8[kb]) v = deq_int8p(code[s][kb], sv, zv, sv, zv, sv, zv, sv, zv);
+        else v = deq_int4(code[s][kb].x, sv, zv, sv, zv, sv, zv, sv, zv);
+      }
+      if (!valid[kb]) v = (u4){0, 0, 0, 0};
+      xop[s][kb] = __builtin_bit_cast(h8, v);
+    }
+  }
+  const int ct_g = (gl * G) / 16 - ct0;      // score tile of this head within the half
+  const int c_lo = (gl * G) % 16;
+  const bool mine = col >= c_lo && col < c_lo + G;
+  const int qrow = (((gl * G) / 16) * 16 + col) * QS;
+  const int fb = kh.frag_base;
+  f4 klo[2][2], khi[2][2];   // [buffer][subtile]
+#pragma unroll
+  for (int kbs = 0; kbs <= NKBS; ++kbs) {
+    if (kbs < NKBS) {        // reconstruct rows 16*kbs.. and 16*kbs + D/2..
+      const int bufn = kbs & 1;
+#pragma unroll
+      for (int s = 0; s < 2; ++s) { klo[bufn][s] = (f4){0, 0, 0, 0}; khi[bufn][s] = (f4){0, 0, 0, 0}; }
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        const h8 a_lo = frag[(fb + kbs * KB + kb) * 64 + lane];
+        const h8 a_hi = frag[(fb + (kbs + NKBS) * KB + kb) * 64 + lane];
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+          klo[bufn][s] = mfma16(a_lo, xop[s][kb], klo[bufn][s]);
+          khi[bufn][s] = mfma16(a_hi, xop[s][kb], khi[bufn][s]);
+        }
+      }
+    }
+    if (kbs > 0) {           // rotate and score k-block kbs-1
+      const int kq = kbs - 1, buf = kq & 1;
+      const h8 qf = *reinterpret_cast<const h8*>(qc + (mine ? qrow + (kq * 4 + quad) * 8 : qzero));
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        u4 kr;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float2 r = cs[s][4 * kq + e];
+          const float a = klo[buf][s][e], bb = khi[buf][s][e];
+          const float bs = bb * r.y, as = a * r.y;
+          const _Float16 ra = (_Float16)__builtin_fmaf(a, r.x, -bs);
+          const _Float16 rb = (_Float16)__builtin_fmaf(bb, r.x, as);
+          kr[e] = as_u32((h2){ra, rb});
+        }
+        const h8 kop = __builtin_bit_cast(h8, kr);
+#pragma unroll
+        for (int c = 0; c < CTH; ++c)
+          if (CTH == 1 || c == ct_g) acc_s[s][c] = mfma16(kop, qf, acc_s[s][c]);
+      }
+    }
+  }
+}
+
+// CT: score tiles (16 query heads) of a head group; CTH = tiles of one half;
+// NTW: value-channel tiles (16 channels) per wave.
 template <int D, int QM, int CT, int NTW>
 __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams p) {
   extern __shared__ __align__(16) uint8_t smem[];
+  constexpr int CTH = (CT + 1) / 2;
   constexpr int NKBS = D / 32;   // score k-blocks (head dimension / 32)
   constexpr int NF = 4 * NKBS;   // RoPE frequencies held per lane
   constexpr int HALF = D / 2;
+  constexpr int QS = D + 8;
   const int tid = threadIdx.x;
-  const int lane = tid & 63, w = tid >> 6;
+  const int lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int tg = w & (kTokenGroups - 1);   // token group: tokens 32*tg.. of each step
+  const int hh = w / kTokenGroups;         // half of the group's KV heads
   const int col = lane & 15, quad = lane >> 4;
   const int split = blockIdx.x, b = blockIdx.y, hg = blockIdx.z;
-  const int g0 = p.hg_first[hg], g1 = p.hg_first[hg + 1];
+  const int g0 = p.hg_first[hg], g1 = p.hg_first[hg + 1], gm = p.hg_mid[hg];
   const int G = p.group_q;
   const int nql = (g1 - g0) * G;
   const int q0 = g0 * G;
+  const int ct_half = ((gm - g0) * G + 15) / 16;          // score tiles of the first half
+  const int ct0 = hh ? ct_half : 0;                        // first score tile of this half
+  const int ctn = hh ? (nql + 15) / 16 - ct_half : ct_half; // its tile count
 
   int L = p.ctx_len[b];
   L = L < 0 ? 0 : (L > p.max_ctx ? p.max_ctx : L);
@@ -148,28 +293,32 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   const int n_steps = (t_end - t_begin + kStepTokens - 1) / kStepTokens;
 
   const int raw_bytes = p.hg_raw_bytes[hg];
-  const SplitLds LL = split_lds(p.hg_frags[hg], nql, D, CT, raw_bytes, p.v_ng);
+  const int my_raw = p.hh_raw[hg][hh];
+  const int vcode_bytes = kStepTokens * p.v_row_bytes;
+  const SplitLds LL = split_lds(p.hg_frags[hg], nql, D, CT, raw_bytes, p.v_ng, vcode_bytes);
   h8* frag = reinterpret_cast<h8*>(smem + LL.frag);
   _Float16* qc = reinterpret_cast<_Float16*>(smem + LL.qc);
   float* red = reinterpret_cast<float*>(smem + LL.red);
   float* alpha_s = reinterpret_cast<float*>(smem + LL.alpha);
+  int* flag_s = reinterpret_cast<int*>(smem + LL.flag);
+  float2* rot_s = reinterpret_cast<float2*>(smem + LL.rot);        // [64] step rotations
   uint8_t* raw = smem + LL.raw + w * raw_bytes;
+  uint8_t* vcode = smem + LL.vcode;
   uint8_t* vmeta = smem + LL.vmeta;
   h8* pbuf = reinterpret_cast<h8*>(smem + LL.pbuf);
   float2* rope_base = reinterpret_cast<float2*>(smem + LL.rope);   // [64]
-  float2* rope_step = rope_base + 64;                               // [64]
-  float2* rope_col = rope_step + 64;                                // [16][64]
+  float2* rope_col = rope_base + 64;                                // [16][64]
   float2* rope_ws = rope_col + 16 * 64;                             // [8][64]
+  const int qzero = nql * QS;
 
   // ---------------------------------------------------------------- prologue
-  // Zero the up-projection fragments (rank padding must read as 0).
   {
     u4* f = reinterpret_cast<u4*>(smem + LL.frag);
     const int n = p.hg_frags[hg] * 64;
     for (int i = tid; i < n; i += kThreads) f[i] = (u4){0, 0, 0, 0};
   }
   // RoPE angle tables: rotation by t*omega_j composed as
-  // base(t_begin) * step-of-wave(32w + 16s) * within-subtile(col).
+  // base(t_begin) * step-of-wave(32*tg + 16s) * within-subtile(col).
   {
     const double l2t = p.log2_theta;
     for (int i = tid; i < HALF; i += kThreads) {
@@ -181,7 +330,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       rope_base[i] = make_float2((float)ca, (float)sa);
       float ss, cs;
       sincosf((float)(kStepTokens * om), &ss, &cs);
-      rope_step[i] = make_float2(cs, ss);
+      rot_s[i] = make_float2(cs, ss);
     }
     for (int i = tid; i < 16 * HALF; i += kThreads) {
       const int c = i / HALF, j = i % HALF;
@@ -198,23 +347,20 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       rope_ws[k * 64 + j] = make_float2(cs, ss);
     }
   }
-  // Query heads of the group, fp16, permuted so that lane (col, quad) of score
-  // k-block kbs reads one 16-byte vector: element 2e = q[j], 2e+1 = q[j + D/2],
-  // j = 16*kbs + 4*quad + e.  A zero vector follows for lanes whose column does
-  // not belong to the KV head being scored.
-  {
-    const int n = nql * D;
-    for (int i = tid; i < n / 2; i += kThreads) {
-      const int il = i / HALF, r = i % HALF;          // r = kbs*16 + quad*4 + e
-      const int kbs = r / 16, qd = (r / 4) % 4, e = r % 4;
-      const int j = 16 * kbs + 4 * qd + e;
-      const int64_t src = ((int64_t)b * p.n_q + q0 + il) * D;
-      _Float16* dst = qc + il * D + (kbs * 4 + qd) * 8 + 2 * e;
-      dst[0] = load_q(p.q, src + j, p.q_bf16);
-      dst[1] = load_q(p.q, src + j + HALF, p.q_bf16);
-    }
-    if (tid < 8) qc[n + tid] = (_Float16)0.0f;
+  // Query heads of the group in fp16, one padded row per head, permuted so that
+  // lane (col, quad) of score k-block kbs reads one 16-byte vector: element
+  // 2e = q[j], 2e+1 = q[j + D/2], j = 16*kbs + 4*quad + e.  A zero vector follows
+  // for lanes whose column is not a query head of the KV head being scored.
+  for (int i = tid; i < nql * HALF; i += kThreads) {
+    const int il = i / HALF, r = i % HALF;          // r = kbs*16 + quad*4 + e
+    const int kbs = r / 16, qd = (r / 4) % 4, e = r % 4;
+    const int j = 16 * kbs + 4 * qd + e;
+    const int64_t src = ((int64_t)b * p.n_q + q0 + il) * D;
+    _Float16* dst = qc + il * QS + (kbs * 4 + qd) * 8 + 2 * e;
+    dst[0] = load_q(p.q, src + j, p.q_bf16);
+    dst[1] = load_q(p.q, src + j + HALF, p.q_bf16);
   }
+  if (tid < 8) qc[qzero + tid] = (_Float16)0.0f;
   __syncthreads();
   // Up-projection fragments.  Fragment (head, m-tile mt, k-block kb), lane
   // (jj, kq): 8 halves = B_k[row][16*mt + jj] for the 8 channels of chunk
@@ -240,33 +386,31 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       }
     }
   }
-  // Per-lane rotations for its two subtiles: angles (t_begin + 32w + 16s + col) * omega_j.
   float2 cs[2][NF];
-  float2 rot[NF];
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
     const int j = 16 * (f / 4) + 4 * quad + (f % 4);
 #pragma unroll
     for (int s = 0; s < 2; ++s)
-      cs[s][f] = cmul(cmul(rope_base[j], rope_ws[(2 * w + s) * 64 + j]), rope_col[col * 64 + j]);
-    rot[f] = rope_step[j];
+      cs[s][f] = cmul(cmul(rope_base[j], rope_ws[(2 * tg + s) * 64 + j]), rope_col[col * 64 + j]);
   }
   __syncthreads();   // RoPE tables are dead from here on (the loop area reuses them)
 
   // ---------------------------------------------------------------- prefetch setup
-  // Key staging: the wave's 32 tokens of every key head of the group, codes then
+  // Key staging: the wave's 32 tokens of every key head of its half, codes then
   // meta per head, as one contiguous LDS area filled by flat 16-byte loads.
   const uint8_t* ld_ptr[kMaxLoads];
   int ld_stride[kMaxLoads];
   {
-    const int64_t blk16 = (int64_t)b * (p.cap_pad / 16) + (t_begin + 32 * w) / 16;
+    const int64_t blk16 = (int64_t)b * (p.cap_pad / 16) + (t_begin + 32 * tg) / 16;
+    const int ha = hh ? gm : g0, hb = hh ? g1 : gm;
 #pragma unroll
     for (int i = 0; i < kMaxLoads; ++i) {
       const int off = (i * 64 + lane) * 16;
       ld_ptr[i] = nullptr;
       ld_stride[i] = 0;
-      if (off < raw_bytes) {
-        for (int gg = g0; gg < g1; ++gg) {
+      if (off < my_raw) {
+        for (int gg = ha; gg < hb; ++gg) {
           const KHeadInfo& kh = p.kh[gg];
           const int ncode = 32 * kh.row_bytes, nmeta = 2 * kh.ngroups * 64;
           if (off >= kh.raw_code && off < kh.raw_code + ncode) {
@@ -286,68 +430,51 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     for (int i = 0; i < kMaxLoads; ++i)
       if (ld_ptr[i]) kraw[i] = *reinterpret_cast<const u4*>(ld_ptr[i] + (int64_t)step * ld_stride[i]);
   };
-  // Value codes of this wave's channel tiles for the four 32-token blocks of a step.
-  constexpr int VW = (QM == STARKV_Q_F16) ? 4 : ((QM == STARKV_Q_MIX8_4) ? 2 : 1);
+  // value codes and meta of one step are copied into LDS ahead of use; per-lane
+  // offsets of this wave's channel tiles inside a 32-token block
   const int NT = p.rv / 16;
-  const int v_ri = p.rv - p.v_ro;
-  uint32_t vraw[4][NTW][VW];
+  int v_off[NTW], v_gi[NTW];
+#pragma unroll
+  for (int t = 0; t < NTW; ++t) {
+    const int nt = w * NTW + t;
+    const int rho = 16 * nt + col;
+    const bool is8 = rho < p.v_ro;
+    if (QM == STARKV_Q_F16) v_off[t] = (rho * 4 + quad) * 16;
+    else if (is8) v_off[t] = (rho * 4 + quad) * 8;
+    else v_off[t] = 32 * p.v_ro + ((rho - p.v_ro) * 4 + quad) * 4;
+    v_gi[t] = is8 ? rho / 32 : p.v_ng8 + (rho - p.v_ro) / 32;
+  }
   const int64_t vblk0 = (int64_t)b * (p.cap_pad / 32) + t_begin / 32;
-  auto load_v = [&](int step) {
-#pragma unroll
-    for (int ww = 0; ww < 4; ++ww) {
-      const uint8_t* blk = p.cache + p.v_code_off +
-                           (vblk0 + (int64_t)step * 4 + ww) * 32 * p.v_row_bytes;
-#pragma unroll
-      for (int t = 0; t < NTW; ++t) {
-        const int nt = w * NTW + t;
-        if (nt < NT) {
-          const int rho = 16 * nt + col;
-          if (QM == STARKV_Q_F16) {
-            const u4 v = *reinterpret_cast<const u4*>(blk + ((int64_t)quad * p.rv + rho) * 16);
-            vraw[ww][t][0] = v.x; vraw[ww][t][1 % VW] = v.y;
-            vraw[ww][t][2 % VW] = v.z; vraw[ww][t][3 % VW] = v.w;
-          } else if (rho < p.v_ro) {
-            const u2 v = *reinterpret_cast<const u2*>(blk + ((int64_t)quad * p.v_ro + rho) * 8);
-            vraw[ww][t][0] = v.x; vraw[ww][t][(VW - 1) & 1] = v.y;
-          } else {
-            vraw[ww][t][0] = *reinterpret_cast<const uint32_t*>(
-                blk + 32 * p.v_ro + ((int64_t)quad * v_ri + (rho - p.v_ro)) * 4);
-          }
-        }
-      }
-    }
-  };
-  u4 vm[kMaxVMeta];
   const int vmeta_bytes = 4 * p.v_ng * 128;
-  auto load_vm = [&](int step) {
-    const uint8_t* src = p.cache + p.v_meta_off + (vblk0 + (int64_t)step * 4) * p.v_ng * 128;
-#pragma unroll
-    for (int i = 0; i < kMaxVMeta; ++i) {
-      const int off = (i * kThreads + tid) * 16;
-      if (off < vmeta_bytes) vm[i] = *reinterpret_cast<const u4*>(src + off);
-    }
+  auto load_v = [&](int step) {
+    copy_to_lds(vcode, p.cache + p.v_code_off + (vblk0 + (int64_t)step * 4) * 32 * p.v_row_bytes,
+                vcode_bytes, w, lane);
+    if (QM != STARKV_Q_F16)
+      copy_to_lds(vmeta, p.cache + p.v_meta_off + (vblk0 + (int64_t)step * 4) * p.v_ng * 128,
+                  vmeta_bytes, w, lane);
   };
 
   // ---------------------------------------------------------------- main loop
-  float m_run[CT], l_part[CT];
+  float m_run[CTH], l_part[CTH];
   f4 acc_v[CT][NTW];
 #pragma unroll
-  for (int c = 0; c < CT; ++c) {
+  for (int c = 0; c < CTH; ++c) {
     m_run[c] = -INFINITY;
     l_part[c] = 0.0f;
+  }
+#pragma unroll
+  for (int c = 0; c < CT; ++c)
 #pragma unroll
     for (int t = 0; t < NTW; ++t) acc_v[c][t] = (f4){0, 0, 0, 0};
-  }
   const float sc = p.score_scale;
 
   load_k(0);
   load_v(0);
-  if (QM != STARKV_Q_F16) load_vm(0);
 
   for (int step = 0; step < n_steps; ++step) {
     const int t_step = t_begin + step * kStepTokens;
-    const int tw = t_step + 32 * w;
-    // stage this step's key bytes, then prefetch the next step's
+    const int tw = t_step + 32 * tg;
+    const bool full = (t_step + kStepTokens <= t_end);
 #pragma unroll
     for (int i = 0; i < kMaxLoads; ++i)
       if (ld_ptr[i]) *reinterpret_cast<u4*>(raw + (i * 64 + lane) * 16) = kraw[i];
@@ -355,157 +482,90 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): staging visible to this wave
 
     // ------------------------------------------ keys: reconstruct, rotate, score
-    f4 acc_s[2][CT];
+    f4 acc_s[2][CTH];
 #pragma unroll
     for (int s = 0; s < 2; ++s)
 #pragma unroll
-      for (int c = 0; c < CT; ++c) acc_s[s][c] = (f4){0, 0, 0, 0};
-
-    for (int gg = g0; gg < g1; ++gg) {
-      const KHeadInfo& kh = p.kh[gg];
-      const int gl = gg - g0;
-      // key operand: lane (tau = col, kq = quad) holds chunk 4*kb + quad of token
-      // tw + 16*s + col
-      h8 xop[2][NKBS];
+      for (int c = 0; c < CTH; ++c) acc_s[s][c] = (f4){0, 0, 0, 0};
 #pragma unroll
-      for (int s = 0; s < 2; ++s) {
-#pragma unroll
-        for (int kb = 0; kb < NKBS; ++kb) {
-          u4 v = (u4){0, 0, 0, 0};
-          const int c = 4 * kb + quad;
-          if (kb < kh.nkb && 8 * c < kh.rank) {
-            const uint8_t* cb = raw + kh.raw_code + s * 16 * kh.row_bytes;
-            if (QM == STARKV_Q_F16) {
-              v = *reinterpret_cast<const u4*>(cb + c * 256 + col * 16);
-            } else {
-              int gi;
-              if (c < kh.n8) gi = (8 * c) / 32;
-              else gi = kh.ng8 + (8 * (c - kh.n8)) / 32;
-              const uint32_t mz = *reinterpret_cast<const uint32_t*>(
-                  raw + kh.raw_meta + (s * kh.ngroups + gi) * 64 + col * 4);
-              const h2 sv = as_h2((mz & 0xFFFFu) * 0x10001u);
-              const h2 zv = as_h2((mz >> 16) * 0x10001u);
-              if (c < kh.n8) {
-                const u2 d = *reinterpret_cast<const u2*>(cb + c * 128 + col * 8);
-                v = deq_int8(d, sv, zv, sv, zv, sv, zv, sv, zv);
-              } else {
-                const uint32_t d = *reinterpret_cast<const uint32_t*>(
-                    cb + kh.n8 * 128 + (c - kh.n8) * 64 + col * 4);
-                v = deq_int4(d, sv, zv, sv, zv, sv, zv, sv, zv);
-              }
-            }
-          }
-          xop[s][kb] = __builtin_bit_cast(h8, v);
-        }
-      }
-      // score tile and column range of this KV head's query heads
-      const int ct_g = (gl * G) / 16;
-      const int c_lo = (gl * G) % 16;
-      const bool mine = col >= c_lo && col < c_lo + G;
-      const int il = ct_g * 16 + col;   // local query head of this lane's column
-#pragma unroll
-      for (int kbs = 0; kbs < NKBS; ++kbs) {
-        f4 k_lo[2], k_hi[2];
-#pragma unroll
-        for (int s = 0; s < 2; ++s) { k_lo[s] = (f4){0, 0, 0, 0}; k_hi[s] = (f4){0, 0, 0, 0}; }
-#pragma unroll
-        for (int kb = 0; kb < NKBS; ++kb) {
-          if (kb < kh.nkb) {
-            const h8 a_lo = frag[(kh.frag_base + kbs * kh.nkb + kb) * 64 + lane];
-            const h8 a_hi = frag[(kh.frag_base + (kbs + NKBS) * kh.nkb + kb) * 64 + lane];
-#pragma unroll
-            for (int s = 0; s < 2; ++s) {
-              k_lo[s] = mfma16(a_lo, xop[s][kb], k_lo[s]);
-              k_hi[s] = mfma16(a_hi, xop[s][kb], k_hi[s]);
-            }
-          }
-        }
-        // lane (tau = col, quad) holds k[j] and k[j + D/2] for j = 16*kbs + 4*quad + e
-        const h8 qf = *reinterpret_cast<const h8*>(
-            qc + (mine ? (il * D + (kbs * 4 + quad) * 8) : nql * D));
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          u4 kr;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float2 r = cs[s][4 * kbs + e];
-            const float a = k_lo[s][e], bb = k_hi[s][e];
-            const float ra = a * r.x - bb * r.y;
-            const float rb = bb * r.x + a * r.y;
-            kr[e] = as_u32((h2){(_Float16)ra, (_Float16)rb});
-          }
-          const h8 kop = __builtin_bit_cast(h8, kr);
-#pragma unroll
-          for (int c = 0; c < CT; ++c)
-            if (c == ct_g) acc_s[s][c] = mfma16(kop, qf, acc_s[s][c]);
-        }
+    for (int k = 1; k <= NKBS; ++k) {
+      const int o_end = p.cls[hg][hh][k];
+      for (int oi = p.cls[hg][hh][k - 1]; oi < o_end; ++oi) {
+        const int gg = p.order[oi];
+        if (k == 1) key_head<D, QM, CTH, 1>(p.kh[gg], raw, frag, qc, qzero, gg - g0, ct0, G, lane, col, quad, cs, acc_s);
+        if (k == 2) key_head<D, QM, CTH, 2>(p.kh[gg], raw, frag, qc, qzero, gg - g0, ct0, G, lane, col, quad, cs, acc_s);
+        if (NKBS > 2 && k == 3) key_head<D, QM, CTH, (NKBS > 2 ? 3 : 1)>(p.kh[gg], raw, frag, qc, qzero, gg - g0, ct0, G, lane, col, quad, cs, acc_s);
+        if (NKBS > 3 && k == 4) key_head<D, QM, CTH, (NKBS > 3 ? 4 : 1)>(p.kh[gg], raw, frag, qc, qzero, gg - g0, ct0, G, lane, col, quad, cs, acc_s);
       }
     }
-    // advance the rotations by one step
 #pragma unroll
     for (int f = 0; f < NF; ++f) {
-      cs[0][f] = cmul(cs[0][f], rot[f]);
-      cs[1][f] = cmul(cs[1][f], rot[f]);
+      const float2 r = rot_s[16 * (f / 4) + 4 * quad + (f % 4)];
+      cs[0][f] = cmul(cs[0][f], r);
+      cs[1][f] = cmul(cs[1][f], r);
     }
 
     // ------------------------------------------ online softmax (log2 domain)
-    float x[CT][2][4];
-    float mx[CT];
+    float x[CTH][2][4];
 #pragma unroll
-    for (int c = 0; c < CT; ++c) {
-      mx[c] = -INFINITY;
+    for (int c = 0; c < CTH; ++c) {
+      if (c >= ctn) break;
+      float mx = -INFINITY;
 #pragma unroll
       for (int s = 0; s < 2; ++s)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int t = tw + 16 * s + 4 * quad + e;
-          const float v = (t < t_end) ? acc_s[s][c][e] * sc : -INFINITY;
+          float v = acc_s[s][c][e] * sc;
+          if (!full && tw + 16 * s + 4 * quad + e >= t_end) v = -INFINITY;
           x[c][s][e] = v;
-          mx[c] = fmaxf(mx[c], v);
+          mx = fmaxf(mx, v);
         }
-      mx[c] = wave_max16(mx[c]);
-      if (quad == 0) red[(w * CT + c) * 16 + col] = mx[c];
+      mx = wave_max16(mx);
+      if (quad == 0) red[(tg * CT + ct0 + c) * 16 + col] = mx;
     }
-    __syncthreads();   // (1) tile maxima visible; previous step's value phase done
-    if (QM != STARKV_Q_F16) {
+    __syncthreads();   // (1) tile maxima visible
+    bool rescale = false;
 #pragma unroll
-      for (int i = 0; i < kMaxVMeta; ++i) {
-        const int off = (i * kThreads + tid) * 16;
-        if (off < vmeta_bytes) *reinterpret_cast<u4*>(vmeta + off) = vm[i];
-      }
-    }
-#pragma unroll
-    for (int c = 0; c < CT; ++c) {
+    for (int c = 0; c < CTH; ++c) {
+      if (c >= ctn) break;
+      const int ct = ct0 + c;
       float mn = m_run[c];
 #pragma unroll
-      for (int ww = 0; ww < kWaves; ++ww) mn = fmaxf(mn, red[(ww * CT + c) * 16 + col]);
-      const float al = exp2f(m_run[c] - mn);   // m_run = -inf on the first step: 0
+      for (int g = 0; g < kTokenGroups; ++g) mn = fmaxf(mn, red[(g * CT + ct) * 16 + col]);
+      const float al = __builtin_amdgcn_exp2f(m_run[c] - mn);   // m_run = -inf first: 0
+      rescale |= (mn != m_run[c]);
       m_run[c] = mn;
       u4 pk;
       float ls = 0.0f;
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        const _Float16 p0 = (_Float16)exp2f(x[c][k / 2][2 * (k % 2)] - mn);
-        const _Float16 p1 = (_Float16)exp2f(x[c][k / 2][2 * (k % 2) + 1] - mn);
+        const _Float16 p0 = (_Float16)__builtin_amdgcn_exp2f(x[c][k / 2][2 * (k % 2)] - mn);
+        const _Float16 p1 = (_Float16)__builtin_amdgcn_exp2f(x[c][k / 2][2 * (k % 2) + 1] - mn);
         ls += (float)p0 + (float)p1;
         pk[k] = as_u32((h2){p0, p1});
       }
       l_part[c] = l_part[c] * al + ls;
-      pbuf[(w * CT + c) * 64 + lane] = __builtin_bit_cast(h8, pk);
-      if (w == 0 && quad == 0) alpha_s[c * 16 + col] = al;
+      pbuf[(tg * CT + ct) * 64 + lane] = __builtin_bit_cast(h8, pk);
+      if (tg == 0 && quad == 0) alpha_s[ct * 16 + col] = al;
     }
-    __syncthreads();   // (2) probabilities, rescale factors and value meta visible
+    // waves of a half hold the same maxima, so their vote agrees; each half
+    // publishes its vote and every wave combines both
+    const bool any_rescale = __any(rescale);
+    if (tg == 0 && lane == 0) flag_s[hh] = any_rescale ? 1 : 0;
+    __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this wave's value copies landed
+    __syncthreads();   // (2) probabilities, rescale factors and the step's values visible
 
     // ------------------------------------------ values: acc += P . V'
+    if (flag_s[0] | flag_s[1]) {
 #pragma unroll
-    for (int c = 0; c < CT; ++c) {
-      const f4 al = *reinterpret_cast<const f4*>(alpha_s + c * 16 + 4 * quad);
+      for (int c = 0; c < CT; ++c) {
+        const f4 al = *reinterpret_cast<const f4*>(alpha_s + c * 16 + 4 * quad);
 #pragma unroll
-      for (int t = 0; t < NTW; ++t) acc_v[c][t] *= al;
+        for (int t = 0; t < NTW; ++t) acc_v[c][t] *= al;
+      }
     }
-    const bool full = (t_step + kStepTokens <= t_end);
 #pragma unroll
-    for (int ww = 0; ww < 4; ++ww) {
+    for (int ww = 0; ww < kTokenGroups; ++ww) {
       h8 pa[CT];
 #pragma unroll
       for (int c = 0; c < CT; ++c) pa[c] = pbuf[(ww * CT + c) * 64 + lane];
@@ -520,58 +580,69 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
           vmask[k] = (t0 < t_end ? 0x0000FFFFu : 0u) | (t0 + 1 < t_end ? 0xFFFF0000u : 0u);
         }
       }
+      const uint8_t* vb = vcode + ww * 32 * p.v_row_bytes;
 #pragma unroll
       for (int t = 0; t < NTW; ++t) {
         const int nt = w * NTW + t;
-        if (nt < NT) {
-          const int rho = 16 * nt + col;
-          u4 v;
-          if (QM == STARKV_Q_F16) {
-            v = (u4){vraw[ww][t][0], vraw[ww][t][1 % VW], vraw[ww][t][2 % VW],
-                     vraw[ww][t][3 % VW]};
+        if (nt >= NT) continue;
+        u4 v;
+        if (QM == STARKV_Q_F16) {
+          v = *reinterpret_cast<const u4*>(vb + v_off[t]);
+        } else {
+          const uint8_t* mb = vmeta + ((ww * p.v_ng + v_gi[t]) * 4 + quad) * 32;
+          const u4 sv = *reinterpret_cast<const u4*>(mb);
+          const u4 zv = *reinterpret_cast<const u4*>(mb + 16);
+          // a 16-channel tile is all 8-bit, all 4-bit, or (only when the outlier
+          // count is not a multiple of 16) mixed across lanes
+          const int lo_ch = 16 * nt, hi_ch = 16 * nt + 16;
+          if (QM == STARKV_Q_MIX8_4 && hi_ch <= p.v_ro) {
+            const u2 d = *reinterpret_cast<const u2*>(vb + v_off[t]);
+            v = deq_int8p(d, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y), as_h2(sv.z),
+                          as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
+          } else if (lo_ch >= p.v_ro) {
+            const uint32_t d = *reinterpret_cast<const uint32_t*>(vb + v_off[t]);
+            v = deq_int4(d, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y), as_h2(sv.z),
+                         as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
+          } else if (16 * nt + col < p.v_ro) {
+            const u2 d = *reinterpret_cast<const u2*>(vb + v_off[t]);
+            v = deq_int8p(d, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y), as_h2(sv.z),
+                          as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
           } else {
-            const int gi = rho < p.v_ro ? rho / 32 : p.v_ng8 + (rho - p.v_ro) / 32;
-            const uint8_t* mb = vmeta + ((ww * p.v_ng + gi) * 4 + quad) * 32;
-            const u4 sv = *reinterpret_cast<const u4*>(mb);
-            const u4 zv = *reinterpret_cast<const u4*>(mb + 16);
-            if (rho < p.v_ro) {
-              v = deq_int8((u2){vraw[ww][t][0], vraw[ww][t][(VW - 1) & 1]}, as_h2(sv.x),
-                           as_h2(zv.x), as_h2(sv.y), as_h2(zv.y), as_h2(sv.z), as_h2(zv.z),
-                           as_h2(sv.w), as_h2(zv.w));
-            } else {
-              v = deq_int4(vraw[ww][t][0], as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y),
-                           as_h2(sv.z), as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
-            }
+            const uint32_t d = *reinterpret_cast<const uint32_t*>(vb + v_off[t]);
+            v = deq_int4(d, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y), as_h2(sv.z),
+                         as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
           }
-          v &= vmask;
-          const h8 vop = __builtin_bit_cast(h8, v);
-#pragma unroll
-          for (int c = 0; c < CT; ++c) acc_v[c][t] = mfma16(pa[c], vop, acc_v[c][t]);
         }
+        if (!full) v &= vmask;
+        const h8 vop = __builtin_bit_cast(h8, v);
+#pragma unroll
+        for (int c = 0; c < CT; ++c) acc_v[c][t] = mfma16(pa[c], vop, acc_v[c][t]);
       }
     }
     if (step + 1 < n_steps) {
+      __syncthreads();   // every wave is done reading this step's values
       load_v(step + 1);
-      if (QM != STARKV_Q_F16) load_vm(step + 1);
     }
   }
 
   // ---------------------------------------------------------------- partials
 #pragma unroll
-  for (int c = 0; c < CT; ++c) {
+  for (int c = 0; c < CTH; ++c) {
+    if (c >= ctn) break;
     const float l = wave_sum16(l_part[c]);
-    if (quad == 0) red[(w * CT + c) * 16 + col] = l;
+    if (quad == 0) red[(tg * CT + ct0 + c) * 16 + col] = l;
   }
   __syncthreads();
   const int64_t pbase = ((int64_t)b * p.n_split + split) * p.n_q;
-  if (w == 0 && quad == 0) {
+  if (tg == 0 && quad == 0) {
 #pragma unroll
-    for (int c = 0; c < CT; ++c) {
-      const int il = c * 16 + col;
+    for (int c = 0; c < CTH; ++c) {
+      if (c >= ctn) break;
+      const int il = (ct0 + c) * 16 + col;
       if (il < nql) {
         float lt = 0.0f;
 #pragma unroll
-        for (int ww = 0; ww < kWaves; ++ww) lt += red[(ww * CT + c) * 16 + col];
+        for (int g = 0; g < kTokenGroups; ++g) lt += red[(g * CT + ct0 + c) * 16 + col];
         float* dst = p.part + (pbase + q0 + il) * p.part_stride + p.rv;
         dst[0] = m_run[c];
         dst[1] = lt;
@@ -595,10 +666,12 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 
 // ---------------------------------------------------------------------- combine
 #ifdef SK_COMMON
+// One workgroup per (query head, sequence).  Merges the splits with weights
+// 2^(m_s - M) and applies the value up-projection of the head's KV group.
 __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   extern __shared__ __align__(16) float sm[];
-  float* a = sm;                 // [rv]
-  float* wts = sm + p.rv;        // [n_split]
+  float* a = sm;                 // [rv] merged value latent
+  float* wts = sm + p.rv;        // [n_split] split weights
   float* red = wts + p.n_split;  // [256]
   const int i = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int D = p.head_dim;
@@ -613,44 +686,49 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   const int ns = (L + p.split_len - 1) / p.split_len;
   const float* part = p.part + ((int64_t)b * p.n_split * p.n_q + i) * p.part_stride;
   const int64_t sstride = (int64_t)p.n_q * p.part_stride;
-  // global maximum of the split maxima
-  float m = -INFINITY;
-  for (int s = tid; s < ns; s += 256) m = fmaxf(m, part[s * sstride + p.rv]);
-  red[tid] = m;
-  __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) {
-    if (tid < o) red[tid] = fmaxf(red[tid], red[tid + o]);
-    __syncthreads();
+  // split maxima and sums: the first wave holds up to 64 splits per lane pass
+  if (tid < 64) {
+    float m = -INFINITY;
+    for (int s = tid; s < ns; s += 64) m = fmaxf(m, part[s * sstride + p.rv]);
+    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    float l = 0.0f;
+    for (int s = tid; s < ns; s += 64) {
+      const float wv = __builtin_amdgcn_exp2f(part[s * sstride + p.rv] - m);
+      wts[s] = wv;
+      l += wv * part[s * sstride + p.rv + 1];
+    }
+    for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o);
+    if (tid == 0) red[0] = 1.0f / l;
   }
-  const float M = red[0];
   __syncthreads();
-  float lsum = 0.0f;
-  for (int s = tid; s < ns; s += 256) {
-    const float wv = exp2f(part[s * sstride + p.rv] - M);
-    wts[s] = wv;
-    lsum += wv * part[s * sstride + p.rv + 1];
-  }
-  red[tid] = lsum;
-  __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) {
-    if (tid < o) red[tid] += red[tid + o];
-    __syncthreads();
-  }
-  const float inv_l = 1.0f / red[0];
+  const float inv_l = red[0];
   for (int r = tid; r < p.rv; r += 256) {
-    float acc = 0.0f;
-    for (int s = 0; s < ns; ++s) acc += wts[s] * part[s * sstride + r];
-    a[r] = acc * inv_l;
+    float acc0 = 0.0f, acc1 = 0.0f, acc2 = 0.0f, acc3 = 0.0f;
+    int s = 0;
+    for (; s + 4 <= ns; s += 4) {
+      acc0 += wts[s] * part[s * sstride + r];
+      acc1 += wts[s + 1] * part[(s + 1) * sstride + r];
+      acc2 += wts[s + 2] * part[(s + 2) * sstride + r];
+      acc3 += wts[s + 3] * part[(s + 3) * sstride + r];
+    }
+    for (; s < ns; ++s) acc0 += wts[s] * part[s * sstride + r];
+    a[r] = ((acc0 + acc1) + (acc2 + acc3)) * inv_l;
   }
   __syncthreads();
-  // o = a . U_V^T restricted to KV head g's d columns (Sec. 3.3 reordering)
+  // o = a . U_V^T restricted to KV head g's d columns (the reordering of Sec. 3.3)
   const int nq4 = 256 / D;   // threads per output element
   const int j = tid % D, part_id = tid / D;
-  float acc = 0.0f;
-  for (int r = part_id; r < p.rv; r += nq4)
-    acc += a[r] * (float)__builtin_bit_cast(_Float16, p.bv[(int64_t)r * p.n_kv * D + g * D + j]);
+  const uint16_t* bv = p.bv + (int64_t)g * D + j;
+  const int64_t ldb = (int64_t)p.n_kv * D;
+  float o0 = 0.0f, o1 = 0.0f;
+  int r = part_id;
+  for (; r + nq4 < p.rv; r += 2 * nq4) {
+    o0 += a[r] * (float)__builtin_bit_cast(_Float16, bv[r * ldb]);
+    o1 += a[r + nq4] * (float)__builtin_bit_cast(_Float16, bv[(r + nq4) * ldb]);
+  }
+  for (; r < p.rv; r += nq4) o0 += a[r] * (float)__builtin_bit_cast(_Float16, bv[r * ldb]);
   __syncthreads();
-  red[tid] = acc;
+  red[tid] = o0 + o1;
   __syncthreads();
   if (tid < D) {
     float o = 0.0f;
@@ -718,8 +796,9 @@ int SK_NAME(SK_D, SK_QM)(const DecodeParams& p, int ct, int ntw, size_t lds, hip
   int launch_split_d##a##_q##b(const DecodeParams& p, int ct, int ntw, size_t lds, hipStream_t st);
 SK_DECL(64, 0) SK_DECL(64, 1) SK_DECL(64, 2) SK_DECL(128, 0) SK_DECL(128, 1) SK_DECL(128, 2)
 
-int split_lds_bytes(int frags, int nql, int head_dim, int ct, int raw_bytes, int v_ng) {
-  return split_lds(frags, nql, head_dim, ct, raw_bytes, v_ng).total;
+int split_lds_bytes(int frags, int nql, int head_dim, int ct, int raw_bytes, int v_ng,
+                    int v_row_bytes) {
+  return split_lds(frags, nql, head_dim, ct, raw_bytes, v_ng, kStepTokens * v_row_bytes).total;
 }
 
 int launch_decode_split_ntw(const DecodeParams& p, int head_dim, int qmode, int ct, int ntw,

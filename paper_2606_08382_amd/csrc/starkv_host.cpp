@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <algorithm>
 #include <new>
 #include <string>
 
@@ -59,7 +60,11 @@ struct starkv_plan {
   int32_t hg_first[STARKV_MAX_KV_HEADS + 1];
   int32_t hg_frags[STARKV_MAX_KV_HEADS];
   int32_t hg_raw[STARKV_MAX_KV_HEADS];
+  int32_t hg_mid[STARKV_MAX_KV_HEADS];
+  int32_t hh_raw[STARKV_MAX_KV_HEADS][2];
   KHeadInfo kh[STARKV_MAX_KV_HEADS];
+  int32_t order[STARKV_MAX_KV_HEADS];
+  int32_t cls[STARKV_MAX_KV_HEADS][2][5];
   int32_t lds_bytes;
 };
 
@@ -183,22 +188,33 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
     k.bk_row = bk_row;
     bk_row += k.rank;
   }
+  // A group of KV heads is processed by one workgroup in two halves split at a
+  // score-tile boundary (16 query heads); each half's key staging is per wave.
+  auto half_split = [&](int g_first, int g_last) {
+    const int tiles = ((g_last - g_first) * G + 15) / 16;
+    if (tiles < 2) return g_last;
+    return g_first + (((tiles + 1) / 2) * 16) / G;
+  };
+  auto raw_of = [&](int a, int b) {
+    int raw = 0;
+    for (int g = a; g < b; ++g) raw += 32 * P->kh[g].row_bytes + 2 * P->kh[g].ngroups * 64;
+    return raw;
+  };
   auto group_fits = [&](int g_first, int g_last, int ct, int* frags_out, int* raw_out) {
-    int frags = 0, raw = 0;
-    for (int g = g_first; g < g_last; ++g) {
-      frags += (D / 16) * P->kh[g].nkb;
-      raw += 32 * P->kh[g].row_bytes + 2 * P->kh[g].ngroups * 64;
-    }
+    int frags = 0;
+    for (int g = g_first; g < g_last; ++g) frags += (D / 16) * P->kh[g].nkb;
+    const int mid = half_split(g_first, g_last);
+    const int raw = std::max(raw_of(g_first, mid), raw_of(mid, g_last));
     *frags_out = frags;
     *raw_out = raw;
     const int nql = (g_last - g_first) * G;
     if (nql > 16 * ct) return false;
-    if (raw > 8 * 64 * 16) return false;   // kMaxLoads 16-byte loads per lane
-    return split_lds_bytes(frags, nql, D, ct, raw, L.value_groups) <= kLdsLimit;
+    if (raw > kMaxLoads * 64 * 16) return false;
+    return split_lds_bytes(frags, nql, D, ct, raw, L.value_groups, L.value_row_bytes) <= kLdsLimit;
   };
   int best_ct = -1;
   for (int ct : {1, 2, 4}) {
-    if (ct == 4 && ntw > 4) break;
+    if (ct * ntw > 16) continue;
     // greedy contiguous grouping at this tile count
     int n_hg = 0, g = 0;
     bool ok = true;
@@ -225,23 +241,43 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
   }
   P->ct = best_ct;
   P->lds_bytes = 0;
+  int pos = 0;
   for (int h = 0; h < P->n_hg; ++h) {
+    const int a = P->hg_first[h], b = P->hg_first[h + 1];
     int fr, rw;
-    group_fits(P->hg_first[h], P->hg_first[h + 1], P->ct, &fr, &rw);
+    group_fits(a, b, P->ct, &fr, &rw);
     P->hg_frags[h] = fr;
     P->hg_raw[h] = rw;
-    int fb = 0, ro = 0;
-    for (int g = P->hg_first[h]; g < P->hg_first[h + 1]; ++g) {
+    const int mid = half_split(a, b);
+    P->hg_mid[h] = mid;
+    P->hh_raw[h][0] = raw_of(a, mid);
+    P->hh_raw[h][1] = raw_of(mid, b);
+    int fb = 0;
+    for (int g = a; g < b; ++g) {
       KHeadInfo& k = P->kh[g];
       k.frag_base = fb;
       fb += (D / 16) * k.nkb;
-      k.raw_code = ro;
-      ro += 32 * k.row_bytes;
-      k.raw_meta = ro;
-      ro += 2 * k.ngroups * 64;
     }
-    const int nql = (P->hg_first[h + 1] - P->hg_first[h]) * G;
-    const int lds = split_lds_bytes(fr, nql, D, P->ct, rw, L.value_groups);
+    for (int half = 0; half < 2; ++half) {
+      const int ha = half ? mid : a, hb = half ? b : mid;
+      int ro = 0;
+      for (int g = ha; g < hb; ++g) {
+        KHeadInfo& k = P->kh[g];
+        k.raw_code = ro;
+        ro += 32 * k.row_bytes;
+        k.raw_meta = ro;
+        ro += 2 * k.ngroups * 64;
+      }
+      // processing order inside the half: heads sorted by k-block count
+      for (int kk = 1; kk <= 4; ++kk) {
+        P->cls[h][half][kk - 1] = pos;
+        for (int g = ha; g < hb; ++g)
+          if (P->kh[g].nkb == kk) P->order[pos++] = g;
+      }
+      P->cls[h][half][4] = pos;
+    }
+    const int nql = (b - a) * G;
+    const int lds = split_lds_bytes(fr, nql, D, P->ct, rw, L.value_groups, L.value_row_bytes);
     if (lds > P->lds_bytes) P->lds_bytes = lds;
   }
   *out = P;
@@ -348,7 +384,11 @@ starkv_status starkv_decode_split(const starkv_plan* P, const void* cache, const
   std::memcpy(p.hg_first, P->hg_first, sizeof(p.hg_first));
   std::memcpy(p.hg_frags, P->hg_frags, sizeof(p.hg_frags));
   std::memcpy(p.hg_raw_bytes, P->hg_raw, sizeof(p.hg_raw_bytes));
+  std::memcpy(p.hg_mid, P->hg_mid, sizeof(p.hg_mid));
+  std::memcpy(p.hh_raw, P->hh_raw, sizeof(p.hh_raw));
   std::memcpy(p.kh, P->kh, sizeof(p.kh));
+  std::memcpy(p.order, P->order, sizeof(p.order));
+  std::memcpy(p.cls, P->cls, sizeof(p.cls));
   const int e = launch_decode_split_ntw(p, c.head_dim, c.qmode, P->ct, P->ntw, P->lds_bytes,
                                         static_cast<void*>(stream));
   return hip_status(e, "decode_split launch");

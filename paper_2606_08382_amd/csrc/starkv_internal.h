@@ -7,11 +7,11 @@
 
 namespace starkv {
 
-constexpr int kWaves = 4;                 // waves per decode workgroup
+constexpr int kTokenGroups = 4;          // token groups of a decode workgroup step
+constexpr int kWaves = 2 * kTokenGroups;  // waves: token group x half of the KV heads
 constexpr int kThreads = 64 * kWaves;
 constexpr int kWaveTokens = 32;           // tokens per wave per step (two 16-token subtiles)
-constexpr int kStepTokens = kWaves * kWaveTokens;
-constexpr int kMaxSeg = 2 * STARKV_MAX_KV_HEADS;
+constexpr int kStepTokens = kTokenGroups * kWaveTokens;
 
 // One key head as seen by the split kernel (all offsets in bytes).
 struct KHeadInfo {
@@ -25,8 +25,8 @@ struct KHeadInfo {
   int32_t row_bytes;
   int32_t bk_row;        // first row of this head in B_k
   int32_t frag_base;     // first 1 KiB up-projection fragment of this head in LDS
-  int32_t raw_code;      // offset of this head's codes in a wave's LDS staging area
-  int32_t raw_meta;      // offset of this head's meta in a wave's LDS staging area
+  int32_t raw_code;      // offset of this head's codes in its wave's LDS staging area
+  int32_t raw_meta;      // offset of this head's meta in its wave's LDS staging area
 };
 
 struct DecodeParams {
@@ -45,12 +45,19 @@ struct DecodeParams {
   int64_t v_code_off, v_meta_off;
   int32_t rv, v_ro, v_ng8, v_ng, v_row_bytes;
   int32_t part_stride;         // floats per (b, split, query head)
-  // head groups (blockIdx.z)
+  // head groups (blockIdx.z); each group is processed in two halves split at a
+  // score-tile boundary (16 query heads), one half per wave of a token group
   int32_t n_hg;
   int32_t hg_first[STARKV_MAX_KV_HEADS + 1];
+  int32_t hg_mid[STARKV_MAX_KV_HEADS];       // first KV head of the second half
   int32_t hg_frags[STARKV_MAX_KV_HEADS];     // fragments used by the group
-  int32_t hg_raw_bytes[STARKV_MAX_KV_HEADS]; // per-wave staging bytes used by the group
+  int32_t hg_raw_bytes[STARKV_MAX_KV_HEADS]; // per-wave staging bytes (max over halves)
+  int32_t hh_raw[STARKV_MAX_KV_HEADS][2];    // staging bytes of each half
   KHeadInfo kh[STARKV_MAX_KV_HEADS];
+  // heads of every half in processing order, grouped by k-block count:
+  // order[cls[hg][h][k-1] .. cls[hg][h][k]) are the half's heads with k k-blocks
+  int32_t order[STARKV_MAX_KV_HEADS];
+  int32_t cls[STARKV_MAX_KV_HEADS][2][5];
 };
 
 struct CombineParams {
@@ -93,9 +100,11 @@ struct DownprojParams {
 };
 
 // launchers (return hipError_t as int)
-int split_lds_bytes(int frags, int nql, int head_dim, int ct, int raw_bytes, int v_ng);
+int split_lds_bytes(int frags, int nql, int head_dim, int ct, int raw_bytes, int v_ng,
+                    int v_row_bytes);
 int launch_decode_split_ntw(const DecodeParams& p, int head_dim, int qmode, int ct, int ntw,
                             size_t lds_bytes, void* stream);
+constexpr int kMaxLoads = 4;   // 16-byte key-staging loads per lane per step
 int launch_decode_combine(const CombineParams& p, void* stream);
 int launch_append_pack(const AppendParams& p, void* stream);
 int launch_downproj(const DownprojParams& p, void* stream);
