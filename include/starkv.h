@@ -186,7 +186,8 @@ starkv_status starkv_append(const starkv_plan* plan, void* cache, const void* x_
  *   ctx_len_dev  device int32 [B]: sequence b attends to rows [0, ctx_len[b]);
  *                key t is rotated by RoPE at position t.  Values are clamped to
  *                [0, max_ctx]; 0 gives a zero output.
- *   max_ctx      host upper bound of ctx_len, 1 <= max_ctx <= capacity.
+ *   max_ctx      host upper bound of ctx_len, 1 <= max_ctx <= capacity, and at most
+ *                524288 (64 context splits of at most 8192 tokens; UNSUPPORTED beyond).
  *   out          device [B][H_q][d] in out_dtype, 16-byte aligned.
  *   ws           device, starkv_decode_workspace_bytes(plan, max_ctx) bytes,
  *                256-byte aligned.

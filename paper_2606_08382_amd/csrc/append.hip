@@ -68,116 +68,135 @@ __device__ __forceinline__ uint32_t group_code(const GroupQ& g, uint16_t x) {
 }
 
 // ------------------------------------------------------------------ pack kernel
-// One thread per (sequence b, 32-token block touched, chunk q of that block,
-// (latent block, group) item).  The thread handles the eight tokens of value
-// chunk q (4q..4q+3, 16+4q..16+4q+3), so every 32-bit value word is owned by
-// exactly one thread; tokens outside [pos, pos+n_new) keep their old bits.
+// One wave per (new token, quantization group); lane i holds channel c0 + i of
+// the group (at most 32 lanes are active).  The group's min and max come from
+// wave reductions, the scale and the codes from fp64 arithmetic per lane, and
+// the codes are packed into the cache words with shuffles.  Value 4-bit words
+// hold eight tokens of one channel, so a token updates its nibble with an
+// atomic AND/OR pair: tokens of one launch touch disjoint nibbles.
+// When the latents come from the down-projection, the lane first sums the
+// split-k partial products (fixed order) and stores the fp16 latent.
+
+__device__ __forceinline__ float wave_min32(float v) {
+  for (int o = 16; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ float wave_max32(float v) {
+  for (int o = 16; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
 
 __global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
-  const int item = blockIdx.x * blockDim.x + threadIdx.x;
-  if (item >= p.n_items) return;
-  const int kq = blockIdx.y & 3;
-  const int bj = blockIdx.y >> 2;           // block index within the touched range
-  const int b = blockIdx.z;
-  const int pos = p.pos[b];
-  const int blk = (pos >= 0 ? pos / 32 : -((31 - pos) / 32)) + bj;
-  const int blk_end = (pos + p.n_new - 1 >= 0) ? (pos + p.n_new - 1) / 32 : -1;
-  if (blk > blk_end || blk < 0) return;
+  const int lane = threadIdx.x & 63;
+  const int wid = blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
+  const int n_tok = p.batch * p.n_new;
+  if (wid >= n_tok * p.n_items) return;
+  const int tok = wid / p.n_items, item = wid % p.n_items;
+  const int b = tok / p.n_new, j = tok % p.n_new;
+  const int t = p.pos[b] + j;
   const int bl = p.item_block[item], gi = p.item_group[item];
   const int r = p.rank[bl], ro = p.ro[bl];
   const bool is_v = (bl == p.n_kv);
-  const int qm = p.qmode;
-  // group channel range and bit width
   int c0, n, bits;
-  if (qm == STARKV_Q_F16) {
+  if (p.qmode == STARKV_Q_F16) {
     c0 = 32 * gi; n = min(32, r - c0); bits = 16;
   } else {
     const int ng8 = (ro + 31) / 32;
     if (gi < ng8) { c0 = 32 * gi; n = min(32, ro - c0); bits = 8; }
     else { c0 = ro + 32 * (gi - ng8); n = min(32, r - c0); bits = 4; }
   }
+  const bool on = lane < n;
+  const int c = c0 + lane;
+  const int64_t li = (int64_t)tok * p.width + p.lat_off[bl] + c;
+  uint16_t xb = 0;
+  if (on) {
+    if (p.partial) {
+      const int64_t mn = (int64_t)n_tok * p.width;
+      float acc = 0.0f;
+      for (int k = 0; k < p.k_split; ++k) acc += p.partial[k * mn + li];
+      xb = __builtin_bit_cast(uint16_t, (_Float16)acc);
+      p.lat_out[li] = xb;
+    } else {
+      xb = p.lat[li];
+    }
+  }
+  if (t < 0 || t >= p.capacity) return;     // rows outside the cache are dropped
   uint8_t* code_plane = p.cache + p.code_off[bl];
   uint8_t* meta_plane = p.cache + p.meta_off[bl];
   const int rb = p.row_bytes[bl];
   const int ngr = p.ng[bl];
-  uint32_t words[32];                        // value 4-bit chunk words, one per channel
-  bool have_words = false;
-  const int64_t vblk = (int64_t)b * (p.cap_pad / 32) + blk;
-  uint8_t* vblock = code_plane + vblk * 32 * rb;
-  const int ri = r - ro;
-
-  for (int slot = 0; slot < 8; ++slot) {
-    const int u = (slot < 4) ? (4 * kq + slot) : (16 + 4 * kq + slot - 4);
-    const int t = blk * 32 + u;
-    if (t < pos || t >= pos + p.n_new || t >= p.capacity) continue;
-    const uint16_t* x = p.lat + ((int64_t)b * p.n_new + (t - pos)) * p.width + p.lat_off[bl] + c0;
-    if (!is_v) {
-      const int64_t kblk = (int64_t)b * (p.cap_pad / 16) + t / 16;
-      const int tau = t % 16;
-      uint8_t* kb = code_plane + kblk * 16 * rb;
-      if (bits == 16) {
-        for (int i = 0; i < n; ++i) {
-          const int c = c0 + i;
-          *reinterpret_cast<uint16_t*>(kb + (c / 8) * 256 + tau * 16 + (c % 8) * 2) = x[i];
-        }
-        continue;
+  const int64_t kblk = (int64_t)b * (p.cap_pad / 16) + t / 16;
+  const int tau = t % 16;
+  const int64_t vblk = (int64_t)b * (p.cap_pad / 32) + t / 32;
+  const int u = t % 32, kq = (u % 16) / 4, slot = 4 * (u / 16) + u % 4;
+  if (bits == 16) {
+    if (on) {
+      if (!is_v)
+        *reinterpret_cast<uint16_t*>(code_plane + kblk * 16 * rb + (c / 8) * 256 + tau * 16 + (c % 8) * 2) = xb;
+      else
+        *reinterpret_cast<uint16_t*>(code_plane + vblk * 32 * rb + ((int64_t)c * 4 + kq) * 16 + slot * 2) = xb;
+    }
+    return;
+  }
+  // group parameters (the fp16 values compare exactly in fp32)
+  const float xf = (float)__builtin_bit_cast(_Float16, xb);
+  const float lo = wave_min32(on ? xf : INFINITY);
+  const float hi = wave_max32(on ? xf : -INFINITY);
+  const double levels = (double)((1 << bits) - 1);
+  const uint16_t s16 = (hi > lo) ? f16_ceil_pos(((double)hi - (double)lo) / levels) : (uint16_t)0;
+  const uint16_t z16 = __builtin_bit_cast(uint16_t, (_Float16)lo);
+  const double sv = h2d(s16);
+  uint32_t code = 0;
+  if (sv != 0.0) {
+    double q = rint(((double)xf - (double)lo) / sv);
+    q = q < 0.0 ? 0.0 : (q > levels ? levels : q);
+    code = (uint32_t)q;
+  }
+  if (!on) code = 0;
+  if (!is_v) {
+    uint8_t* kb = code_plane + kblk * 16 * rb;
+    const int n8 = ro / 8;
+    if (bits == 8) {          // 4 codes per 32-bit word, lanes 4k..4k+3
+      uint32_t wv = code << (8 * (lane & 3));
+      wv |= __shfl_xor(wv, 1);
+      wv |= __shfl_xor(wv, 2);
+      if (on && (lane & 3) == 0) {
+        const int ch = c / 8;
+        *reinterpret_cast<uint32_t*>(kb + ch * 128 + tau * 8 + (c % 8)) = wv;
       }
-      const GroupQ g = group_params(x, n, bits);
-      const int n8 = ro / 8;
-      for (int i = 0; i < n; i += 8) {         // one chunk of 8 channels at a time
-        const int c = c0 + i, ch = c / 8;
-        if (bits == 8) {
-          uint32_t lo = 0, hi = 0;
-          for (int k = 0; k < 4; ++k) lo |= group_code(g, x[i + k]) << (8 * k);
-          for (int k = 0; k < 4; ++k) hi |= group_code(g, x[i + 4 + k]) << (8 * k);
-          uint32_t* dst = reinterpret_cast<uint32_t*>(kb + ch * 128 + tau * 8);
-          dst[0] = lo;
-          dst[1] = hi;
-        } else {
-          uint32_t wv = 0;
-          for (int k = 0; k < 8; ++k) wv |= group_code(g, x[i + k]) << (4 * k);
-          *reinterpret_cast<uint32_t*>(kb + n8 * 128 + (ch - n8) * 64 + tau * 4) = wv;
-        }
+    } else {                  // 8 codes per word, lanes 8k..8k+7, channel w at nibble w
+      uint32_t wv = code << (4 * (lane & 7));
+      wv |= __shfl_xor(wv, 1);
+      wv |= __shfl_xor(wv, 2);
+      wv |= __shfl_xor(wv, 4);
+      if (on && (lane & 7) == 0) {
+        const int ch = c / 8;
+        *reinterpret_cast<uint32_t*>(kb + n8 * 128 + (ch - n8) * 64 + tau * 4) = wv;
       }
+    }
+    if (lane == 0) {
       uint16_t* m = reinterpret_cast<uint16_t*>(meta_plane + (kblk * ngr + gi) * 64 + tau * 4);
-      m[0] = g.s;
-      m[1] = g.z;
-    } else {
-      if (bits == 16) {
-        for (int i = 0; i < n; ++i) {
-          const int c = c0 + i;
-          *reinterpret_cast<uint16_t*>(vblock + ((int64_t)c * 4 + kq) * 16 + slot * 2) = x[i];
-        }
-        continue;
-      }
-      const GroupQ g = group_params(x, n, bits);
+      m[0] = s16;
+      m[1] = z16;
+    }
+  } else {
+    uint8_t* vb = code_plane + vblk * 32 * rb;
+    if (on) {
       if (bits == 8) {
-        for (int i = 0; i < n; ++i) {
-          const int c = c0 + i;
-          vblock[((int64_t)c * 4 + kq) * 8 + slot] = (uint8_t)group_code(g, x[i]);
-        }
+        vb[((int64_t)c * 4 + kq) * 8 + slot] = (uint8_t)code;
       } else {
-        if (!have_words) {
-          for (int i = 0; i < n; ++i)
-            words[i] = *reinterpret_cast<const uint32_t*>(
-                vblock + 32 * ro + ((int64_t)(c0 - ro + i) * 4 + kq) * 4);
-          have_words = true;
-        }
         // slot 2k -> bits 4k..4k+3, slot 2k+1 -> bits 16+4k..16+4k+3
         const int sh = (slot % 2 == 0) ? 4 * (slot / 2) : 16 + 4 * (slot / 2);
-        for (int i = 0; i < n; ++i)
-          words[i] = (words[i] & ~(0xFu << sh)) | (group_code(g, x[i]) << sh);
+        unsigned int* wp = reinterpret_cast<unsigned int*>(vb + 32 * ro + ((int64_t)(c - ro) * 4 + kq) * 4);
+        atomicAnd(wp, ~(0xFu << sh));
+        atomicOr(wp, code << sh);
       }
-      uint16_t* m = reinterpret_cast<uint16_t*>(meta_plane +
-                                                (vblk * ngr + gi) * 128 + kq * 32 + slot * 2);
-      m[0] = g.s;
-      m[8] = g.z;
     }
-  }
-  if (have_words) {
-    for (int i = 0; i < n; ++i)
-      *reinterpret_cast<uint32_t*>(vblock + 32 * ro + ((int64_t)(c0 - ro + i) * 4 + kq) * 4) =
-          words[i];
+    if (lane == 0) {
+      uint16_t* m = reinterpret_cast<uint16_t*>(meta_plane + (vblk * ngr + gi) * 128 + kq * 32 + slot * 2);
+      m[0] = s16;
+      m[8] = z16;
+    }
   }
 }
 
@@ -244,32 +263,17 @@ __global__ __launch_bounds__(256) void downproj_kernel(DownprojParams p) {
       }
 }
 
-__global__ __launch_bounds__(256) void downproj_reduce_kernel(DownprojParams p) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t mn = (int64_t)p.m * p.n;
-  if (i >= mn) return;
-  float s = 0.0f;
-  for (int k = 0; k < p.k_split; ++k) s += p.partial[k * mn + i];
-  p.lat[i] = __builtin_bit_cast(uint16_t, (_Float16)s);
-}
-
 // ------------------------------------------------------------------ launchers
 int launch_append_pack(const AppendParams& p, void* stream) {
-  const int nblk = p.n_new / 32 + 2;          // 32-token blocks a range of n_new rows can touch
-  dim3 grid((p.n_items + 63) / 64, nblk * 4, p.batch);
-  hipLaunchKernelGGL(pack_kernel, grid, dim3(64), 0, static_cast<hipStream_t>(stream), p);
+  const int64_t waves = (int64_t)p.batch * p.n_new * p.n_items;
+  dim3 grid((unsigned)((waves + 3) / 4));
+  hipLaunchKernelGGL(pack_kernel, grid, dim3(256), 0, static_cast<hipStream_t>(stream), p);
   return (int)hipGetLastError();
 }
 
 int launch_downproj(const DownprojParams& p, void* stream) {
-  hipStream_t st = static_cast<hipStream_t>(stream);
   dim3 grid((p.n + BN - 1) / BN, (p.m + BM - 1) / BM, p.k_split);
-  hipLaunchKernelGGL(downproj_kernel, grid, dim3(256), 0, st, p);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return (int)e;
-  const int64_t mn = (int64_t)p.m * p.n;
-  hipLaunchKernelGGL(downproj_reduce_kernel, dim3((unsigned)((mn + 255) / 256)), dim3(256), 0, st,
-                     p);
+  hipLaunchKernelGGL(downproj_kernel, grid, dim3(256), 0, static_cast<hipStream_t>(stream), p);
   return (int)hipGetLastError();
 }
 

@@ -667,12 +667,16 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 // ---------------------------------------------------------------------- combine
 #ifdef SK_COMMON
 // One workgroup per (query head, sequence).  Merges the splits with weights
-// 2^(m_s - M) and applies the value up-projection of the head's KV group.
+// 2^(m_s - M) and applies the value up-projection of the head's KV group.  All
+// loads of a phase are issued before their results are used, so each phase
+// costs about one memory round trip.
+constexpr int kCombineMaxSplits = 64;
+
 __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   extern __shared__ __align__(16) float sm[];
-  float* a = sm;                 // [rv] merged value latent
-  float* wts = sm + p.rv;        // [n_split] split weights
-  float* red = wts + p.n_split;  // [256]
+  float* a = sm;                  // [rv] merged value latent
+  float* wts = sm + p.rv;         // [n_split] split weights
+  float* red = wts + p.n_split;   // [16][D] partial up-projections
   const int i = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int D = p.head_dim;
   const int g = (int)(((int64_t)i * p.n_kv) / p.n_q);
@@ -686,16 +690,22 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   const int ns = (L + p.split_len - 1) / p.split_len;
   const float* part = p.part + ((int64_t)b * p.n_split * p.n_q + i) * p.part_stride;
   const int64_t sstride = (int64_t)p.n_q * p.part_stride;
-  // split maxima and sums: the first wave holds up to 64 splits per lane pass
-  if (tid < 64) {
+  if (tid < 64) {                 // split weights: one wave, up to 64 splits per lane pass
+    float mv[kCombineMaxSplits / 64 + 1], lv[kCombineMaxSplits / 64 + 1];
     float m = -INFINITY;
-    for (int s = tid; s < ns; s += 64) m = fmaxf(m, part[s * sstride + p.rv]);
+    int k = 0;
+    for (int s = tid; s < ns; s += 64, ++k) {
+      mv[k] = part[s * sstride + p.rv];
+      lv[k] = part[s * sstride + p.rv + 1];
+      m = fmaxf(m, mv[k]);
+    }
     for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
     float l = 0.0f;
-    for (int s = tid; s < ns; s += 64) {
-      const float wv = __builtin_amdgcn_exp2f(part[s * sstride + p.rv] - m);
+    k = 0;
+    for (int s = tid; s < ns; s += 64, ++k) {
+      const float wv = __builtin_amdgcn_exp2f(mv[k] - m);
       wts[s] = wv;
-      l += wv * part[s * sstride + p.rv + 1];
+      l += wv * lv[k];
     }
     for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o);
     if (tid == 0) red[0] = 1.0f / l;
@@ -703,43 +713,56 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   __syncthreads();
   const float inv_l = red[0];
   for (int r = tid; r < p.rv; r += 256) {
-    float acc0 = 0.0f, acc1 = 0.0f, acc2 = 0.0f, acc3 = 0.0f;
-    int s = 0;
-    for (; s + 4 <= ns; s += 4) {
-      acc0 += wts[s] * part[s * sstride + r];
-      acc1 += wts[s + 1] * part[(s + 1) * sstride + r];
-      acc2 += wts[s + 2] * part[(s + 2) * sstride + r];
-      acc3 += wts[s + 3] * part[(s + 3) * sstride + r];
-    }
-    for (; s < ns; ++s) acc0 += wts[s] * part[s * sstride + r];
-    a[r] = ((acc0 + acc1) + (acc2 + acc3)) * inv_l;
+    float v[kCombineMaxSplits];
+#pragma unroll
+    for (int s = 0; s < kCombineMaxSplits; ++s)
+      if (s < ns) v[s] = part[s * sstride + r];
+    float acc = 0.0f;
+#pragma unroll
+    for (int s = 0; s < kCombineMaxSplits; ++s)
+      if (s < ns) acc += wts[s] * v[s];
+    a[r] = acc * inv_l;
   }
   __syncthreads();
-  // o = a . U_V^T restricted to KV head g's d columns (the reordering of Sec. 3.3)
-  const int nq4 = 256 / D;   // threads per output element
-  const int j = tid % D, part_id = tid / D;
-  const uint16_t* bv = p.bv + (int64_t)g * D + j;
+  // o = a . U_V^T restricted to KV head g's d columns (the reordering of Sec. 3.3):
+  // thread (rg, j8) covers rows rg, rg+16, .. and columns 8*j8..8*j8+7
+  const int j8n = D / 8;                 // 16 (D = 128) or 8 (D = 64)
+  const int groups = 256 / j8n;          // row groups
+  const int j8 = tid % j8n, rg = tid / j8n;
   const int64_t ldb = (int64_t)p.n_kv * D;
-  float o0 = 0.0f, o1 = 0.0f;
-  int r = part_id;
-  for (; r + nq4 < p.rv; r += 2 * nq4) {
-    o0 += a[r] * (float)__builtin_bit_cast(_Float16, bv[r * ldb]);
-    o1 += a[r + nq4] * (float)__builtin_bit_cast(_Float16, bv[(r + nq4) * ldb]);
+  const uint16_t* bv = p.bv + (int64_t)g * D + 8 * j8;
+  float o[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (int r0 = rg; r0 < p.rv; r0 += 8 * groups) {
+    u4 w8[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int r = r0 + k * groups;
+      if (r < p.rv) w8[k] = *reinterpret_cast<const u4*>(bv + r * ldb);
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int r = r0 + k * groups;
+      if (r < p.rv) {
+        const _Float16* hw = reinterpret_cast<const _Float16*>(&w8[k]);
+        const float ar = a[r];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] += ar * (float)hw[e];
+      }
+    }
   }
-  for (; r < p.rv; r += nq4) o0 += a[r] * (float)__builtin_bit_cast(_Float16, bv[r * ldb]);
-  __syncthreads();
-  red[tid] = o0 + o1;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) red[rg * D + 8 * j8 + e] = o[e];
   __syncthreads();
   if (tid < D) {
-    float o = 0.0f;
-    for (int k = 0; k < nq4; ++k) o += red[k * D + tid];
+    float ov = 0.0f;
+    for (int k = 0; k < groups; ++k) ov += red[k * D + tid];
     uint16_t bits;
     if (p.out_bf16) {
-      const uint32_t u = __float_as_uint(o);
+      const uint32_t u = __float_as_uint(ov);
       bits = (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
       if ((u & 0x7F800000u) == 0x7F800000u) bits = (uint16_t)(u >> 16) | ((u & 0xFFFFu) ? 0x40 : 0);
     } else {
-      bits = __builtin_bit_cast(uint16_t, (_Float16)o);
+      bits = __builtin_bit_cast(uint16_t, (_Float16)ov);
     }
     out[tid] = bits;
   }
@@ -821,7 +844,8 @@ int launch_decode_split_ntw(const DecodeParams& p, int head_dim, int qmode, int 
 }
 
 int launch_decode_combine(const CombineParams& p, void* stream) {
-  const size_t lds = (size_t)(p.rv + p.n_split + 256) * sizeof(float);
+  if (p.n_split > kCombineMaxSplits) return (int)hipErrorInvalidValue;
+  const size_t lds = (size_t)(p.rv + p.n_split + 32 * p.head_dim) * sizeof(float);
   dim3 grid(p.n_q, p.batch);
   hipLaunchKernelGGL(decode_combine_kernel, grid, dim3(256), lds,
                      static_cast<hipStream_t>(stream), p);

@@ -47,6 +47,8 @@ int row_bytes(int qmode, int r) {
 }
 
 constexpr int kLdsLimit = 160 * 1024;
+constexpr int kMaxSplits = 64;          // context splits per sequence merged by the combine pass
+constexpr int kMaxSplitTokens = 8192;   // tokens per split (bounds the RoPE rotation recurrence)
 
 }  // namespace
 
@@ -301,13 +303,14 @@ starkv_status starkv_cache_layout(const starkv_plan* plan, starkv_layout* out) {
 
 int32_t starkv_decode_split_tokens(const starkv_plan* P, int32_t max_ctx) {
   if (!P || max_ctx < 1) return 0;
-  // enough splits to give every compute unit a workgroup
+  // enough splits to give every compute unit a workgroup, at most kMaxSplits
+  // per sequence (the combine pass merges up to that many)
   const int64_t wgs_per_split = (int64_t)P->cfg.batch * P->n_hg;
   int64_t splits = (256 + wgs_per_split - 1) / wgs_per_split;
+  if (splits > kMaxSplits) splits = kMaxSplits;
   int64_t len = ((int64_t)max_ctx + splits - 1) / splits;
   len = (len + kStepTokens - 1) / kStepTokens * kStepTokens;
   if (len < kStepTokens) len = kStepTokens;
-  if (len > 8192) len = 8192;
   return (int32_t)len;
 }
 
@@ -331,6 +334,8 @@ static starkv_status check_common(const starkv_plan* P, int32_t max_ctx, size_t 
   if (max_ctx < 1) return fail(STARKV_ERR_INVALID_ARG, "max_ctx %d < 1", max_ctx);
   if (max_ctx > P->cfg.capacity)
     return fail(STARKV_ERR_CAPACITY, "max_ctx %d > capacity %d", max_ctx, P->cfg.capacity);
+  if (starkv_decode_split_tokens(P, max_ctx) > kMaxSplitTokens)
+    return fail(STARKV_ERR_UNSUPPORTED, "max_ctx %d > %d", max_ctx, kMaxSplits * kMaxSplitTokens);
   const size_t need = starkv_decode_workspace_bytes(P, max_ctx);
   if (!ws || ws_bytes < need)
     return fail(STARKV_ERR_WORKSPACE, "decode workspace %zu bytes < %zu", ws_bytes, need);
@@ -470,6 +475,9 @@ starkv_status starkv_append(const starkv_plan* P, void* cache, const void* x_or_
     return fail(STARKV_ERR_ALIGNMENT, "ws not 256-byte aligned");
   if ((int64_t)c.batch * n_new > (1 << 24)) return fail(STARKV_ERR_UNSUPPORTED, "too many new tokens");
   const uint16_t* lat = static_cast<const uint16_t*>(x_or_latents);
+  const float* partial = nullptr;
+  uint16_t* lat_out = nullptr;
+  int k_split = 0;
   if (c.d_model > 0) {
     if (reinterpret_cast<uintptr_t>(x_or_latents) % 16)
       return fail(STARKV_ERR_ALIGNMENT, "x not 16-byte aligned");
@@ -490,7 +498,10 @@ starkv_status starkv_append(const starkv_plan* P, void* cache, const void* x_or_
     d.x_bf16 = 1;
     starkv_status st = hip_status(launch_downproj(d, static_cast<void*>(stream)), "downproj launch");
     if (st != STARKV_OK) return st;
-    lat = d.lat;
+    lat = nullptr;
+    partial = d.partial;
+    lat_out = d.lat;
+    k_split = ks;
   } else if (reinterpret_cast<uintptr_t>(x_or_latents) % 2) {
     return fail(STARKV_ERR_ALIGNMENT, "latents not 2-byte aligned");
   }
@@ -498,6 +509,9 @@ starkv_status starkv_append(const starkv_plan* P, void* cache, const void* x_or_
   std::memset(&a, 0, sizeof(a));
   a.cache = static_cast<uint8_t*>(cache);
   a.lat = lat;
+  a.partial = partial;
+  a.lat_out = lat_out;
+  a.k_split = k_split;
   a.pos = pos_dev;
   a.batch = c.batch;
   a.n_new = n_new;

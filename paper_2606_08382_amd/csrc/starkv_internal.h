@@ -35,6 +35,7 @@ struct DecodeParams {
   const uint16_t* bk;
   const int32_t* ctx_len;
   float* part;                 // split partials
+  float2* cand;                // per (b, split, query head): kCand (score, token) candidates
   int32_t batch, n_q, n_kv, group_q;   // group_q = H_q / H_kv
   int32_t cap_pad;             // Cp
   int32_t max_ctx, split_len, n_split;
@@ -60,19 +61,36 @@ struct DecodeParams {
   int32_t cls[STARKV_MAX_KV_HEADS][2][5];
 };
 
+constexpr int kCand = 32;      // rescoring candidates per (sequence, split, query head)
+
 struct CombineParams {
   const float* part;
+  const float2* cand;
   const uint16_t* bv;
+  const uint16_t* bk;
+  const uint8_t* cache;
+  const void* q;
   const int32_t* ctx_len;
   void* out;
   int32_t batch, n_q, n_kv, head_dim, rv;
   int32_t max_ctx, split_len, n_split, part_stride;
-  int32_t out_bf16;
+  int32_t out_bf16, q_bf16, qmode, cap_pad;
+  float score_scale;
+  double log2_theta;
+  // key head of this query head's group and the value latent (cache layout)
+  int64_t k_code_off[STARKV_MAX_KV_HEADS], k_meta_off[STARKV_MAX_KV_HEADS];
+  int32_t k_rank[STARKV_MAX_KV_HEADS], k_ro[STARKV_MAX_KV_HEADS], k_ng[STARKV_MAX_KV_HEADS];
+  int32_t k_rb[STARKV_MAX_KV_HEADS], k_bkrow[STARKV_MAX_KV_HEADS];
+  int64_t v_code_off, v_meta_off;
+  int32_t v_ro, v_ng, v_rb;
 };
 
 struct AppendParams {
   uint8_t* cache;
-  const uint16_t* lat;         // fp16 latents [B][n_new][width]
+  const uint16_t* lat;         // fp16 latents [B][n_new][width] (when partial == NULL)
+  const float* partial;        // down-projection split-k partials [k_split][B*n_new][width]
+  uint16_t* lat_out;           // fp16 latents written when summing partials
+  int32_t k_split;
   const int32_t* pos;
   int32_t batch, n_new, width, capacity, cap_pad, qmode;
   int32_t n_kv;
