@@ -109,7 +109,7 @@ def main():
         S.starkv_decode_split(layer.plan, layer.cache, q, Bk, ctx, L, layer.dec_ws)
         if events:
             events[2].record(stream)
-        S.starkv_decode_combine(layer.plan, Bv, ctx, L, layer.out, layer.dec_ws)
+        S.starkv_decode_combine(layer.plan, layer.cache, q, Bk, Bv, ctx, L, layer.out, layer.dec_ws)
         if events:
             events[3].record(stream)
 

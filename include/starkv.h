@@ -62,7 +62,8 @@ typedef enum {
  *           the remaining channels (inlier block) at 4 bits. */
 typedef enum { STARKV_Q_F16 = 0, STARKV_Q_INT4 = 1, STARKV_Q_MIX8_4 = 2 } starkv_qmode;
 
-typedef enum { STARKV_DT_F16 = 0, STARKV_DT_BF16 = 1 } starkv_dtype;
+/* Element types.  F32 is accepted for the attention output only. */
+typedef enum { STARKV_DT_F16 = 0, STARKV_DT_BF16 = 1, STARKV_DT_F32 = 2 } starkv_dtype;
 
 #define STARKV_MAX_KV_HEADS 16
 #define STARKV_MAX_Q_HEADS 64
@@ -80,7 +81,7 @@ typedef struct {
   double  rope_theta;     /* RoPE base, > 1 */
   int32_t d_model;        /* hidden size for starkv_append's down-projection; 0 = latents given */
   int32_t q_dtype;        /* starkv_dtype of q */
-  int32_t out_dtype;      /* starkv_dtype of the attention output */
+  int32_t out_dtype;      /* starkv_dtype of the attention output (F16, BF16 or F32) */
   int32_t x_dtype;        /* starkv_dtype of hidden states (when d_model > 0) */
 } starkv_config;
 
@@ -180,17 +181,23 @@ starkv_status starkv_append(const starkv_plan* plan, void* cache, const void* x_
  *   q            device [B][H_q][d] in q_dtype, already rotated (RoPE) for the
  *                current position; 16-byte aligned.
  *   B_k          device fp16 [sum_r][d]: U_K,g^T of head g at rows
- *                sum_{g'<g} r_g' .. +r_g (the key up-projection, Sec. 3.2).
+ *                sum_{g'<g} r_g' .. +r_g (the key up-projection, Sec. 3.2);
+ *                16-byte aligned.
  *   B_v          device fp16 [r_v][H_kv*d]: U_V^T; query head i uses columns
- *                g*d .. g*d+d-1 of its KV head g.
+ *                g*d .. g*d+d-1 of its KV head g; 16-byte aligned.
  *   ctx_len_dev  device int32 [B]: sequence b attends to rows [0, ctx_len[b]);
  *                key t is rotated by RoPE at position t.  Values are clamped to
  *                [0, max_ctx]; 0 gives a zero output.
  *   max_ctx      host upper bound of ctx_len, 1 <= max_ctx <= capacity, and at most
  *                524288 (64 context splits of at most 8192 tokens; UNSUPPORTED beyond).
- *   out          device [B][H_q][d] in out_dtype, 16-byte aligned.
+ *   out          device [B][H_q][d] in out_dtype, 16-byte aligned; 16-bit types are
+ *                rounded to nearest even from the fp32 result.
  *   ws           device, starkv_decode_workspace_bytes(plan, max_ctx) bytes,
  *                256-byte aligned.
+ * Accuracy: scores are computed with fp16 operands and fp32 accumulation; the
+ * tokens that hold most of the softmax mass are rescored exactly in fp32 (see
+ * the combine pass below), so near-ties between dominant tokens are resolved at
+ * fp32 accuracy.
  * Errors: INVALID_ARG, CAPACITY (max_ctx > capacity), WORKSPACE, ALIGNMENT, HIP. */
 starkv_status starkv_decode_attn(const starkv_plan* plan, const void* cache, const void* q,
                                  const void* B_k, const void* B_v, const int32_t* ctx_len_dev,
@@ -198,13 +205,19 @@ starkv_status starkv_decode_attn(const starkv_plan* plan, const void* cache, con
                                  starkv_stream_t stream);
 
 /* The two launches of starkv_decode_attn, exposed separately so that each can be
- * timed on its own: the split pass (keys, scores, softmax state and value
- * latents per context split, written to ws) and the combine pass (merge of the
- * splits and the value up-projection into out).  Same arguments and errors. */
+ * timed on its own, with the same arguments and errors:
+ *   split    keys, scores, softmax state and value latents per context split, and
+ *            the largest approximate scores of each split, written to ws;
+ *   combine  merge of the splits (log-sum-exp weights), exact fp32 rescoring of
+ *            the tokens that dominate the softmax (re-read from the cache), and
+ *            the value up-projection into out.
+ * The combine pass must follow a split pass with the same cache, q, B_k,
+ * ctx_len, max_ctx and ws. */
 starkv_status starkv_decode_split(const starkv_plan* plan, const void* cache, const void* q,
                                   const void* B_k, const int32_t* ctx_len_dev, int32_t max_ctx,
                                   void* ws, size_t ws_bytes, starkv_stream_t stream);
-starkv_status starkv_decode_combine(const starkv_plan* plan, const void* B_v,
+starkv_status starkv_decode_combine(const starkv_plan* plan, const void* cache, const void* q,
+                                    const void* B_k, const void* B_v,
                                     const int32_t* ctx_len_dev, int32_t max_ctx, void* out,
                                     void* ws, size_t ws_bytes, starkv_stream_t stream);
 

@@ -137,6 +137,22 @@ __device__ __forceinline__ void copy_to_lds(uint8_t* lds, const uint8_t* src, in
   }
 }
 
+// Wait until at most n (wave-uniform) vector memory operations of this wave are
+// outstanding; they complete in issue order.
+__device__ __forceinline__ void wait_vm(int n) {
+  switch (__builtin_amdgcn_readfirstlane(n)) {
+    case 1: __builtin_amdgcn_s_waitcnt(0x0F71); break;
+    case 2: __builtin_amdgcn_s_waitcnt(0x0F72); break;
+    case 3: __builtin_amdgcn_s_waitcnt(0x0F73); break;
+    case 4: __builtin_amdgcn_s_waitcnt(0x0F74); break;
+    case 5: __builtin_amdgcn_s_waitcnt(0x0F75); break;
+    case 6: __builtin_amdgcn_s_waitcnt(0x0F76); break;
+    case 7: __builtin_amdgcn_s_waitcnt(0x0F77); break;
+    case 8: __builtin_amdgcn_s_waitcnt(0x0F78); break;
+    default: __builtin_amdgcn_s_waitcnt(0x0F70); break;   // vmcnt(0)
+  }
+}
+
 __device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel) {
   return __builtin_amdgcn_perm(hi, lo, sel);
 }
@@ -424,11 +440,15 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       }
     }
   }
-  u4 kraw[kMaxLoads];
+  // direct-to-LDS copies; lane 0 of every issued copy is active, so the wave
+  // issues exactly n_kw of them per step
+  const int n_kw = (my_raw + 1023) / 1024;
   auto load_k = [&](int step) {
 #pragma unroll
     for (int i = 0; i < kMaxLoads; ++i)
-      if (ld_ptr[i]) kraw[i] = *reinterpret_cast<const u4*>(ld_ptr[i] + (int64_t)step * ld_stride[i]);
+      if (ld_ptr[i])
+        __builtin_amdgcn_global_load_lds(ld_ptr[i] + (int64_t)step * ld_stride[i], raw + i * 1024,
+                                         16, 0, 0);
   };
   // value codes and meta of one step are copied into LDS ahead of use; per-lane
   // offsets of this wave's channel tiles inside a 32-token block
@@ -446,6 +466,10 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   }
   const int64_t vblk0 = (int64_t)b * (p.cap_pad / 32) + t_begin / 32;
   const int vmeta_bytes = 4 * p.v_ng * 128;
+  // value copies this wave issues per step (copy_to_lds: one per 8 KB stride)
+  auto n_copies = [&](int n_bytes) { return w * 1024 < n_bytes ? (n_bytes - w * 1024 + 8191) / 8192 : 0; };
+  const int n_vw = __builtin_amdgcn_readfirstlane(
+      n_copies(vcode_bytes) + (QM != STARKV_Q_F16 ? n_copies(vmeta_bytes) : 0));
   auto load_v = [&](int step) {
     copy_to_lds(vcode, p.cache + p.v_code_off + (vblk0 + (int64_t)step * 4) * 32 * p.v_row_bytes,
                 vcode_bytes, w, lane);
@@ -456,11 +480,17 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 
   // ---------------------------------------------------------------- main loop
   float m_run[CTH], l_part[CTH];
+  // the two largest scores this lane has seen per tile, with their tokens: the
+  // combine pass rescores the dominant tokens exactly
+  float b1x[CTH], b2x[CTH];
+  uint32_t bt[CTH];   // token offsets from t_begin: first in bits 0..15, second in 16..31
   f4 acc_v[CT][NTW];
 #pragma unroll
   for (int c = 0; c < CTH; ++c) {
     m_run[c] = -INFINITY;
     l_part[c] = 0.0f;
+    b1x[c] = -INFINITY; b2x[c] = -INFINITY;
+    bt[c] = 0;
   }
 #pragma unroll
   for (int c = 0; c < CT; ++c)
@@ -475,11 +505,9 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     const int t_step = t_begin + step * kStepTokens;
     const int tw = t_step + 32 * tg;
     const bool full = (t_step + kStepTokens <= t_end);
-#pragma unroll
-    for (int i = 0; i < kMaxLoads; ++i)
-      if (ld_ptr[i]) *reinterpret_cast<u4*>(raw + (i * 64 + lane) * 16) = kraw[i];
-    if (step + 1 < n_steps) load_k(step + 1);
-    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): staging visible to this wave
+    // this step's keys were copied before the value copies of the step, which
+    // may still be in flight
+    wait_vm(n_vw);
 
     // ------------------------------------------ keys: reconstruct, rotate, score
     f4 acc_s[2][CTH];
@@ -498,6 +526,8 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
         if (NKBS > 3 && k == 4) key_head<D, QM, CTH, (NKBS > 3 ? 4 : 1)>(p.kh[gg], raw, frag, qc, qzero, gg - g0, ct0, G, lane, col, quad, cs, acc_s);
       }
     }
+    // the staging area has been read: copy the next step's keys into it
+    if (step + 1 < n_steps) load_k(step + 1);
 #pragma unroll
     for (int f = 0; f < NF; ++f) {
       const float2 r = rot_s[16 * (f / 4) + 4 * quad + (f % 4)];
@@ -515,10 +545,16 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       for (int s = 0; s < 2; ++s)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
+          const int tok = tw + 16 * s + 4 * quad + e;
           float v = acc_s[s][c][e] * sc;
-          if (!full && tw + 16 * s + 4 * quad + e >= t_end) v = -INFINITY;
+          if (!full && tok >= t_end) v = -INFINITY;
           x[c][s][e] = v;
           mx = fmaxf(mx, v);
+          const uint32_t to = (uint32_t)(tok - t_begin);
+          const bool gt1 = v > b1x[c], gt2 = v > b2x[c];
+          b2x[c] = gt1 ? b1x[c] : (gt2 ? v : b2x[c]);
+          bt[c] = gt1 ? (bt[c] << 16) | to : (gt2 ? (bt[c] & 0xFFFFu) | (to << 16) : bt[c]);
+          b1x[c] = gt1 ? v : b1x[c];
         }
       mx = wave_max16(mx);
       if (quad == 0) red[(tg * CT + ct0 + c) * 16 + col] = mx;
@@ -552,7 +588,9 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     // publishes its vote and every wave combines both
     const bool any_rescale = __any(rescale);
     if (tg == 0 && lane == 0) flag_s[hh] = any_rescale ? 1 : 0;
-    __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this wave's value copies landed
+    // this wave's value copies landed (the next step's key copies, issued after
+    // them, may still be in flight)
+    wait_vm(step + 1 < n_steps ? n_kw : 0);
     __syncthreads();   // (2) probabilities, rescale factors and the step's values visible
 
     // ------------------------------------------ values: acc += P . V'
@@ -634,6 +672,16 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   }
   __syncthreads();
   const int64_t pbase = ((int64_t)b * p.n_split + split) * p.n_q;
+#pragma unroll
+  for (int c = 0; c < CTH; ++c) {
+    if (c >= ctn) break;
+    const int il = (ct0 + c) * 16 + col;
+    if (il < nql) {
+      float2* cd = p.cand + (pbase + q0 + il) * kCand + (tg * 4 + quad) * 2;
+      cd[0] = make_float2(b1x[c], __int_as_float(t_begin + (int)(bt[c] & 0xFFFFu)));
+      cd[1] = make_float2(b2x[c], __int_as_float(t_begin + (int)(bt[c] >> 16)));
+    }
+  }
   if (tg == 0 && quad == 0) {
 #pragma unroll
     for (int c = 0; c < CTH; ++c) {
@@ -667,29 +715,112 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 // ---------------------------------------------------------------------- combine
 #ifdef SK_COMMON
 // One workgroup per (query head, sequence).  Merges the splits with weights
-// 2^(m_s - M) and applies the value up-projection of the head's KV group.  All
-// loads of a phase are issued before their results are used, so each phase
+// 2^(m_s - M), corrects the few tokens that dominate the softmax with exactly
+// recomputed scores, and applies the value up-projection of the head's KV group.
+// All loads of a phase are issued before their results are used, so each phase
 // costs about one memory round trip.
+//
+// Exact rescoring.  The split pass scores with fp16 rotated keys and fp16
+// dequantized latents; the relative error of a score is a few fp16 ulps, so a
+// token's weight is off by about (score magnitude) x 2^-11.  That only matters
+// for tokens holding a large share of the softmax mass, and the split pass
+// reports the two largest approximate scores of every lane (kCand per split and
+// query head).  Candidates whose share times (1 + |score|) reaches kRescoreTau
+// are recomputed here in fp32 from the cache (fp32 dequantization, fp32
+// reconstruction, RoPE angle reduced in fp64), and their contribution to the
+// normalizer and to the merged value latent is moved from the approximate to the
+// exact weight.
 constexpr int kCombineMaxSplits = 64;
+constexpr int kRescoreMax = 32;                        // tokens rescored per query head
+constexpr float kRescoreTau = 1.0f / 64.0f;
+constexpr int kCandPerThread = kCombineMaxSplits * kCand / 256;
+
+__device__ __forceinline__ float h2f(uint16_t u) { return (float)__builtin_bit_cast(_Float16, u); }
+
+// Dequantized key latent channel ch of head g at token t of sequence b.
+__device__ float key_latent(const CombineParams& p, int g, int b, int t, int ch) {
+  const int64_t blk = (int64_t)b * (p.cap_pad / 16) + t / 16;
+  const int tau = t % 16, c = ch / 8, wi = ch % 8;
+  const uint8_t* code = p.cache + p.k_code_off[g] + blk * 16 * p.k_rb[g];
+  if (p.qmode == STARKV_Q_F16)
+    return h2f(*reinterpret_cast<const uint16_t*>(code + c * 256 + tau * 16 + wi * 2));
+  const int ro = p.k_ro[g];
+  int q, grp;
+  if (ch < ro) {
+    q = code[c * 128 + tau * 8 + wi];
+    grp = ch / 32;
+  } else {
+    const int n8 = ro / 8;
+    const uint8_t byte = code[n8 * 128 + (c - n8) * 64 + tau * 4 + wi / 2];
+    q = (wi & 1) ? (byte >> 4) : (byte & 15);
+    grp = (ro + 31) / 32 + (ch - ro) / 32;
+  }
+  const uint16_t* m = reinterpret_cast<const uint16_t*>(
+      p.cache + p.k_meta_off[g] + (blk * p.k_ng[g] + grp) * 64 + tau * 4);
+  return __builtin_fmaf((float)q, h2f(m[0]), h2f(m[1]));
+}
+
+// Dequantized value latent channel r at token t of sequence b.
+__device__ float value_latent(const CombineParams& p, int b, int t, int r) {
+  const int64_t blk = (int64_t)b * (p.cap_pad / 32) + t / 32;
+  const int u = t % 32, kq = (u % 16) / 4, slot = 4 * (u / 16) + u % 4;
+  const uint8_t* code = p.cache + p.v_code_off + blk * 32 * p.v_rb;
+  if (p.qmode == STARKV_Q_F16)
+    return h2f(*reinterpret_cast<const uint16_t*>(code + (r * 4 + kq) * 16 + slot * 2));
+  int q, grp;
+  if (r < p.v_ro) {
+    q = code[(r * 4 + kq) * 8 + slot];
+    grp = r / 32;
+  } else {
+    const uint32_t wd =
+        *reinterpret_cast<const uint32_t*>(code + 32 * p.v_ro + ((r - p.v_ro) * 4 + kq) * 4);
+    const int sh = (slot & 1) ? 16 + 4 * (slot / 2) : 4 * (slot / 2);
+    q = (wd >> sh) & 15;
+    grp = (p.v_ro + 31) / 32 + (r - p.v_ro) / 32;
+  }
+  const uint8_t* m = p.cache + p.v_meta_off + blk * p.v_ng * 128 + (grp * 4 + kq) * 32;
+  return __builtin_fmaf((float)q, h2f(reinterpret_cast<const uint16_t*>(m)[slot]),
+                        h2f(reinterpret_cast<const uint16_t*>(m + 16)[slot]));
+}
 
 __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   extern __shared__ __align__(16) float sm[];
-  float* a = sm;                  // [rv] merged value latent
-  float* wts = sm + p.rv;         // [n_split] split weights
-  float* red = wts + p.n_split;   // [16][D] partial up-projections
-  const int i = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int D = p.head_dim;
+  float* a = sm;                         // [rv] merged value latent
+  float* wts = sm + p.rv;                // [n_split] split weights
+  float* red = wts + p.n_split;          // [32][D] partial up-projections
+  float* c_x = red + 32 * D;             // [kRescoreMax] approximate scores
+  float* c_d = c_x + kRescoreMax;        // [kRescoreMax] weight corrections
+  int* c_t = reinterpret_cast<int*>(c_d + kRescoreMax);   // [kRescoreMax] tokens
+  float* lat = reinterpret_cast<float*>(c_t + kRescoreMax); // [kRescoreMax][128] key latents
+  float* misc = lat + kRescoreMax * 128; // M, L, L', unused, wave counts [4]
+  int* cnt = reinterpret_cast<int*>(misc + 4);
+  const int i = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
   const int g = (int)(((int64_t)i * p.n_kv) / p.n_q);
   int L = p.ctx_len[b];
   L = L < 0 ? 0 : (L > p.max_ctx ? p.max_ctx : L);
-  uint16_t* out = static_cast<uint16_t*>(p.out) + ((int64_t)b * p.n_q + i) * D;
+  const int64_t out_row = ((int64_t)b * p.n_q + i) * D;
   if (L == 0) {
-    for (int j = tid; j < D; j += 256) out[j] = 0;
+    for (int j = tid; j < D; j += 256) {
+      if (p.out_dtype == STARKV_DT_F32) static_cast<float*>(p.out)[out_row + j] = 0.0f;
+      else static_cast<uint16_t*>(p.out)[out_row + j] = 0;
+    }
     return;
   }
   const int ns = (L + p.split_len - 1) / p.split_len;
   const float* part = p.part + ((int64_t)b * p.n_split * p.n_q + i) * p.part_stride;
   const int64_t sstride = (int64_t)p.n_q * p.part_stride;
+  // candidates of all splits, loaded ahead of the split weights
+  const int n_ent = ns * kCand;
+  const float2* cand = p.cand + ((int64_t)b * p.n_split * p.n_q + i) * kCand;
+  float2 ce[kCandPerThread];
+#pragma unroll
+  for (int k = 0; k < kCandPerThread; ++k) {
+    const int e = k * 256 + tid;
+    ce[k] = make_float2(-INFINITY, 0.0f);
+    if (e < n_ent) ce[k] = cand[(int64_t)(e / kCand) * p.n_q * kCand + e % kCand];
+  }
   if (tid < 64) {                 // split weights: one wave, up to 64 splits per lane pass
     float mv[kCombineMaxSplits / 64 + 1], lv[kCombineMaxSplits / 64 + 1];
     float m = -INFINITY;
@@ -708,10 +839,102 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
       l += wv * lv[k];
     }
     for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o);
-    if (tid == 0) red[0] = 1.0f / l;
+    if (tid == 0) { misc[0] = m; misc[1] = l; }
   }
   __syncthreads();
-  const float inv_l = red[0];
+  const float M = misc[0], Lsum = misc[1];
+
+  // ---- candidate selection: share x (1 + |x|) >= tau, tau raised until at most
+  // kRescoreMax remain; compaction in entry order (deterministic)
+  float prio[kCandPerThread];
+#pragma unroll
+  for (int k = 0; k < kCandPerThread; ++k) {
+    const float x = ce[k].x;
+    prio[k] = (x == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(x - M) / Lsum * (1.0f + fabsf(x));
+  }
+  float tau = kRescoreTau;
+  int n_sel = 0;
+  for (int it = 0; it < 8; ++it) {
+    int c = 0;
+#pragma unroll
+    for (int k = 0; k < kCandPerThread; ++k) c += prio[k] >= tau;
+    for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o);
+    if (lane == 0) cnt[w] = c;
+    __syncthreads();
+    n_sel = cnt[0] + cnt[1] + cnt[2] + cnt[3];
+    __syncthreads();
+    if (n_sel <= kRescoreMax) break;
+    tau *= 4.0f;
+  }
+  if (n_sel > kRescoreMax) n_sel = 0;   // too flat to matter at any threshold tried
+  if (n_sel > 0) {
+    int base = 0;
+#pragma unroll
+    for (int k = 0; k < kCandPerThread; ++k) {
+      const bool sel = prio[k] >= tau;
+      const uint64_t bal = __ballot(sel);
+      const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
+      if (lane == 0) cnt[w] = __builtin_popcountll(bal);
+      __syncthreads();
+      int off = base;
+      for (int ww = 0; ww < w; ++ww) off += cnt[ww];
+      if (sel) {
+        c_x[off + rank] = ce[k].x;
+        c_t[off + rank] = __float_as_int(ce[k].y);
+      }
+      base += cnt[0] + cnt[1] + cnt[2] + cnt[3];
+      __syncthreads();
+    }
+    // ---- exact scores: dequantized key latents of every candidate, then one
+    // (candidate, RoPE pair) item per thread; the items of a candidate are
+    // consecutive lanes of one wave and are summed with shuffles
+    const int HALF = D / 2;
+    const int r_g = p.k_rank[g];
+    for (int it = tid; it < n_sel * r_g; it += 256) {
+      const int j = it / r_g, ch = it % r_g;
+      lat[j * 128 + ch] = key_latent(p, g, b, c_t[j], ch);
+    }
+    __syncthreads();
+    const uint16_t* bk = p.bk + (int64_t)p.k_bkrow[g] * D;
+    const uint16_t* qs = static_cast<const uint16_t*>(p.q) + ((int64_t)b * p.n_q + i) * D;
+    for (int it0 = 0; it0 < n_sel * HALF; it0 += 256) {
+      const int it = it0 + tid;
+      const int j = it / HALF, l = it % HALF;
+      float dot = 0.0f;
+      if (j < n_sel) {
+        const float* lj = lat + j * 128;
+        float klo = 0.0f, khi = 0.0f;
+#pragma unroll 8
+        for (int ch = 0; ch < r_g; ++ch) {
+          klo = __builtin_fmaf(lj[ch], h2f(bk[ch * D + l]), klo);
+          khi = __builtin_fmaf(lj[ch], h2f(bk[ch * D + l + HALF]), khi);
+        }
+        const float q_lo = p.q_bf16 ? __uint_as_float((uint32_t)qs[l] << 16) : h2f(qs[l]);
+        const float q_hi = p.q_bf16 ? __uint_as_float((uint32_t)qs[l + HALF] << 16) : h2f(qs[l + HALF]);
+        // angle t * theta^(-2l/D), reduced modulo 2 pi in fp64
+        double ph = (double)c_t[j] * exp2(-(2.0 * l / D) * p.log2_theta);
+        ph -= 6.283185307179586476925286766559 * floor(ph * 0.15915494309189533576888376337251);
+        float sf, cf;
+        sincosf((float)ph, &sf, &cf);
+        dot = q_lo * (klo * cf - khi * sf) + q_hi * (khi * cf + klo * sf);
+      }
+      for (int o = HALF / 2; o > 0; o >>= 1) dot += __shfl_xor(dot, o);
+      if (l == 0 && j < n_sel)
+        c_d[j] = __builtin_amdgcn_exp2f(dot * p.score_scale - M) - __builtin_amdgcn_exp2f(c_x[j] - M);
+    }
+    __syncthreads();
+    if (tid == 0) {
+      float l2 = Lsum;
+      for (int j = 0; j < n_sel; ++j) l2 += c_d[j];
+      misc[2] = l2;
+    }
+    __syncthreads();
+  } else if (tid == 0) {
+    misc[2] = Lsum;
+  }
+  __syncthreads();
+  const float inv_l = 1.0f / misc[2];
   for (int r = tid; r < p.rv; r += 256) {
     float v[kCombineMaxSplits];
 #pragma unroll
@@ -721,6 +944,14 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
 #pragma unroll
     for (int s = 0; s < kCombineMaxSplits; ++s)
       if (s < ns) acc += wts[s] * v[s];
+    for (int j0 = 0; j0 < n_sel; j0 += 8) {   // eight candidates' loads in flight
+      float vl[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) vl[u] = j0 + u < n_sel ? value_latent(p, b, c_t[j0 + u], r) : 0.0f;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (j0 + u < n_sel) acc = __builtin_fmaf(c_d[j0 + u], vl[u], acc);
+    }
     a[r] = acc * inv_l;
   }
   __syncthreads();
@@ -756,15 +987,19 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   if (tid < D) {
     float ov = 0.0f;
     for (int k = 0; k < groups; ++k) ov += red[k * D + tid];
-    uint16_t bits;
-    if (p.out_bf16) {
-      const uint32_t u = __float_as_uint(ov);
-      bits = (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
-      if ((u & 0x7F800000u) == 0x7F800000u) bits = (uint16_t)(u >> 16) | ((u & 0xFFFFu) ? 0x40 : 0);
+    if (p.out_dtype == STARKV_DT_F32) {
+      static_cast<float*>(p.out)[out_row + tid] = ov;
     } else {
-      bits = __builtin_bit_cast(uint16_t, (_Float16)ov);
+      uint16_t bits;
+      if (p.out_dtype == STARKV_DT_BF16) {
+        const uint32_t u = __float_as_uint(ov);
+        bits = (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+        if ((u & 0x7F800000u) == 0x7F800000u) bits = (uint16_t)(u >> 16) | ((u & 0xFFFFu) ? 0x40 : 0);
+      } else {
+        bits = __builtin_bit_cast(uint16_t, (_Float16)ov);
+      }
+      static_cast<uint16_t*>(p.out)[out_row + tid] = bits;
     }
-    out[tid] = bits;
   }
 }
 #endif  // SK_COMMON
@@ -845,7 +1080,9 @@ int launch_decode_split_ntw(const DecodeParams& p, int head_dim, int qmode, int 
 
 int launch_decode_combine(const CombineParams& p, void* stream) {
   if (p.n_split > kCombineMaxSplits) return (int)hipErrorInvalidValue;
-  const size_t lds = (size_t)(p.rv + p.n_split + 32 * p.head_dim) * sizeof(float);
+  const size_t lds =
+      (size_t)(p.rv + p.n_split + 32 * p.head_dim + 3 * kRescoreMax + kRescoreMax * 128 + 8) *
+      sizeof(float);
   dim3 grid(p.n_q, p.batch);
   hipLaunchKernelGGL(decode_combine_kernel, grid, dim3(256), lds,
                      static_cast<hipStream_t>(stream), p);

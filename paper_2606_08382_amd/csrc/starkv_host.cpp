@@ -105,8 +105,10 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
   if (!(c->rope_theta > 1.0) || !std::isfinite(c->rope_theta))
     return fail(STARKV_ERR_INVALID_ARG, "rope_theta must be finite and > 1");
   if (c->d_model < 0) return fail(STARKV_ERR_INVALID_ARG, "d_model < 0");
-  for (int dt : {c->q_dtype, c->out_dtype, c->x_dtype})
+  for (int dt : {c->q_dtype, c->x_dtype})
     if (dt != STARKV_DT_F16 && dt != STARKV_DT_BF16) return fail(STARKV_ERR_INVALID_ARG, "dtype %d", dt);
+  if (c->out_dtype != STARKV_DT_F16 && c->out_dtype != STARKV_DT_BF16 && c->out_dtype != STARKV_DT_F32)
+    return fail(STARKV_ERR_INVALID_ARG, "out_dtype %d", c->out_dtype);
   if (c->n_kv_heads > STARKV_MAX_KV_HEADS)
     return fail(STARKV_ERR_UNSUPPORTED, "n_kv_heads %d > %d", c->n_kv_heads, STARKV_MAX_KV_HEADS);
   if (c->n_q_heads > STARKV_MAX_Q_HEADS)
@@ -322,10 +324,18 @@ int32_t starkv_decode_splits(const starkv_plan* P, int32_t max_ctx) {
 
 static int part_stride(const starkv_plan* P) { return P->cfg.value_rank + 4; }
 
+// Workspace: the split partials [B][splits][H_q][part_stride] fp32, then the
+// rescoring candidates [B][splits][H_q][kCand] (score, token) pairs.
+static int64_t cand_offset(const starkv_plan* P, int32_t max_ctx) {
+  const int64_t ns = starkv_decode_splits(P, max_ctx);
+  return align256((int64_t)P->cfg.batch * ns * P->cfg.n_q_heads * part_stride(P) * 4);
+}
+
 size_t starkv_decode_workspace_bytes(const starkv_plan* P, int32_t max_ctx) {
   if (!P || max_ctx < 1) return 0;
   const int64_t ns = starkv_decode_splits(P, max_ctx);
-  return (size_t)align256((int64_t)P->cfg.batch * ns * P->cfg.n_q_heads * part_stride(P) * 4);
+  return (size_t)(cand_offset(P, max_ctx) +
+                  align256((int64_t)P->cfg.batch * ns * P->cfg.n_q_heads * kCand * 8));
 }
 
 static starkv_status check_common(const starkv_plan* P, int32_t max_ctx, size_t ws_bytes,
@@ -343,6 +353,27 @@ static starkv_status check_common(const starkv_plan* P, int32_t max_ctx, size_t 
   return STARKV_OK;
 }
 
+// Arguments of the decode entry points; B_v and out are checked when non-null
+// is required (need_out).
+static starkv_status check_decode(const starkv_plan* P, const void* cache, const void* q,
+                                  const void* B_k, const void* B_v, const int32_t* ctx_len_dev,
+                                  int32_t max_ctx, const void* out, const void* ws,
+                                  size_t ws_bytes, bool need_out) {
+  starkv_status st = check_common(P, max_ctx, ws_bytes, ws);
+  if (st != STARKV_OK) return st;
+  if (!cache || !q || !B_k || !ctx_len_dev || (need_out && (!B_v || !out)))
+    return fail(STARKV_ERR_INVALID_ARG, "NULL device pointer");
+  if (reinterpret_cast<uintptr_t>(cache) % 256) return fail(STARKV_ERR_ALIGNMENT, "cache not 256-byte aligned");
+  if (reinterpret_cast<uintptr_t>(q) % 16) return fail(STARKV_ERR_ALIGNMENT, "q not 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(B_k) % 16) return fail(STARKV_ERR_ALIGNMENT, "B_k not 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(ctx_len_dev) % 4) return fail(STARKV_ERR_ALIGNMENT, "ctx_len not 4-byte aligned");
+  if (need_out) {
+    if (reinterpret_cast<uintptr_t>(B_v) % 16) return fail(STARKV_ERR_ALIGNMENT, "B_v not 16-byte aligned");
+    if (reinterpret_cast<uintptr_t>(out) % 16) return fail(STARKV_ERR_ALIGNMENT, "out not 16-byte aligned");
+  }
+  return STARKV_OK;
+}
+
 static starkv_status hip_status(int e, const char* what) {
   if (e != hipSuccess) return fail(STARKV_ERR_HIP, "%s: %s", what, hipGetErrorString((hipError_t)e));
   return STARKV_OK;
@@ -351,13 +382,9 @@ static starkv_status hip_status(int e, const char* what) {
 starkv_status starkv_decode_split(const starkv_plan* P, const void* cache, const void* q,
                                   const void* B_k, const int32_t* ctx_len_dev, int32_t max_ctx,
                                   void* ws, size_t ws_bytes, starkv_stream_t stream) {
-  starkv_status st = check_common(P, max_ctx, ws_bytes, ws);
+  starkv_status st = check_decode(P, cache, q, B_k, nullptr, ctx_len_dev, max_ctx, nullptr, ws,
+                                  ws_bytes, false);
   if (st != STARKV_OK) return st;
-  if (!cache || !q || !B_k || !ctx_len_dev) return fail(STARKV_ERR_INVALID_ARG, "NULL device pointer");
-  if (reinterpret_cast<uintptr_t>(cache) % 256) return fail(STARKV_ERR_ALIGNMENT, "cache not 256-byte aligned");
-  if (reinterpret_cast<uintptr_t>(q) % 16) return fail(STARKV_ERR_ALIGNMENT, "q not 16-byte aligned");
-  if (reinterpret_cast<uintptr_t>(B_k) % 16) return fail(STARKV_ERR_ALIGNMENT, "B_k not 16-byte aligned");
-  if (reinterpret_cast<uintptr_t>(ctx_len_dev) % 4) return fail(STARKV_ERR_ALIGNMENT, "ctx_len not 4-byte aligned");
   const starkv_config& c = P->cfg;
   DecodeParams p;
   std::memset(&p, 0, sizeof(p));
@@ -366,6 +393,7 @@ starkv_status starkv_decode_split(const starkv_plan* P, const void* cache, const
   p.bk = static_cast<const uint16_t*>(B_k);
   p.ctx_len = ctx_len_dev;
   p.part = static_cast<float*>(ws);
+  p.cand = reinterpret_cast<float2*>(static_cast<uint8_t*>(ws) + cand_offset(P, max_ctx));
   p.batch = c.batch;
   p.n_q = c.n_q_heads;
   p.n_kv = c.n_kv_heads;
@@ -399,18 +427,23 @@ starkv_status starkv_decode_split(const starkv_plan* P, const void* cache, const
   return hip_status(e, "decode_split launch");
 }
 
-starkv_status starkv_decode_combine(const starkv_plan* P, const void* B_v,
+starkv_status starkv_decode_combine(const starkv_plan* P, const void* cache, const void* q,
+                                    const void* B_k, const void* B_v,
                                     const int32_t* ctx_len_dev, int32_t max_ctx, void* out,
                                     void* ws, size_t ws_bytes, starkv_stream_t stream) {
-  starkv_status st = check_common(P, max_ctx, ws_bytes, ws);
+  starkv_status st = check_decode(P, cache, q, B_k, B_v, ctx_len_dev, max_ctx, out, ws, ws_bytes,
+                                  true);
   if (st != STARKV_OK) return st;
-  if (!B_v || !ctx_len_dev || !out) return fail(STARKV_ERR_INVALID_ARG, "NULL device pointer");
-  if (reinterpret_cast<uintptr_t>(out) % 16) return fail(STARKV_ERR_ALIGNMENT, "out not 16-byte aligned");
-  if (reinterpret_cast<uintptr_t>(B_v) % 2) return fail(STARKV_ERR_ALIGNMENT, "B_v not 2-byte aligned");
   const starkv_config& c = P->cfg;
+  const starkv_layout& L = P->layout;
   CombineParams p;
+  std::memset(&p, 0, sizeof(p));
   p.part = static_cast<const float*>(ws);
+  p.cand = reinterpret_cast<const float2*>(static_cast<const uint8_t*>(ws) + cand_offset(P, max_ctx));
   p.bv = static_cast<const uint16_t*>(B_v);
+  p.bk = static_cast<const uint16_t*>(B_k);
+  p.cache = static_cast<const uint8_t*>(cache);
+  p.q = q;
   p.ctx_len = ctx_len_dev;
   p.out = out;
   p.batch = c.batch;
@@ -422,7 +455,26 @@ starkv_status starkv_decode_combine(const starkv_plan* P, const void* B_v,
   p.split_len = starkv_decode_split_tokens(P, max_ctx);
   p.n_split = starkv_decode_splits(P, max_ctx);
   p.part_stride = part_stride(P);
-  p.out_bf16 = c.out_dtype == STARKV_DT_BF16;
+  p.out_dtype = c.out_dtype;
+  p.q_bf16 = c.q_dtype == STARKV_DT_BF16;
+  p.qmode = c.qmode;
+  p.cap_pad = L.padded_capacity;
+  p.score_scale = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
+  p.log2_theta = std::log2(c.rope_theta);
+  for (int g = 0; g < c.n_kv_heads; ++g) {
+    p.k_code_off[g] = L.key_code_offset[g];
+    p.k_meta_off[g] = L.key_meta_offset[g];
+    p.k_rank[g] = P->key_rank[g];
+    p.k_ro[g] = L.key_outlier_channels[g];
+    p.k_ng[g] = L.key_groups[g];
+    p.k_rb[g] = L.key_row_bytes[g];
+    p.k_bkrow[g] = P->kh[g].bk_row;
+  }
+  p.v_code_off = L.value_code_offset;
+  p.v_meta_off = L.value_meta_offset;
+  p.v_ro = L.value_outlier_channels;
+  p.v_ng = L.value_groups;
+  p.v_rb = L.value_row_bytes;
   return hip_status(launch_decode_combine(p, static_cast<void*>(stream)), "decode_combine launch");
 }
 
@@ -430,10 +482,13 @@ starkv_status starkv_decode_attn(const starkv_plan* P, const void* cache, const 
                                  const void* B_k, const void* B_v, const int32_t* ctx_len_dev,
                                  int32_t max_ctx, void* out, void* ws, size_t ws_bytes,
                                  starkv_stream_t stream) {
-  if (!B_v || !out) return fail(STARKV_ERR_INVALID_ARG, "NULL device pointer");
-  starkv_status st = starkv_decode_split(P, cache, q, B_k, ctx_len_dev, max_ctx, ws, ws_bytes, stream);
+  starkv_status st = check_decode(P, cache, q, B_k, B_v, ctx_len_dev, max_ctx, out, ws, ws_bytes,
+                                  true);
   if (st != STARKV_OK) return st;
-  return starkv_decode_combine(P, B_v, ctx_len_dev, max_ctx, out, ws, ws_bytes, stream);
+  st = starkv_decode_split(P, cache, q, B_k, ctx_len_dev, max_ctx, ws, ws_bytes, stream);
+  if (st != STARKV_OK) return st;
+  return starkv_decode_combine(P, cache, q, B_k, B_v, ctx_len_dev, max_ctx, out, ws, ws_bytes,
+                               stream);
 }
 
 // ---------------------------------------------------------------- append

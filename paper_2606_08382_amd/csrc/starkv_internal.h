@@ -74,7 +74,7 @@ struct CombineParams {
   void* out;
   int32_t batch, n_q, n_kv, head_dim, rv;
   int32_t max_ctx, split_len, n_split, part_stride;
-  int32_t out_bf16, q_bf16, qmode, cap_pad;
+  int32_t out_dtype, q_bf16, qmode, cap_pad;
   float score_scale;
   double log2_theta;
   // key head of this query head's group and the value latent (cache layout)

@@ -41,7 +41,9 @@ class Layer:
         self.dec_ws = torch.empty(max(S.starkv_decode_workspace_bytes(self.plan, self.max_ctx), 256),
                                   dtype=torch.uint8, device=device)
         self.app_ws = None
-        self.out = torch.empty((batch, n_q_heads, head_dim), dtype=torch.int16, device=device)
+        self.out = torch.empty((batch, n_q_heads, head_dim),
+                               dtype=torch.float32 if out_dtype == S.DT_F32 else torch.int16,
+                               device=device)
 
     def _app_ws(self, n_new: int):
         import torch
@@ -68,6 +70,8 @@ class Layer:
         """Output bit patterns -> float64 numpy."""
         import torch
         o = (self.out if out is None else out).cpu()
+        if self.out_dtype == S.DT_F32:
+            return o.to(torch.float64).numpy()
         if self.out_dtype == S.DT_BF16:
             return o.view(torch.bfloat16).to(torch.float64).numpy()
         return o.view(torch.float16).to(torch.float64).numpy()

@@ -18,7 +18,7 @@ STARKV_OK = 0
 STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "UNSUPPORTED", 3: "CAPACITY", 4: "WORKSPACE",
                 5: "ALIGNMENT", 6: "HIP"}
 Q_F16, Q_INT4, Q_MIX8_4 = 0, 1, 2
-DT_F16, DT_BF16 = 0, 1
+DT_F16, DT_BF16, DT_F32 = 0, 1, 2   # F32: attention output only
 MAX_KV_HEADS = 16
 
 
@@ -85,7 +85,7 @@ def lib():
         L.starkv_decode_attn.restype = C.c_int
         L.starkv_decode_split.argtypes = [P, P, P, P, P, C.c_int32, P, S, P]
         L.starkv_decode_split.restype = C.c_int
-        L.starkv_decode_combine.argtypes = [P, P, P, C.c_int32, P, P, S, P]
+        L.starkv_decode_combine.argtypes = [P, P, P, P, P, P, C.c_int32, P, P, S, P]
         L.starkv_decode_combine.restype = C.c_int
         L.starkv_decode_splits.argtypes = [P, C.c_int32]
         L.starkv_decode_splits.restype = C.c_int32
@@ -208,10 +208,10 @@ def starkv_decode_split(plan: Plan, cache, q, B_k, ctx_len, max_ctx: int, ws,
                                      _stream(stream)))
 
 
-def starkv_decode_combine(plan: Plan, B_v, ctx_len, max_ctx: int, out, ws,
+def starkv_decode_combine(plan: Plan, cache, q, B_k, B_v, ctx_len, max_ctx: int, out, ws,
                           ws_bytes: Optional[int] = None, stream=None) -> None:
-    _check(lib().starkv_decode_combine(plan.handle, _ptr(B_v), _ptr(ctx_len), max_ctx,
-                                       _ptr(out), _ptr(ws),
+    _check(lib().starkv_decode_combine(plan.handle, _ptr(cache), _ptr(q), _ptr(B_k), _ptr(B_v),
+                                       _ptr(ctx_len), max_ctx, _ptr(out), _ptr(ws),
                                        _nbytes(ws) if ws_bytes is None else ws_bytes,
                                        _stream(stream)))
 

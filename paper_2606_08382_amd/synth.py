@@ -14,8 +14,9 @@ and weights are not available):
   * B_k,g ~ N(0,1)/sqrt(r_g), B_v ~ N(0,1)/sqrt(r_v), stored fp16;
   * q ~ N(0,1) (already rotated), fp16 or bf16;
   * hidden states x ~ N(0,1) bf16; down-projection column i ~ N(0,1)*sigma_i/sqrt(d_model);
-  * peaked variant: q x 4 and four needle tokens per sequence whose key latents are
-    scaled x8 (attention concentrates on a few tokens; outputs of order 0.5-1.5).
+  * peaked variant of strength k (peaked=True is k = 1): q x 4k and four needle
+    tokens per sequence whose key latents are scaled x 8k (attention concentrates
+    on a few tokens with large scores; outputs of order 0.5-1.5).
 """
 from __future__ import annotations
 
@@ -25,7 +26,7 @@ from typing import List, Optional
 import numpy as np
 
 Q_F16, Q_INT4, Q_MIX8_4 = 0, 1, 2
-DT_F16, DT_BF16 = 0, 1
+DT_F16, DT_BF16, DT_F32 = 0, 1, 2
 
 
 @dataclass
@@ -123,7 +124,7 @@ class Inputs:
         return sum(self.key_rank) + self.value_rank
 
 
-def generate(w: Workload, seed: Optional[int] = None, peaked: bool = False,
+def generate(w: Workload, seed: Optional[int] = None, peaked: int = 0,
              with_latents: bool = True, with_hidden: bool = False,
              n_hidden_tokens: Optional[int] = None) -> Inputs:
     rng = np.random.Generator(np.random.PCG64(w.seed if seed is None else seed))
@@ -139,8 +140,9 @@ def generate(w: Workload, seed: Optional[int] = None, peaked: bool = False,
     Bk = np.concatenate([rng.standard_normal((r, d)) / np.sqrt(r) for r in ranks], axis=0)
     Bv = rng.standard_normal((w.value_rank, w.n_kv_heads * d)) / np.sqrt(w.value_rank)
     q = rng.standard_normal((w.batch, w.n_q_heads, d))
-    if peaked:
-        q = q * 4.0
+    strength = int(peaked)
+    if strength:
+        q = q * (4.0 * strength)
     if w.ragged is not None:
         lo, hi = w.ragged
         ctx = rng.integers(lo, hi + 1, size=w.batch).astype(np.int32)
@@ -162,7 +164,7 @@ def generate(w: Workload, seed: Optional[int] = None, peaked: bool = False,
         ksum = sum(ranks)
         for b in range(w.batch):
             for t in needles[b]:
-                v = latents[b, t, :ksum].view(np.float16).astype(np.float32) * 8.0
+                v = latents[b, t, :ksum].view(np.float16).astype(np.float32) * (8.0 * strength)
                 latents[b, t, :ksum] = np.ascontiguousarray(v.astype(np.float16)).view(np.uint16)
     x = A = None
     if with_hidden:

@@ -52,6 +52,7 @@ def _cfg(**kw):
     (dict(qmode=7), 1), (dict(rope_theta=1.0), 1), (dict(capacity=0), 1),
     (dict(head_dim=96), 2), (dict(group_size=64), 2), (dict(n_q_heads=96, n_kv_heads=2), 2),
     (dict(n_q_heads=6, n_kv_heads=2), 2), (dict(d_model=100), 2),
+    (dict(q_dtype=S.DT_F32), 1), (dict(out_dtype=3), 1),
 ])
 def test_plan_create_rejects_bad_configs(kw, status):
     with pytest.raises(S.StarkvError) as ei:
@@ -79,6 +80,18 @@ def test_entry_points_validate_before_launch():
     with pytest.raises(S.StarkvError) as ei:
         S.starkv_decode_attn(plan, fake, fake, fake, fake, fake, 0, fake, fake, need)
     assert ei.value.status == 1
+    with pytest.raises(S.StarkvError) as ei:            # B_v misaligned: caught before the split
+        S.starkv_decode_attn(plan, fake, fake, fake, fake + 2, fake, 1000, fake, fake, need)
+    assert ei.value.status == 5
+    with pytest.raises(S.StarkvError) as ei:
+        S.starkv_decode_combine(plan, fake, fake, None, fake, fake, 1000, fake, fake, need)
+    assert ei.value.status == 1                       # combine re-reads the keys: B_k required
+    with pytest.raises(S.StarkvError) as ei:
+        S.starkv_decode_combine(plan, fake, fake, fake, fake, fake, 1000, fake + 4, fake, need)
+    assert ei.value.status == 5                       # out misaligned
+    with pytest.raises(S.StarkvError) as ei:
+        S.starkv_decode_split(plan, fake, fake + 2, fake, fake, 1000, fake, need)
+    assert ei.value.status == 5                       # q misaligned
     with pytest.raises(S.StarkvError) as ei:
         S.starkv_append(plan, fake, fake, None, fake, 0, None, 0)
     assert ei.value.status == 1                       # n_new < 1

@@ -48,7 +48,7 @@ def _run_case(w, inp, capacity=None, max_ctx=None, ctx_len=None):
     ref, _ = O.decode_attn(cfg, cache, inp.q, w.q_dtype == synth.DT_BF16, inp.Bk, inp.Bv,
                            np.minimum(ctx, mc))
     got = layer.out_float()
-    e, s = assert_close(got, ref, w.name)
+    e, s = assert_close(got, ref, w.name, w.out_dtype)
     say(f"  max err {e:.3e}  max |o| {s:.3e}")
     return layer, got, ref
 
@@ -56,10 +56,36 @@ def _run_case(w, inp, capacity=None, max_ctx=None, ctx_len=None):
 @pytest.mark.parametrize("name,ctx,batch", [("c1", 1024, None), ("c1", 1000, None),
                                             ("c2", 700, 2), ("c3", 1100, 2), ("c3", 129, 1),
                                             ("c5", 600, 2)])
-@pytest.mark.parametrize("peaked", [False, True])
+@pytest.mark.parametrize("peaked", [0, 1])
 def test_decode_matches_oracle(name, ctx, batch, peaked):
     w = small(name, ctx, batch)
     inp = synth.generate(w, peaked=peaked)
+    _run_case(w, inp)
+
+
+@pytest.mark.parametrize("name,ctx,batch", [("c1", 1024, None), ("c2", 700, 2), ("c3", 1100, 2),
+                                            ("c5", 600, 2)])
+@pytest.mark.parametrize("out_dtype", [None, synth.DT_F32])
+def test_decode_strongly_peaked(name, ctx, batch, out_dtype):
+    """Scores of tens (log2 units) with several needles competing: the fp16 score path alone
+    misses the tolerance here; the exact rescoring of the dominant tokens restores it.  With
+    an fp32 output the tolerance applies to the arithmetic alone."""
+    w = small(name, ctx, batch)
+    if out_dtype is not None:
+        w = w.with_(out_dtype=out_dtype)
+    inp = synth.generate(w, peaked=2)
+    _run_case(w, inp)
+
+
+def test_decode_needle_near_tie():
+    """Two needle tokens with the same key latent at different positions: their scores differ
+    only through RoPE, and the output is a near-even mix of their values."""
+    w = small("c3", ctx=1500, batch=2)
+    inp = synth.generate(w, peaked=2)
+    ksum = sum(inp.key_rank)
+    for b in range(w.batch):
+        t0, t1 = int(inp.needles[b][0]), int(inp.needles[b][1])
+        inp.latents[b, t1, :ksum] = inp.latents[b, t0, :ksum]
     _run_case(w, inp)
 
 
@@ -172,5 +198,5 @@ def test_full_size_128k_sampled_heads():
     ref, _ = O.decode_attn(cfg, cache, inp.q, True, inp.Bk, inp.Bv, inp.ctx_len, sel=sel)
     got = layer.out_float()
     for (b, i) in sel:
-        e, s = assert_close(got[b, i], ref[b, i], f"b={b} head={i}")
+        e, s = assert_close(got[b, i], ref[b, i], f"b={b} head={i}", w.out_dtype)
     say(f"  sampled heads ok, last max err {e:.3e} |o| {s:.3e}")
