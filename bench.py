@@ -24,6 +24,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+COPY_BYTES = 256 << 20           # the plain device-to-device copy timed beside the path
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_split_c3_traffic.json")
+SPLIT_SOURCE = os.path.join(ROOT, "paper_2606_08382_amd", "csrc", "decode.hip")
 
 
 def log(*a):
@@ -46,6 +49,42 @@ def cpu_baseline(w, inp, sample_ctx: int):
     return {"value": 1.0 / full, "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": (f"1 sequence x {w.n_q_heads} query heads over the first {sample_ctx} of "
                        f"{w.ctx} tokens took {dt:.2f} s; scaled linearly in context length")}
+
+
+def measured_traffic(workload_name):
+    """HBM bytes per split launch from the committed rocprofv3 counter summary (FETCH_SIZE and
+    WRITE_SIZE, each scaled by the same counter's reading for a copy of known size), or None
+    when the summary is missing, covers another workload, or the kernel source has changed
+    since the counters were taken."""
+    import hashlib
+    try:
+        with open(TRAFFIC_SUMMARY) as f:
+            t = json.load(f)
+        with open(SPLIT_SOURCE, "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()
+    except (OSError, ValueError):
+        return None, None
+    if t.get("source_sha256") != sha or t.get("workload") != workload_name:
+        return None, None
+    return float(t["traffic_bytes_per_launch"]), t
+
+
+def copy_stream(torch, stream, reps=5):
+    """Bandwidth of a plain device-to-device copy of COPY_BYTES (read + write), for context."""
+    src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda")
+    src.fill_(1)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(reps)]
+    for a, b in evs:
+        a.record(stream)
+        dst.copy_(src)
+        b.record(stream)
+    torch.cuda.synchronize()
+    ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    return {"bytes_read": COPY_BYTES, "bytes_written": COPY_BYTES, "us": ms * 1e3,
+            "GBps": 2 * COPY_BYTES / (ms / 1e3) / 1e9}
 
 
 def main():
@@ -136,6 +175,9 @@ def main():
     log(f"append {t_app.mean() * 1e3:.1f} us  split {t_split.mean() * 1e3:.1f} us "
         f"(median {np.median(t_split) * 1e3:.1f})  combine {t_comb.mean() * 1e3:.1f} us  "
         f"wall/step {ms_step * 1e3:.1f} us")
+    copy = copy_stream(torch, stream)
+    log(f"device copy {copy['GBps']:.0f} GB/s (read + write)")
+    traffic, tsum = measured_traffic(w.name)
     result = {
         "metric": "decode-attention tokens/s at 128K ctx; achieved HBM GB/s vs peak",
         "value": B / (ms_step / 1e3),
@@ -153,10 +195,15 @@ def main():
         "kernels_us": {"append": float(t_app.mean() * 1e3), "decode_split": float(t_split.mean() * 1e3),
                        "decode_combine": float(t_comb.mean() * 1e3)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": "decode_split", "alg_bytes_per_launch": alg_bytes,
                      "bytes_per_token": per_token},
+        "copy_stream": copy,
     }
+    if tsum is not None:
+        result["roofline"]["traffic_detail"] = {
+            k: tsum[k] for k in ("fetch_bytes_per_launch", "write_bytes_per_launch",
+                                 "fetch_scale", "write_scale") if k in tsum}
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         result["cpu_baseline"] = cpu_baseline(w, inp, min(args.cpu_sample_ctx, L))

@@ -1,8 +1,9 @@
 // Decode attention read from the low-rank, quantized cache (gfx950).
 //
-// decode_split: one workgroup per (context split, sequence, KV-head group).
-//   Four waves each take 32 tokens per step (two 16-token subtiles).  For every
-//   KV head of the group a wave
+// decode_split: one workgroup per (context split, sequence, KV-head group), eight
+//   waves: four token groups (32 tokens of every 128-token step each, two
+//   16-token subtiles) times two halves of the group's KV heads.  For every KV
+//   head of its half a wave
 //     - dequantizes the key latents of its tokens into MFMA operands (registers),
 //     - rebuilds the keys with v_mfma_f32_16x16x32_f16 against the head's
 //       up-projection block held in LDS as MFMA fragments (Sec. 3.2, 4.3.3),
@@ -16,10 +17,12 @@
 //   probabilities of all waves can be stacked into one matrix and multiplied
 //   with the shared value latent V' as one MFMA GEMM, each wave owning a slice
 //   of V' channels (the reordered value path of Sec. 3.3 and the stacked
-//   p.V' GEMM of App. A.6).  The split's softmax state and value-latent
-//   accumulator go to the workspace.
-// decode_combine: merges the splits (log-sum-exp weights) and applies the value
-//   up-projection U_V once per query head (Sec. 3.3), casting to the output type.
+//   p.V' GEMM of App. A.6).  The split's softmax state, value-latent
+//   accumulator and the largest approximate scores (rescoring candidates) go
+//   to the workspace.
+// decode_combine: merges the splits (log-sum-exp weights), rescores the
+//   dominant tokens exactly, and applies the value up-projection U_V once per
+//   query head (Sec. 3.3), casting to the output type.
 #include <hip/hip_runtime.h>
 
 #include "starkv_internal.h"
