@@ -34,6 +34,7 @@ typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+typedef float f2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ f4 mfma16(h8 a, h8 b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
@@ -48,34 +49,6 @@ __device__ __forceinline__ uint32_t as_u32(h2 h) { return __builtin_bit_cast(uin
 __device__ __forceinline__ uint32_t deq_pair(uint32_t magic_pair, h2 s, h2 z) {
   h2 c = as_h2(magic_pair) - (h2){(_Float16)1024.0f, (_Float16)1024.0f};
   return as_u32(__builtin_elementwise_fma(c, s, z));
-}
-
-// 4-bit word: element pairs (nibble k, nibble k+4), k = 0..3.
-__device__ __forceinline__ u4 deq_int4(uint32_t w, h2 s0, h2 z0, h2 s1, h2 z1, h2 s2, h2 z2,
-                                       h2 s3, h2 z3) {
-  u4 r;
-  r.x = deq_pair(((w >> 0) & 0x000F000Fu) | 0x64006400u, s0, z0);
-  r.y = deq_pair(((w >> 4) & 0x000F000Fu) | 0x64006400u, s1, z1);
-  r.z = deq_pair(((w >> 8) & 0x000F000Fu) | 0x64006400u, s2, z2);
-  r.w = deq_pair(((w >> 12) & 0x000F000Fu) | 0x64006400u, s3, z3);
-  return r;
-}
-
-// 8-bit chunk (bytes 0..7): element pairs (byte 2k, byte 2k+1).
-__device__ __forceinline__ uint32_t bytes01(uint32_t d) {
-  return (d & 0xFFu) | ((d & 0xFF00u) << 8) | 0x64006400u;
-}
-__device__ __forceinline__ uint32_t bytes23(uint32_t d) {
-  return ((d >> 16) & 0xFFu) | ((d >> 8) & 0xFF0000u) | 0x64006400u;
-}
-__device__ __forceinline__ u4 deq_int8(u2 d, h2 s0, h2 z0, h2 s1, h2 z1, h2 s2, h2 z2, h2 s3,
-                                       h2 z3) {
-  u4 r;
-  r.x = deq_pair(bytes01(d.x), s0, z0);
-  r.y = deq_pair(bytes23(d.x), s1, z1);
-  r.z = deq_pair(bytes01(d.y), s2, z2);
-  r.w = deq_pair(bytes23(d.y), s3, z3);
-  return r;
 }
 
 __device__ __forceinline__ float wave_max16(float v) {
@@ -93,18 +66,35 @@ __device__ __forceinline__ float2 cmul(float2 a, float2 b) {
   return make_float2(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x);
 }
 
-__device__ __forceinline__ _Float16 load_q(const void* q, int64_t idx, int bf16) {
-  uint16_t u = static_cast<const uint16_t*>(q)[idx];
-  if (bf16) {
-    float f = __uint_as_float(static_cast<uint32_t>(u) << 16);
-    return (_Float16)f;
-  }
-  return __builtin_bit_cast(_Float16, u);
+__device__ __forceinline__ float load_qf(const uint16_t* q, int idx, int bf16) {
+  const uint16_t u = q[idx];
+  if (bf16) return __uint_as_float(static_cast<uint32_t>(u) << 16);
+  return (float)__builtin_bit_cast(_Float16, u);
+}
+
+// A value the compiler cannot fold into instructions as a literal, so that it
+// stays in a register (lets v_and_or_b32 take it as an operand).
+__device__ __forceinline__ uint32_t opaque_u32(uint32_t v) {
+  uint32_t r;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(r) : "s"(v));
+  return r;
+}
+
+// 4-bit word of pairs (nibble k, nibble k+4), k = 0..3, with the nibble mask
+// held in a register.
+__device__ __forceinline__ u4 deq_int4m(uint32_t w, uint32_t mask, h2 s0, h2 z0, h2 s1, h2 z1,
+                                        h2 s2, h2 z2, h2 s3, h2 z3) {
+  u4 r;
+  r.x = deq_pair((w & mask) | 0x64006400u, s0, z0);
+  r.y = deq_pair(((w >> 4) & mask) | 0x64006400u, s1, z1);
+  r.z = deq_pair(((w >> 8) & mask) | 0x64006400u, s2, z2);
+  r.w = deq_pair(((w >> 12) & mask) | 0x64006400u, s3, z3);
+  return r;
 }
 
 // LDS layout of the split kernel (byte offsets); identical on the host.
 struct SplitLds {
-  int frag, qc, red, alpha, flag, rot, loop, raw, vcode, vmeta, pbuf, rope, total;
+  int frag, qc, red, alpha, flag, rot, qmap, loop, raw, vcode, vmeta, pbuf, rope, total;
 };
 
 // vcode_bytes: value codes of one step (kStepTokens tokens), a multiple of 16.
@@ -117,14 +107,15 @@ __host__ __device__ inline SplitLds split_lds(int frags, int nql, int head_dim, 
   L.alpha = L.red + kTokenGroups * ct * 16 * 4;
   L.flag = L.alpha + ct * 16 * 4;
   L.rot = L.flag + 16;
-  L.loop = L.rot + 64 * 8;
+  L.qmap = L.rot + 64 * 8;
+  L.loop = L.qmap + 64 * 4;
   L.raw = L.loop;
   L.vcode = L.raw + kWaves * raw_bytes;
   L.vmeta = L.vcode + vcode_bytes;
   L.pbuf = L.vmeta + 4 * v_ng * 128;
   int loop_end = L.pbuf + kTokenGroups * ct * 1024;
   L.rope = L.loop;   // RoPE tables (prologue only) alias the loop area
-  int rope_end = L.rope + (64 + 16 * 64 + 8 * 64) * 8;
+  int rope_end = L.rope + (16 * 64 + 8 * 64) * 8;
   L.total = loop_end > rope_end ? loop_end : rope_end;
   return L;
 }
@@ -171,41 +162,56 @@ __device__ __forceinline__ u4 deq_int8p(u2 d, h2 s0, h2 z0, h2 s1, h2 z1, h2 s2,
   return r;
 }
 
+// Packed fp16 cos/sin of one lane's four RoPE frequencies j0 + e (j0 = 16 kq +
+// 4 quad) at one token offset: c01 = (cos j0, cos j0+1), c23, s01, s23.
+struct CS4 {
+  h2 c01, c23, s01, s23;
+};
+
+// 4-bit codes x (nibble k = channel k) -> bytes: nibbles 0,2,4,6 in the first
+// word, 1,3,5,7 in the second, so the 8-bit dequantizer applies; the element
+// order becomes channels 0,2,4,6,1,3,5,7 (the up-projection fragments match).
+__device__ __forceinline__ u2 nibble_bytes(uint32_t x) {
+  return (u2){x & 0x0F0F0F0Fu, (x >> 4) & 0x0F0F0F0Fu};
+}
+
 // One KV head with KB k-blocks for the wave's 32 tokens: dequantize the key
 // latents from the LDS staging area into MFMA operands, rebuild the keys
 // (16 rows of the head dimension per MFMA, both halves of every RoPE pair),
-// rotate, and accumulate the scores of the head's query heads.  The
-// reconstruction of score k-block kbs+1 is issued before the rotation of
+// rotate them by the lane's fixed in-step offset (the step's base position is
+// applied to the query), and accumulate the scores of the head's query heads.
+// The reconstruction of score k-block kbs+1 is issued before the rotation of
 // kbs so the matrix cores and the vector ALUs overlap.
 template <int D, int QM, int CTH, int KB>
 __device__ __forceinline__ void key_head(const KHeadInfo& kh, const uint8_t* raw, const h8* frag,
                                          const _Float16* qc, int qzero, int gl, int ct0, int G,
                                          int lane, int col, int quad,
-                                         const float2 (&cs)[2][4 * (D / 32)],
-                                         f4 (&acc_s)[2][CTH]) {
+                                         const CS4 (&cs)[2][D / 32], f4 (&acc_s)[2][CTH]) {
   constexpr int NKBS = D / 32;
   constexpr int QS = D + 8;                  // padded query row (halves)
   const uint8_t* rc = raw + kh.raw_code;
   const uint8_t* rm = raw + kh.raw_meta;
   const int rb16 = 16 * kh.row_bytes;        // bytes of one 16-token block
-  // all LDS reads of the head first, then the dequantization
+  // all LDS reads of the head first, then the dequantization.  Lanes whose
+  // chunk lies beyond the rank read chunk 0 (finite values that meet zero
+  // up-projection rows).
   u2 code[2][KB];
   uint32_t meta[2][KB];
   u4 cf[2][KB];
-  bool valid[KB], is8[KB];
+  bool is8[KB];
 #pragma unroll
   for (int kb = 0; kb < KB; ++kb) {
     const int c = 4 * kb + quad;
-    valid[kb] = (kb < KB - 1) || (8 * c < kh.rank);
+    const bool valid = (kb < KB - 1) || (8 * c < kh.rank);
     if (QM == STARKV_Q_F16) {
-      const int off = valid[kb] ? kb * 1024 + lane * 16 : 0;
+      const int off = valid ? kb * 1024 + lane * 16 : 0;
 #pragma unroll
       for (int s = 0; s < 2; ++s) cf[s][kb] = *reinterpret_cast<const u4*>(rc + s * rb16 + off);
     } else {
-      is8[kb] = c < kh.n8;
+      is8[kb] = QM == STARKV_Q_MIX8_4 && c < kh.n8;
       int off = is8[kb] ? kb * 512 + lane * 8 : kh.n8 * 64 + kb * 256 + lane * 4;
       int gi = is8[kb] ? 0 : kh.ng8 + (c - kh.n8) / 4;
-      if (!valid[kb]) { off = 0; gi = 0; }
+      if (!valid) { off = 0; gi = 0; }
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
         meta[s][kb] = *reinterpret_cast<const uint32_t*>(rm + (s * kh.ngroups + gi) * 64 + col * 4);
@@ -225,10 +231,16 @@ __device__ __forceinline__ void key_head(const KHeadInfo& kh, const uint8_t* raw
         const uint32_t mz = meta[s][kb];
         const h2 sv = as_h2(perm(mz, mz, 0x01000100u));
         const h2 zv = as_h2(perm(mz, mz, 0x03020302u));
-        if (QM == STARKV_Q_MIX8_4 && is8[kb]) v = deq_int8p(code[s][kb], sv, zv, sv, zv, sv, zv, sv, zv);
-        else v = deq_int4(code[s][kb].x, sv, zv, sv, zv, sv, zv, sv, zv);
+        u2 d = code[s][kb];
+        const u2 nb = nibble_bytes(d.x);
+        if (QM == STARKV_Q_INT4) {
+          d = nb;
+        } else {
+          d.x = is8[kb] ? d.x : nb.x;
+          d.y = is8[kb] ? d.y : nb.y;
+        }
+        v = deq_int8p(d, sv, zv, sv, zv, sv, zv, sv, zv);
       }
-      if (!valid[kb]) v = (u4){0, 0, 0, 0};
       xop[s][kb] = __builtin_bit_cast(h8, v);
     }
   }
@@ -255,26 +267,62 @@ __device__ __forceinline__ void key_head(const KHeadInfo& kh, const uint8_t* raw
         }
       }
     }
-    if (kbs > 0) {           // rotate and score k-block kbs-1
+    if (kbs > 0) {           // rotate and score k-block kbs-1 (packed fp16)
       const int kq = kbs - 1, buf = kq & 1;
       const h8 qf = *reinterpret_cast<const h8*>(qc + (mine ? qrow + (kq * 4 + quad) * 8 : qzero));
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
+        const CS4& r = cs[s][kq];
+        const f4 a = klo[buf][s], bb = khi[buf][s];
+        const h2 a01 = __builtin_convertvector((f2){a[0], a[1]}, h2);
+        const h2 a23 = __builtin_convertvector((f2){a[2], a[3]}, h2);
+        const h2 b01 = __builtin_convertvector((f2){bb[0], bb[1]}, h2);
+        const h2 b23 = __builtin_convertvector((f2){bb[2], bb[3]}, h2);
         u4 kr;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float2 r = cs[s][4 * kq + e];
-          const float a = klo[buf][s][e], bb = khi[buf][s][e];
-          const float bs = bb * r.y, as = a * r.y;
-          const _Float16 ra = (_Float16)__builtin_fmaf(a, r.x, -bs);
-          const _Float16 rb = (_Float16)__builtin_fmaf(bb, r.x, as);
-          kr[e] = as_u32((h2){ra, rb});
-        }
+        kr[0] = as_u32(__builtin_elementwise_fma(a01, r.c01, -(b01 * r.s01)));
+        kr[1] = as_u32(__builtin_elementwise_fma(a23, r.c23, -(b23 * r.s23)));
+        kr[2] = as_u32(__builtin_elementwise_fma(b01, r.c01, a01 * r.s01));
+        kr[3] = as_u32(__builtin_elementwise_fma(b23, r.c23, a23 * r.s23));
         const h8 kop = __builtin_bit_cast(h8, kr);
 #pragma unroll
         for (int c = 0; c < CTH; ++c)
           if (CTH == 1 || c == ct_g) acc_s[s][c] = mfma16(kop, qf, acc_s[s][c]);
       }
+    }
+  }
+}
+
+// The group's query heads rotated to the step's base position t (RoPE applied to
+// the query as R(t)^T q, so that q . R(t + u) k = (R(t)^T q) . (R(u) k)), one
+// padded fp16 row per head, permuted so that lane (col, quad) of score k-block
+// kbs reads one 16-byte vector: elements e = q'[j0 + e], 4 + e = q'[j0 + e + D/2],
+// j0 = 16*kbs + 4*quad.  Thread t owns vectors t, t + 512, .. (frequencies
+// j0 .. j0+3 fixed per thread).
+template <int D, int NQV>
+__device__ __forceinline__ void store_rotated_q(_Float16* qc, int nql, int tid,
+                                                const float (&qo)[NQV][8], const float2 (&bs)[4]) {
+  constexpr int QS = D + 8;
+  constexpr int NV = D / 8;                  // vectors per query row
+#pragma unroll
+  for (int v = 0; v < NQV; ++v) {
+    const int vi = tid + v * kThreads;
+    const int il = vi / NV, jg = vi % NV;
+    if (il < nql) {
+      u4 o;
+#pragma unroll
+      for (int e = 0; e < 4; e += 2) {
+        float lo[2], hi[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const float a = qo[v][e + u], b = qo[v][4 + e + u];
+          const float c = bs[e + u].x, s = bs[e + u].y;
+          lo[u] = __builtin_fmaf(a, c, b * s);
+          hi[u] = __builtin_fmaf(b, c, -(a * s));
+        }
+        o[e / 2] = as_u32(__builtin_convertvector((f2){lo[0], lo[1]}, h2));
+        o[2 + e / 2] = as_u32(__builtin_convertvector((f2){hi[0], hi[1]}, h2));
+      }
+      *reinterpret_cast<u4*>(qc + il * QS + jg * 8) = o;
     }
   }
 }
@@ -286,9 +334,9 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   extern __shared__ __align__(16) uint8_t smem[];
   constexpr int CTH = (CT + 1) / 2;
   constexpr int NKBS = D / 32;   // score k-blocks (head dimension / 32)
-  constexpr int NF = 4 * NKBS;   // RoPE frequencies held per lane
   constexpr int HALF = D / 2;
   constexpr int QS = D + 8;
+  constexpr int NQV = (16 * CT * (D / 8) + kThreads - 1) / kThreads;   // query vectors per thread
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -299,7 +347,6 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   const int g0 = p.hg_first[hg], g1 = p.hg_first[hg + 1], gm = p.hg_mid[hg];
   const int G = p.group_q;
   const int nql = (g1 - g0) * G;
-  const int q0 = g0 * G;
   const int ct_half = ((gm - g0) * G + 15) / 16;          // score tiles of the first half
   const int ct0 = hh ? ct_half : 0;                        // first score tile of this half
   const int ctn = hh ? (nql + 15) / 16 - ct_half : ct_half; // its tile count
@@ -321,13 +368,13 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   float* alpha_s = reinterpret_cast<float*>(smem + LL.alpha);
   int* flag_s = reinterpret_cast<int*>(smem + LL.flag);
   float2* rot_s = reinterpret_cast<float2*>(smem + LL.rot);        // [64] step rotations
+  int* qmap = reinterpret_cast<int*>(smem + LL.qmap);             // slot-local -> query head
   uint8_t* raw = smem + LL.raw + w * raw_bytes;
   uint8_t* vcode = smem + LL.vcode;
   uint8_t* vmeta = smem + LL.vmeta;
   h8* pbuf = reinterpret_cast<h8*>(smem + LL.pbuf);
-  float2* rope_base = reinterpret_cast<float2*>(smem + LL.rope);   // [64]
-  float2* rope_col = rope_base + 64;                                // [16][64]
-  float2* rope_ws = rope_col + 16 * 64;                             // [8][64]
+  float2* rope_col = reinterpret_cast<float2*>(smem + LL.rope);   // [16][64]
+  float2* rope_ws = rope_col + 16 * 64;                           // [8][64]
   const int qzero = nql * QS;
 
   // ---------------------------------------------------------------- prologue
@@ -336,17 +383,15 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     const int n = p.hg_frags[hg] * 64;
     for (int i = tid; i < n; i += kThreads) f[i] = (u4){0, 0, 0, 0};
   }
-  // RoPE angle tables: rotation by t*omega_j composed as
-  // base(t_begin) * step-of-wave(32*tg + 16s) * within-subtile(col).
+  if (tid < nql) qmap[tid] = p.kh[g0 + tid / G].head * G + tid % G;
+  if (tid < 8) qc[qzero + tid] = (_Float16)0.0f;
+  // RoPE tables: the lane's in-step offset u = 32*tg + 16*s + col composed as
+  // the subtile rotation (16*(2*tg + s)) times the column rotation (col), and
+  // the rotation by one step (kStepTokens) for the query's base position.
   {
     const double l2t = p.log2_theta;
     for (int i = tid; i < HALF; i += kThreads) {
       const double om = exp2(-(2.0 * i / D) * l2t);
-      double a = (double)t_begin * om;
-      a -= 6.283185307179586476925286766559 * floor(a * 0.15915494309189533576888376337251);
-      double sa, ca;
-      sincos(a, &sa, &ca);
-      rope_base[i] = make_float2((float)ca, (float)sa);
       float ss, cs;
       sincosf((float)(kStepTokens * om), &ss, &cs);
       rot_s[i] = make_float2(cs, ss);
@@ -366,25 +411,40 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       rope_ws[k * 64 + j] = make_float2(cs, ss);
     }
   }
-  // Query heads of the group in fp16, one padded row per head, permuted so that
-  // lane (col, quad) of score k-block kbs reads one 16-byte vector: element
-  // 2e = q[j], 2e+1 = q[j + D/2], j = 16*kbs + 4*quad + e.  A zero vector follows
-  // for lanes whose column is not a query head of the KV head being scored.
-  for (int i = tid; i < nql * HALF; i += kThreads) {
-    const int il = i / HALF, r = i % HALF;          // r = kbs*16 + quad*4 + e
-    const int kbs = r / 16, qd = (r / 4) % 4, e = r % 4;
-    const int j = 16 * kbs + 4 * qd + e;
-    const int64_t src = ((int64_t)b * p.n_q + q0 + il) * D;
-    _Float16* dst = qc + il * QS + (kbs * 4 + qd) * 8 + 2 * e;
-    dst[0] = load_q(p.q, src + j, p.q_bf16);
-    dst[1] = load_q(p.q, src + j + HALF, p.q_bf16);
+  __syncthreads();   // qmap, tables
+  // this thread's query vectors (fp32) and the base rotation of its four
+  // frequencies at t_begin (angle reduced in fp64)
+  float qo[NQV][8];
+  float2 bs[4];
+  {
+    const int jg = tid % (D / 8);
+    const int j0 = 4 * jg;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const double om = exp2(-(2.0 * (j0 + e) / D) * p.log2_theta);
+      double a = (double)t_begin * om;
+      a -= 6.283185307179586476925286766559 * floor(a * 0.15915494309189533576888376337251);
+      double sa, ca;
+      sincos(a, &sa, &ca);
+      bs[e] = make_float2((float)ca, (float)sa);
+    }
+#pragma unroll
+    for (int v = 0; v < NQV; ++v) {
+      const int il = (tid + v * kThreads) / (D / 8);
+      const int qh = il < nql ? qmap[il] : 0;
+      const uint16_t* qs = static_cast<const uint16_t*>(p.q) + ((int64_t)b * p.n_q + qh) * D;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        qo[v][e] = load_qf(qs, j0 + e, p.q_bf16);
+        qo[v][4 + e] = load_qf(qs, j0 + e + HALF, p.q_bf16);
+      }
+    }
   }
-  if (tid < 8) qc[qzero + tid] = (_Float16)0.0f;
-  __syncthreads();
-  // Up-projection fragments.  Fragment (head, m-tile mt, k-block kb), lane
+  store_rotated_q<D, NQV>(qc, nql, tid, qo, bs);
+  // Up-projection fragments.  Fragment (slot, m-tile mt, k-block kb), lane
   // (jj, kq): 8 halves = B_k[row][16*mt + jj] for the 8 channels of chunk
-  // 4*kb + kq, ordered as the key operand delivers them (4-bit chunks pair
-  // channels (k, k+4); 8-bit and fp16 chunks are in order).
+  // 4*kb + kq, in the order the key operand delivers them (4-bit chunks:
+  // channels 0,2,4,6,1,3,5,7; 8-bit and fp16 chunks in order).
   for (int gg = g0; gg < g1; ++gg) {
     const KHeadInfo& kh = p.kh[gg];
     const int nvec = kh.rank * (D / 8);
@@ -395,7 +455,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       const int c = row / 8, wi = row % 8;
       const int kb = c / 4, kq = c % 4;
       int e = wi;
-      if (QM != STARKV_Q_F16 && c >= kh.n8) e = (wi < 4) ? 2 * wi : 2 * (wi - 4) + 1;
+      if (QM != STARKV_Q_F16 && c >= kh.n8) e = (wi % 2 == 0) ? wi / 2 : 4 + wi / 2;
       for (int u = 0; u < 8; ++u) {
         const int j = 8 * j8 + u;
         const int mt = j / 16, jj = j % 16;
@@ -405,19 +465,30 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       }
     }
   }
-  float2 cs[2][NF];
+  // the lane's fixed key rotations, packed fp16
+  CS4 cs[2][NKBS];
 #pragma unroll
-  for (int f = 0; f < NF; ++f) {
-    const int j = 16 * (f / 4) + 4 * quad + (f % 4);
+  for (int s = 0; s < 2; ++s)
 #pragma unroll
-    for (int s = 0; s < 2; ++s)
-      cs[s][f] = cmul(cmul(rope_base[j], rope_ws[(2 * tg + s) * 64 + j]), rope_col[col * 64 + j]);
-  }
+    for (int kq = 0; kq < NKBS; ++kq) {
+      float cc[4], ss[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int j = 16 * kq + 4 * quad + e;
+        const float2 r = cmul(rope_ws[(2 * tg + s) * 64 + j], rope_col[col * 64 + j]);
+        cc[e] = r.x;
+        ss[e] = r.y;
+      }
+      cs[s][kq].c01 = __builtin_convertvector((f2){cc[0], cc[1]}, h2);
+      cs[s][kq].c23 = __builtin_convertvector((f2){cc[2], cc[3]}, h2);
+      cs[s][kq].s01 = __builtin_convertvector((f2){ss[0], ss[1]}, h2);
+      cs[s][kq].s23 = __builtin_convertvector((f2){ss[2], ss[3]}, h2);
+    }
   __syncthreads();   // RoPE tables are dead from here on (the loop area reuses them)
 
   // ---------------------------------------------------------------- prefetch setup
   // Key staging: the wave's 32 tokens of every key head of its half, codes then
-  // meta per head, as one contiguous LDS area filled by flat 16-byte loads.
+  // meta per head, as one contiguous LDS area filled by flat 16-byte copies.
   const uint8_t* ld_ptr[kMaxLoads];
   int ld_stride[kMaxLoads];
   {
@@ -480,6 +551,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       copy_to_lds(vmeta, p.cache + p.v_meta_off + (vblk0 + (int64_t)step * 4) * p.v_ng * 128,
                   vmeta_bytes, w, lane);
   };
+  const uint32_t nib_mask = opaque_u32(0x000F000Fu);
 
   // ---------------------------------------------------------------- main loop
   float m_run[CTH], l_part[CTH];
@@ -503,6 +575,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 
   load_k(0);
   load_v(0);
+  __syncthreads();   // rotated queries of step 0 and the fragments visible
 
   for (int step = 0; step < n_steps; ++step) {
     const int t_step = t_begin + step * kStepTokens;
@@ -531,12 +604,6 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     }
     // the staging area has been read: copy the next step's keys into it
     if (step + 1 < n_steps) load_k(step + 1);
-#pragma unroll
-    for (int f = 0; f < NF; ++f) {
-      const float2 r = rot_s[16 * (f / 4) + 4 * quad + (f % 4)];
-      cs[0][f] = cmul(cs[0][f], r);
-      cs[1][f] = cmul(cs[1][f], r);
-    }
 
     // ------------------------------------------ online softmax (log2 domain)
     float x[CTH][2][4];
@@ -562,7 +629,13 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       mx = wave_max16(mx);
       if (quad == 0) red[(tg * CT + ct0 + c) * 16 + col] = mx;
     }
-    __syncthreads();   // (1) tile maxima visible
+    __syncthreads();   // (1) tile maxima visible; every wave is done with the queries
+    if (step + 1 < n_steps) {   // rotate the queries to the next step's base position
+      const int j0 = 4 * (tid % (D / 8));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) bs[e] = cmul(bs[e], rot_s[j0 + e]);
+      store_rotated_q<D, NQV>(qc, nql, tid, qo, bs);
+    }
     bool rescale = false;
 #pragma unroll
     for (int c = 0; c < CTH; ++c) {
@@ -578,10 +651,10 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       float ls = 0.0f;
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        const _Float16 p0 = (_Float16)__builtin_amdgcn_exp2f(x[c][k / 2][2 * (k % 2)] - mn);
-        const _Float16 p1 = (_Float16)__builtin_amdgcn_exp2f(x[c][k / 2][2 * (k % 2) + 1] - mn);
-        ls += (float)p0 + (float)p1;
-        pk[k] = as_u32((h2){p0, p1});
+        const float e0 = __builtin_amdgcn_exp2f(x[c][k / 2][2 * (k % 2)] - mn);
+        const float e1 = __builtin_amdgcn_exp2f(x[c][k / 2][2 * (k % 2) + 1] - mn);
+        ls += e0 + e1;
+        pk[k] = as_u32(__builtin_convertvector((f2){e0, e1}, h2));
       }
       l_part[c] = l_part[c] * al + ls;
       pbuf[(tg * CT + ct) * 64 + lane] = __builtin_bit_cast(h8, pk);
@@ -642,16 +715,16 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
                           as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
           } else if (lo_ch >= p.v_ro) {
             const uint32_t d = *reinterpret_cast<const uint32_t*>(vb + v_off[t]);
-            v = deq_int4(d, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y), as_h2(sv.z),
-                         as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
+            v = deq_int4m(d, nib_mask, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y),
+                          as_h2(sv.z), as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
           } else if (16 * nt + col < p.v_ro) {
             const u2 d = *reinterpret_cast<const u2*>(vb + v_off[t]);
             v = deq_int8p(d, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y), as_h2(sv.z),
                           as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
           } else {
             const uint32_t d = *reinterpret_cast<const uint32_t*>(vb + v_off[t]);
-            v = deq_int4(d, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y), as_h2(sv.z),
-                         as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
+            v = deq_int4m(d, nib_mask, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y),
+                          as_h2(sv.z), as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
           }
         }
         if (!full) v &= vmask;
@@ -680,7 +753,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     if (c >= ctn) break;
     const int il = (ct0 + c) * 16 + col;
     if (il < nql) {
-      float2* cd = p.cand + (pbase + q0 + il) * kCand + (tg * 4 + quad) * 2;
+      float2* cd = p.cand + (pbase + qmap[il]) * kCand + (tg * 4 + quad) * 2;
       cd[0] = make_float2(b1x[c], __int_as_float(t_begin + (int)(bt[c] & 0xFFFFu)));
       cd[1] = make_float2(b2x[c], __int_as_float(t_begin + (int)(bt[c] >> 16)));
     }
@@ -694,7 +767,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
         float lt = 0.0f;
 #pragma unroll
         for (int g = 0; g < kTokenGroups; ++g) lt += red[(g * CT + ct0 + c) * 16 + col];
-        float* dst = p.part + (pbase + q0 + il) * p.part_stride + p.rv;
+        float* dst = p.part + (pbase + qmap[il]) * p.part_stride + p.rv;
         dst[0] = m_run[c];
         dst[1] = lt;
       }
@@ -709,7 +782,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int il = c * 16 + 4 * quad + e;
-          if (il < nql) p.part[(pbase + q0 + il) * p.part_stride + 16 * nt + col] = acc_v[c][t][e];
+          if (il < nql) p.part[(pbase + qmap[il]) * p.part_stride + 16 * nt + col] = acc_v[c][t][e];
         }
       }
     }

@@ -64,7 +64,8 @@ struct starkv_plan {
   int32_t hg_raw[STARKV_MAX_KV_HEADS];
   int32_t hg_mid[STARKV_MAX_KV_HEADS];
   int32_t hh_raw[STARKV_MAX_KV_HEADS][2];
-  KHeadInfo kh[STARKV_MAX_KV_HEADS];
+  KHeadInfo kh[STARKV_MAX_KV_HEADS];      // per slot (see the decode kernel shape)
+  int32_t bk_row[STARKV_MAX_KV_HEADS];    // per KV head: first row in B_k
   int32_t order[STARKV_MAX_KV_HEADS];
   int32_t cls[STARKV_MAX_KV_HEADS][2][5];
   int32_t lds_bytes;
@@ -178,11 +179,14 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
   int ntw = (NT + kWaves - 1) / kWaves;
   ntw = ntw <= 1 ? 1 : ntw <= 2 ? 2 : ntw <= 4 ? 4 : 8;
   P->ntw = ntw;
+  KHeadInfo info[STARKV_MAX_KV_HEADS];   // per KV head, in head order
   int bk_row = 0;
   for (int g = 0; g < c->n_kv_heads; ++g) {
-    KHeadInfo& k = P->kh[g];
+    KHeadInfo& k = info[g];
+    std::memset(&k, 0, sizeof(k));
     k.code_off = L.key_code_offset[g];
     k.meta_off = L.key_meta_offset[g];
+    k.head = g;
     k.rank = c->key_rank[g];
     k.nkb = (k.rank + 31) / 32;
     k.n8 = L.key_outlier_channels[g] / 8;
@@ -192,23 +196,42 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
     k.bk_row = bk_row;
     bk_row += k.rank;
   }
-  // A group of KV heads is processed by one workgroup in two halves split at a
-  // score-tile boundary (16 query heads); each half's key staging is per wave.
-  auto half_split = [&](int g_first, int g_last) {
-    const int tiles = ((g_last - g_first) * G + 15) / 16;
-    if (tiles < 2) return g_last;
-    return g_first + (((tiles + 1) / 2) * 16) / G;
+  // A group of KV heads [a, b) is processed by one workgroup whose waves split
+  // the heads into two halves; each half owns whole score tiles (16 query
+  // heads).  The heads are assigned to the halves to balance their key work
+  // (about 2 + k-blocks units per head: the rotation is per head, the
+  // reconstruction per k-block); slots list half 0's heads, then half 1's.
+  auto assign = [&](int a, int b, int* slots, int* n_first) {
+    const int n = b - a;
+    const int tiles = (n * G + 15) / 16;
+    const int cap0 = tiles < 2 ? n : std::min(n, ((tiles + 1) / 2) * 16 / G);
+    int order_idx[STARKV_MAX_KV_HEADS];
+    for (int i = 0; i < n; ++i) order_idx[i] = a + i;
+    std::stable_sort(order_idx, order_idx + n,
+                     [&](int x, int y) { return info[x].nkb > info[y].nkb; });
+    int h0[STARKV_MAX_KV_HEADS], h1[STARKV_MAX_KV_HEADS], n0 = 0, n1 = 0, w0 = 0, w1 = 0;
+    for (int i = 0; i < n; ++i) {
+      const int g = order_idx[i], cost = 2 + info[g].nkb;
+      const bool to0 = n0 < cap0 && (n1 >= n - cap0 || w0 <= w1);
+      if (to0) { h0[n0++] = g; w0 += cost; } else { h1[n1++] = g; w1 += cost; }
+    }
+    std::sort(h0, h0 + n0);
+    std::sort(h1, h1 + n1);
+    for (int i = 0; i < n0; ++i) slots[i] = h0[i];
+    for (int i = 0; i < n1; ++i) slots[n0 + i] = h1[i];
+    *n_first = n0;
   };
-  auto raw_of = [&](int a, int b) {
+  auto raw_of = [&](const int* heads, int n) {
     int raw = 0;
-    for (int g = a; g < b; ++g) raw += 32 * P->kh[g].row_bytes + 2 * P->kh[g].ngroups * 64;
+    for (int i = 0; i < n; ++i) raw += 32 * info[heads[i]].row_bytes + 2 * info[heads[i]].ngroups * 64;
     return raw;
   };
   auto group_fits = [&](int g_first, int g_last, int ct, int* frags_out, int* raw_out) {
     int frags = 0;
-    for (int g = g_first; g < g_last; ++g) frags += (D / 16) * P->kh[g].nkb;
-    const int mid = half_split(g_first, g_last);
-    const int raw = std::max(raw_of(g_first, mid), raw_of(mid, g_last));
+    for (int g = g_first; g < g_last; ++g) frags += (D / 16) * info[g].nkb;
+    int slots[STARKV_MAX_KV_HEADS], n0;
+    assign(g_first, g_last, slots, &n0);
+    const int raw = std::max(raw_of(slots, n0), raw_of(slots + n0, g_last - g_first - n0));
     *frags_out = frags;
     *raw_out = raw;
     const int nql = (g_last - g_first) * G;
@@ -252,31 +275,34 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
     group_fits(a, b, P->ct, &fr, &rw);
     P->hg_frags[h] = fr;
     P->hg_raw[h] = rw;
-    const int mid = half_split(a, b);
+    int slots[STARKV_MAX_KV_HEADS], n0;
+    assign(a, b, slots, &n0);
+    const int mid = a + n0;          // first slot of half 1
     P->hg_mid[h] = mid;
-    P->hh_raw[h][0] = raw_of(a, mid);
-    P->hh_raw[h][1] = raw_of(mid, b);
+    P->hh_raw[h][0] = raw_of(slots, n0);
+    P->hh_raw[h][1] = raw_of(slots + n0, b - a - n0);
     int fb = 0;
-    for (int g = a; g < b; ++g) {
-      KHeadInfo& k = P->kh[g];
+    for (int sl = a; sl < b; ++sl) {
+      KHeadInfo& k = P->kh[sl];
+      k = info[slots[sl - a]];
       k.frag_base = fb;
       fb += (D / 16) * k.nkb;
     }
     for (int half = 0; half < 2; ++half) {
       const int ha = half ? mid : a, hb = half ? b : mid;
       int ro = 0;
-      for (int g = ha; g < hb; ++g) {
-        KHeadInfo& k = P->kh[g];
+      for (int sl = ha; sl < hb; ++sl) {
+        KHeadInfo& k = P->kh[sl];
         k.raw_code = ro;
         ro += 32 * k.row_bytes;
         k.raw_meta = ro;
         ro += 2 * k.ngroups * 64;
       }
-      // processing order inside the half: heads sorted by k-block count
+      // processing order inside the half: slots sorted by k-block count
       for (int kk = 1; kk <= 4; ++kk) {
         P->cls[h][half][kk - 1] = pos;
-        for (int g = ha; g < hb; ++g)
-          if (P->kh[g].nkb == kk) P->order[pos++] = g;
+        for (int sl = ha; sl < hb; ++sl)
+          if (P->kh[sl].nkb == kk) P->order[pos++] = sl;
       }
       P->cls[h][half][4] = pos;
     }
@@ -284,6 +310,7 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
     const int lds = split_lds_bytes(fr, nql, D, P->ct, rw, L.value_groups, L.value_row_bytes);
     if (lds > P->lds_bytes) P->lds_bytes = lds;
   }
+  for (int g = 0; g < c->n_kv_heads; ++g) P->bk_row[g] = info[g].bk_row;
   *out = P;
   g_last_error.clear();
   return STARKV_OK;
@@ -468,7 +495,7 @@ starkv_status starkv_decode_combine(const starkv_plan* P, const void* cache, con
     p.k_ro[g] = L.key_outlier_channels[g];
     p.k_ng[g] = L.key_groups[g];
     p.k_rb[g] = L.key_row_bytes[g];
-    p.k_bkrow[g] = P->kh[g].bk_row;
+    p.k_bkrow[g] = P->bk_row[g];
   }
   p.v_code_off = L.value_code_offset;
   p.v_meta_off = L.value_meta_offset;

@@ -17,6 +17,7 @@ constexpr int kStepTokens = kTokenGroups * kWaveTokens;
 struct KHeadInfo {
   int64_t code_off;      // key code plane
   int64_t meta_off;      // key meta plane
+  int32_t head;          // KV head index (query heads head*G .. head*G + G - 1)
   int32_t rank;
   int32_t nkb;           // 32-channel k-blocks: ceil(rank/32)
   int32_t n8;            // 8-bit chunks (8 channels each)
@@ -46,17 +47,19 @@ struct DecodeParams {
   int64_t v_code_off, v_meta_off;
   int32_t rv, v_ro, v_ng8, v_ng, v_row_bytes;
   int32_t part_stride;         // floats per (b, split, query head)
-  // head groups (blockIdx.z); each group is processed in two halves split at a
-  // score-tile boundary (16 query heads), one half per wave of a token group
+  // head groups (blockIdx.z).  A group occupies the slots hg_first[hg] ..
+  // hg_first[hg+1]-1; slot s holds KV head kh[s].head.  Each group is processed
+  // in two halves (slots before and from hg_mid), each owning whole score tiles
+  // of 16 query columns (slot-local query column = slot * G + j).
   int32_t n_hg;
   int32_t hg_first[STARKV_MAX_KV_HEADS + 1];
-  int32_t hg_mid[STARKV_MAX_KV_HEADS];       // first KV head of the second half
+  int32_t hg_mid[STARKV_MAX_KV_HEADS];       // first slot of the second half
   int32_t hg_frags[STARKV_MAX_KV_HEADS];     // fragments used by the group
   int32_t hg_raw_bytes[STARKV_MAX_KV_HEADS]; // per-wave staging bytes (max over halves)
   int32_t hh_raw[STARKV_MAX_KV_HEADS][2];    // staging bytes of each half
-  KHeadInfo kh[STARKV_MAX_KV_HEADS];
-  // heads of every half in processing order, grouped by k-block count:
-  // order[cls[hg][h][k-1] .. cls[hg][h][k]) are the half's heads with k k-blocks
+  KHeadInfo kh[STARKV_MAX_KV_HEADS];         // per slot
+  // slots of every half in processing order, grouped by k-block count:
+  // order[cls[hg][h][k-1] .. cls[hg][h][k]) are the half's slots with k k-blocks
   int32_t order[STARKV_MAX_KV_HEADS];
   int32_t cls[STARKV_MAX_KV_HEADS][2][5];
 };
