@@ -12,8 +12,8 @@
 //       k-index is the head dimension (Sec. 3.1).
 //   The rows of the score tile are the 16 tokens and the columns are query
 //   heads: each KV head only fills its own columns, so up to 16 query heads
-//   share one tile.  The online softmax keeps one running maximum per query
-//   head for the whole workgroup (maxima exchanged through LDS), so the
+//   share one tile.  The online softmax keeps one reference maximum per query
+//   head for the whole workgroup (raised only when scores outgrow it), so the
 //   probabilities of all waves can be stacked into one matrix and multiplied
 //   with the shared value latent V' as one MFMA GEMM, each wave owning a slice
 //   of V' channels (the reordered value path of Sec. 3.3 and the stacked
@@ -50,6 +50,10 @@ __device__ __forceinline__ uint32_t deq_pair(uint32_t magic_pair, h2 s, h2 z) {
   h2 c = as_h2(magic_pair) - (h2){(_Float16)1024.0f, (_Float16)1024.0f};
   return as_u32(__builtin_elementwise_fma(c, s, z));
 }
+
+// Scores may exceed the shared softmax reference by this much (log2 units)
+// before it is raised: probabilities stay below 2^8 in fp16.
+constexpr float kLazyMargin = 8.0f;
 
 __device__ __forceinline__ float wave_max16(float v) {
   v = fmaxf(v, __shfl_xor(v, 16));
@@ -106,7 +110,7 @@ __host__ __device__ inline SplitLds split_lds(int frags, int nql, int head_dim, 
   L.red = L.qc + ((nql * (head_dim + 8) * 2 + 16 + 15) / 16) * 16;
   L.alpha = L.red + kTokenGroups * ct * 16 * 4;
   L.flag = L.alpha + ct * 16 * 4;
-  L.rot = L.flag + 16;
+  L.rot = L.flag + kWaves * 4;
   L.qmap = L.rot + 64 * 8;
   L.loop = L.qmap + 64 * 4;
   L.raw = L.loop;
@@ -143,7 +147,24 @@ __device__ __forceinline__ void wait_vm(int n) {
     case 6: __builtin_amdgcn_s_waitcnt(0x0F76); break;
     case 7: __builtin_amdgcn_s_waitcnt(0x0F77); break;
     case 8: __builtin_amdgcn_s_waitcnt(0x0F78); break;
+    case 9: __builtin_amdgcn_s_waitcnt(0x0F79); break;
+    case 10: __builtin_amdgcn_s_waitcnt(0x0F7A); break;
+    case 11: __builtin_amdgcn_s_waitcnt(0x0F7B); break;
+    case 12: __builtin_amdgcn_s_waitcnt(0x0F7C); break;
+    case 13: __builtin_amdgcn_s_waitcnt(0x0F7D); break;
+    case 14: __builtin_amdgcn_s_waitcnt(0x0F7E); break;
+    case 15: __builtin_amdgcn_s_waitcnt(0x0F7F); break;
     default: __builtin_amdgcn_s_waitcnt(0x0F70); break;   // vmcnt(0)
+  }
+}
+
+// The same by one wave: n_bytes (a multiple of 16) at src into lds, one copy
+// instruction per KiB, lane 0 active in each.
+__device__ __forceinline__ void copy_to_lds_wave(uint8_t* lds, const uint8_t* src, int n_bytes,
+                                                 int lane) {
+  for (int base = 0; base < n_bytes; base += 1024) {
+    if (base + lane * 16 < n_bytes)
+      __builtin_amdgcn_global_load_lds(src + base + lane * 16, lds + base, 16, 0, 0);
   }
 }
 
@@ -182,8 +203,15 @@ __device__ __forceinline__ u2 nibble_bytes(uint32_t x) {
 // applied to the query), and accumulate the scores of the head's query heads.
 // The reconstruction of score k-block kbs+1 is issued before the rotation of
 // kbs so the matrix cores and the vector ALUs overlap.
+// Per-head values used inside the step loop (wave-uniform, read from a lane of
+// the wave's head table so that the loop does no scalar memory loads).
+struct HeadRt {
+  int raw_code, raw_meta, row_bytes, rank, n8, ng8, ngroups, frag_base, gl;
+  int64_t code_off, meta_off;
+};
+
 template <int D, int QM, int CTH, int KB>
-__device__ __forceinline__ void key_head(const KHeadInfo& kh, const uint8_t* raw, const h8* frag,
+__device__ __forceinline__ void key_head(const HeadRt& kh, const uint8_t* raw, const h8* frag,
                                          const _Float16* qc, int qzero, int gl, int ct0, int G,
                                          int lane, int col, int quad,
                                          const CS4 (&cs)[2][D / 32], f4 (&acc_s)[2][CTH]) {
@@ -215,7 +243,14 @@ __device__ __forceinline__ void key_head(const KHeadInfo& kh, const uint8_t* raw
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
         meta[s][kb] = *reinterpret_cast<const uint32_t*>(rm + (s * kh.ngroups + gi) * 64 + col * 4);
-        code[s][kb] = *reinterpret_cast<const u2*>(rc + s * rb16 + off);
+        if (QM == STARKV_Q_INT4) {
+          code[s][kb].x = *reinterpret_cast<const uint32_t*>(rc + s * rb16 + off);
+        } else {
+          // 8-byte aligned reads only (a 4-bit lane takes its half of the word)
+          const u2 d = *reinterpret_cast<const u2*>(rc + s * rb16 + (off & ~7));
+          code[s][kb] = d;
+          if (off & 4) code[s][kb].x = d.y;
+        }
       }
     }
   }
@@ -301,6 +336,7 @@ __device__ __forceinline__ void key_head(const KHeadInfo& kh, const uint8_t* raw
 template <int D, int NQV>
 __device__ __forceinline__ void store_rotated_q(_Float16* qc, int nql, int tid,
                                                 const float (&qo)[NQV][8], const float2 (&bs)[4]) {
+  // qo holds the query already multiplied by log2(e)/sqrt(d)
   constexpr int QS = D + 8;
   constexpr int NV = D / 8;                  // vectors per query row
 #pragma unroll
@@ -359,7 +395,6 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   const int n_steps = (t_end - t_begin + kStepTokens - 1) / kStepTokens;
 
   const int raw_bytes = p.hg_raw_bytes[hg];
-  const int my_raw = p.hh_raw[hg][hh];
   const int vcode_bytes = kStepTokens * p.v_row_bytes;
   const SplitLds LL = split_lds(p.hg_frags[hg], nql, D, CT, raw_bytes, p.v_ng, vcode_bytes);
   h8* frag = reinterpret_cast<h8*>(smem + LL.frag);
@@ -435,8 +470,8 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       const uint16_t* qs = static_cast<const uint16_t*>(p.q) + ((int64_t)b * p.n_q + qh) * D;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        qo[v][e] = load_qf(qs, j0 + e, p.q_bf16);
-        qo[v][4 + e] = load_qf(qs, j0 + e + HALF, p.q_bf16);
+        qo[v][e] = load_qf(qs, j0 + e, p.q_bf16) * p.score_scale;
+        qo[v][4 + e] = load_qf(qs, j0 + e + HALF, p.q_bf16) * p.score_scale;
       }
     }
   }
@@ -488,41 +523,60 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 
   // ---------------------------------------------------------------- prefetch setup
   // Key staging: the wave's 32 tokens of every key head of its half, codes then
-  // meta per head, as one contiguous LDS area filled by flat 16-byte copies.
-  const uint8_t* ld_ptr[kMaxLoads];
-  int ld_stride[kMaxLoads];
-  {
-    const int64_t blk16 = (int64_t)b * (p.cap_pad / 16) + (t_begin + 32 * tg) / 16;
-    const int ha = hh ? gm : g0, hb = hh ? g1 : gm;
+  // meta per head, copied straight into the wave's LDS area.  A head's copy for
+  // the next step is issued as soon as the head has been processed, so the
+  // copies have most of a step to land.  Lane 0 of every issued copy is active,
+  // so the wave issues exactly n_kw copies per step.
+  const int64_t blk16 = (int64_t)b * (p.cap_pad / 16) + (t_begin + 32 * tg) / 16;
+  auto copy_head = [&](const HeadRt& kh, int step) {
+    const int64_t blk = blk16 + (int64_t)step * (kStepTokens / 16);
+    copy_to_lds_wave(raw + kh.raw_code, p.cache + kh.code_off + blk * 16 * kh.row_bytes,
+                     32 * kh.row_bytes, lane);
+    if (QM != STARKV_Q_F16)
+      copy_to_lds_wave(raw + kh.raw_meta, p.cache + kh.meta_off + blk * kh.ngroups * 64,
+                       2 * kh.ngroups * 64, lane);
+  };
+  // The half's heads in processing order (grouped by k-block count): lane i
+  // of the head table holds the i-th head's values.
+  const int c0 = p.cls[hg][hh][0];
+  int cls_end[NKBS + 1];
 #pragma unroll
-    for (int i = 0; i < kMaxLoads; ++i) {
-      const int off = (i * 64 + lane) * 16;
-      ld_ptr[i] = nullptr;
-      ld_stride[i] = 0;
-      if (off < my_raw) {
-        for (int gg = ha; gg < hb; ++gg) {
-          const KHeadInfo& kh = p.kh[gg];
-          const int ncode = 32 * kh.row_bytes, nmeta = 2 * kh.ngroups * 64;
-          if (off >= kh.raw_code && off < kh.raw_code + ncode) {
-            ld_ptr[i] = p.cache + kh.code_off + blk16 * 16 * kh.row_bytes + (off - kh.raw_code);
-            ld_stride[i] = (kStepTokens / 16) * 16 * kh.row_bytes;
-          } else if (nmeta > 0 && off >= kh.raw_meta && off < kh.raw_meta + nmeta) {
-            ld_ptr[i] = p.cache + kh.meta_off + blk16 * kh.ngroups * 64 + (off - kh.raw_meta);
-            ld_stride[i] = (kStepTokens / 16) * kh.ngroups * 64;
-          }
-        }
-      }
+  for (int k = 0; k <= NKBS; ++k) cls_end[k] = p.cls[hg][hh][k] - c0;
+  const int n_h = cls_end[NKBS];
+  int t_raw_code = 0, t_raw_meta = 0, t_rb = 0, t_rank = 0, t_n8 = 0, t_ng8 = 0, t_ng = 0,
+      t_fb = 0, t_gl = 0;
+  int64_t t_code = 0, t_meta = 0;
+  int n_kw = 0;
+  for (int i = 0; i < n_h; ++i) {
+    const int gg = p.order[c0 + i];
+    const KHeadInfo& kh = p.kh[gg];
+    n_kw += (32 * kh.row_bytes + 1023) / 1024;
+    if (QM != STARKV_Q_F16) n_kw += (2 * kh.ngroups * 64 + 1023) / 1024;
+    if (lane == i) {
+      t_raw_code = kh.raw_code; t_raw_meta = kh.raw_meta; t_rb = kh.row_bytes;
+      t_rank = kh.rank; t_n8 = kh.n8; t_ng8 = kh.ng8; t_ng = kh.ngroups;
+      t_fb = kh.frag_base; t_gl = gg - g0;
+      t_code = kh.code_off; t_meta = kh.meta_off;
     }
   }
-  // direct-to-LDS copies; lane 0 of every issued copy is active, so the wave
-  // issues exactly n_kw of them per step
-  const int n_kw = (my_raw + 1023) / 1024;
-  auto load_k = [&](int step) {
-#pragma unroll
-    for (int i = 0; i < kMaxLoads; ++i)
-      if (ld_ptr[i])
-        __builtin_amdgcn_global_load_lds(ld_ptr[i] + (int64_t)step * ld_stride[i], raw + i * 1024,
-                                         16, 0, 0);
+  auto head_rt = [&](int i) {
+    HeadRt h;
+    h.raw_code = __builtin_amdgcn_readlane(t_raw_code, i);
+    h.raw_meta = __builtin_amdgcn_readlane(t_raw_meta, i);
+    h.row_bytes = __builtin_amdgcn_readlane(t_rb, i);
+    h.rank = __builtin_amdgcn_readlane(t_rank, i);
+    h.n8 = __builtin_amdgcn_readlane(t_n8, i);
+    h.ng8 = __builtin_amdgcn_readlane(t_ng8, i);
+    h.ngroups = __builtin_amdgcn_readlane(t_ng, i);
+    h.frag_base = __builtin_amdgcn_readlane(t_fb, i);
+    h.gl = __builtin_amdgcn_readlane(t_gl, i);
+    const uint32_t clo = __builtin_amdgcn_readlane((uint32_t)t_code, i);
+    const uint32_t chi = __builtin_amdgcn_readlane((uint32_t)(t_code >> 32), i);
+    const uint32_t mlo = __builtin_amdgcn_readlane((uint32_t)t_meta, i);
+    const uint32_t mhi = __builtin_amdgcn_readlane((uint32_t)(t_meta >> 32), i);
+    h.code_off = (int64_t)(((uint64_t)chi << 32) | clo);
+    h.meta_off = (int64_t)(((uint64_t)mhi << 32) | mlo);
+    return h;
   };
   // value codes and meta of one step are copied into LDS ahead of use; per-lane
   // offsets of this wave's channel tiles inside a 32-token block
@@ -555,25 +609,25 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 
   // ---------------------------------------------------------------- main loop
   float m_run[CTH], l_part[CTH];
-  // the two largest scores this lane has seen per tile, with their tokens: the
-  // combine pass rescores the dominant tokens exactly
-  float b1x[CTH], b2x[CTH];
-  uint32_t bt[CTH];   // token offsets from t_begin: first in bits 0..15, second in 16..31
+  // the largest score this lane has seen per tile and subtile, with its token
+  // (offset from t_begin minus the lane's 32*tg + 4*quad): the combine pass
+  // rescores the dominant tokens exactly
+  float bx[CTH][2];
+  int bt[CTH][2];
   f4 acc_v[CT][NTW];
 #pragma unroll
   for (int c = 0; c < CTH; ++c) {
     m_run[c] = -INFINITY;
     l_part[c] = 0.0f;
-    b1x[c] = -INFINITY; b2x[c] = -INFINITY;
-    bt[c] = 0;
+    bx[c][0] = bx[c][1] = -INFINITY;
+    bt[c][0] = bt[c][1] = 0;
   }
 #pragma unroll
   for (int c = 0; c < CT; ++c)
 #pragma unroll
     for (int t = 0; t < NTW; ++t) acc_v[c][t] = (f4){0, 0, 0, 0};
-  const float sc = p.score_scale;
 
-  load_k(0);
+  for (int i = 0; i < n_h; ++i) copy_head(head_rt(i), 0);
   load_v(0);
   __syncthreads();   // rotated queries of step 0 and the fragments visible
 
@@ -593,91 +647,125 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       for (int c = 0; c < CTH; ++c) acc_s[s][c] = (f4){0, 0, 0, 0};
 #pragma unroll
     for (int k = 1; k <= NKBS; ++k) {
-      const int o_end = p.cls[hg][hh][k];
-      for (int oi = p.cls[hg][hh][k - 1]; oi < o_end; ++oi) {
-        const int gg = p.order[oi];
-        if (k == 1) key_head<D, QM, CTH, 1>(p.kh[gg], raw, frag, qc, qzero, gg - g0, ct0, G, lane, col, quad, cs, acc_s);
-        if (k == 2) key_head<D, QM, CTH, 2>(p.kh[gg], raw, frag, qc, qzero, gg - g0, ct0, G, lane, col, quad, cs, acc_s);
-        if (NKBS > 2 && k == 3) key_head<D, QM, CTH, (NKBS > 2 ? 3 : 1)>(p.kh[gg], raw, frag, qc, qzero, gg - g0, ct0, G, lane, col, quad, cs, acc_s);
-        if (NKBS > 3 && k == 4) key_head<D, QM, CTH, (NKBS > 3 ? 4 : 1)>(p.kh[gg], raw, frag, qc, qzero, gg - g0, ct0, G, lane, col, quad, cs, acc_s);
+      for (int i = cls_end[k - 1]; i < cls_end[k]; ++i) {
+        const HeadRt kh = head_rt(i);
+        if (k == 1) key_head<D, QM, CTH, 1>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, quad, cs, acc_s);
+        if (k == 2) key_head<D, QM, CTH, 2>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, quad, cs, acc_s);
+        if (NKBS > 2 && k == 3) key_head<D, QM, CTH, (NKBS > 2 ? 3 : 1)>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, quad, cs, acc_s);
+        if (NKBS > 3 && k == 4) key_head<D, QM, CTH, (NKBS > 3 ? 4 : 1)>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, quad, cs, acc_s);
+        // the head's staging has been read (its values are consumed): copy
+        // the next step's codes and meta of this head into it
+        if (step + 1 < n_steps) copy_head(kh, step + 1);
       }
     }
-    // the staging area has been read: copy the next step's keys into it
-    if (step + 1 < n_steps) load_k(step + 1);
 
     // ------------------------------------------ online softmax (log2 domain)
+    // scores are already in log2 units (the query carries log2(e)/sqrt(d))
     float x[CTH][2][4];
 #pragma unroll
+    for (int c = 0; c < CTH; ++c)
+#pragma unroll
+      for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[c][s][e] = acc_s[s][c][e];
+    if (!full) {
+#pragma unroll
+      for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const bool out = tw + 16 * s + 4 * quad + e >= t_end;
+#pragma unroll
+          for (int c = 0; c < CTH; ++c) x[c][s][e] = out ? -INFINITY : x[c][s][e];
+        }
+    }
+    // Probabilities are taken against a reference maximum m_run per query
+    // column that all waves share without exchanging maxima each step; it is
+    // raised (with a rescale of the accumulators) only when a score exceeds it
+    // by more than kLazyMargin, so p stays below 2^kLazyMargin.  The first step
+    // always sets it.
+    bool over = false;
+    float ls[CTH];
+#pragma unroll
     for (int c = 0; c < CTH; ++c) {
+      ls[c] = 0.0f;
       if (c >= ctn) break;
+      const int ct = ct0 + c;
       float mx = -INFINITY;
 #pragma unroll
       for (int s = 0; s < 2; ++s)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int tok = tw + 16 * s + 4 * quad + e;
-          float v = acc_s[s][c][e] * sc;
-          if (!full && tok >= t_end) v = -INFINITY;
-          x[c][s][e] = v;
+          const float v = x[c][s][e];
           mx = fmaxf(mx, v);
-          const uint32_t to = (uint32_t)(tok - t_begin);
-          const bool gt1 = v > b1x[c], gt2 = v > b2x[c];
-          b2x[c] = gt1 ? b1x[c] : (gt2 ? v : b2x[c]);
-          bt[c] = gt1 ? (bt[c] << 16) | to : (gt2 ? (bt[c] & 0xFFFFu) | (to << 16) : bt[c]);
-          b1x[c] = gt1 ? v : b1x[c];
+          const bool gt = v > bx[c][s];
+          bt[c][s] = gt ? step * kStepTokens + 16 * s + e : bt[c][s];
+          bx[c][s] = fmaxf(bx[c][s], v);
         }
       mx = wave_max16(mx);
-      if (quad == 0) red[(tg * CT + ct0 + c) * 16 + col] = mx;
+      if (quad == 0) red[(ct * 16 + col) * kTokenGroups + tg] = mx;
+      over |= mx > m_run[c] + kLazyMargin;
+      const float mr = m_run[c];
+      u4 pk;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float e0 = __builtin_amdgcn_exp2f(x[c][k / 2][2 * (k % 2)] - mr);
+        const float e1 = __builtin_amdgcn_exp2f(x[c][k / 2][2 * (k % 2) + 1] - mr);
+        ls[c] += e0 + e1;
+        pk[k] = as_u32(__builtin_convertvector((f2){e0, e1}, h2));
+      }
+      pbuf[(tg * CT + ct) * 64 + lane] = __builtin_bit_cast(h8, pk);
     }
-    __syncthreads();   // (1) tile maxima visible; every wave is done with the queries
-    if (step + 1 < n_steps) {   // rotate the queries to the next step's base position
+    const bool any_over = __any(over);
+    if (lane == 0) flag_s[w] = any_over ? 1 : 0;
+    // this wave's value copies landed (the next step's key copies, issued after
+    // them, may still be in flight)
+    wait_vm(step + 1 < n_steps ? n_kw : 0);
+    __syncthreads();   // (1) probabilities, maxima, flags and the step's values visible
+    if (step + 1 < n_steps) {   // every wave is done with the queries: rotate them
       const int j0 = 4 * (tid % (D / 8));
 #pragma unroll
       for (int e = 0; e < 4; ++e) bs[e] = cmul(bs[e], rot_s[j0 + e]);
       store_rotated_q<D, NQV>(qc, nql, tid, qo, bs);
     }
-    bool rescale = false;
+    const int4 f0 = *reinterpret_cast<const int4*>(flag_s);
+    const int4 f1 = *reinterpret_cast<const int4*>(flag_s + 4);
+    if ((f0.x | f0.y | f0.z | f0.w | f1.x | f1.y | f1.z | f1.w) != 0) {
+      // raise the reference of every column to the running maximum and redo
+      // this step's probabilities against it
 #pragma unroll
-    for (int c = 0; c < CTH; ++c) {
-      if (c >= ctn) break;
-      const int ct = ct0 + c;
-      float mn = m_run[c];
+      for (int c = 0; c < CTH; ++c) {
+        if (c >= ctn) break;
+        const int ct = ct0 + c;
+        const f4 tm = *reinterpret_cast<const f4*>(red + (ct * 16 + col) * kTokenGroups);
+        const float mn = fmaxf(fmaxf(m_run[c], fmaxf(tm[0], tm[1])), fmaxf(tm[2], tm[3]));
+        const float al = __builtin_amdgcn_exp2f(m_run[c] - mn);   // m_run = -inf first: 0
+        m_run[c] = mn;
+        u4 pk;
+        float l2 = 0.0f;
 #pragma unroll
-      for (int g = 0; g < kTokenGroups; ++g) mn = fmaxf(mn, red[(g * CT + ct) * 16 + col]);
-      const float al = __builtin_amdgcn_exp2f(m_run[c] - mn);   // m_run = -inf first: 0
-      rescale |= (mn != m_run[c]);
-      m_run[c] = mn;
-      u4 pk;
-      float ls = 0.0f;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const float e0 = __builtin_amdgcn_exp2f(x[c][k / 2][2 * (k % 2)] - mn);
-        const float e1 = __builtin_amdgcn_exp2f(x[c][k / 2][2 * (k % 2) + 1] - mn);
-        ls += e0 + e1;
-        pk[k] = as_u32(__builtin_convertvector((f2){e0, e1}, h2));
+        for (int k = 0; k < 4; ++k) {
+          const float e0 = __builtin_amdgcn_exp2f(x[c][k / 2][2 * (k % 2)] - mn);
+          const float e1 = __builtin_amdgcn_exp2f(x[c][k / 2][2 * (k % 2) + 1] - mn);
+          l2 += e0 + e1;
+          pk[k] = as_u32(__builtin_convertvector((f2){e0, e1}, h2));
+        }
+        l_part[c] = l_part[c] * al + l2;
+        pbuf[(tg * CT + ct) * 64 + lane] = __builtin_bit_cast(h8, pk);
+        if (tg == 0 && quad == 0) alpha_s[ct * 16 + col] = al;
       }
-      l_part[c] = l_part[c] * al + ls;
-      pbuf[(tg * CT + ct) * 64 + lane] = __builtin_bit_cast(h8, pk);
-      if (tg == 0 && quad == 0) alpha_s[ct * 16 + col] = al;
-    }
-    // waves of a half hold the same maxima, so their vote agrees; each half
-    // publishes its vote and every wave combines both
-    const bool any_rescale = __any(rescale);
-    if (tg == 0 && lane == 0) flag_s[hh] = any_rescale ? 1 : 0;
-    // this wave's value copies landed (the next step's key copies, issued after
-    // them, may still be in flight)
-    wait_vm(step + 1 < n_steps ? n_kw : 0);
-    __syncthreads();   // (2) probabilities, rescale factors and the step's values visible
-
-    // ------------------------------------------ values: acc += P . V'
-    if (flag_s[0] | flag_s[1]) {
+      __syncthreads();   // new probabilities and rescale factors visible
 #pragma unroll
       for (int c = 0; c < CT; ++c) {
         const f4 al = *reinterpret_cast<const f4*>(alpha_s + c * 16 + 4 * quad);
 #pragma unroll
         for (int t = 0; t < NTW; ++t) acc_v[c][t] *= al;
       }
+    } else {
+#pragma unroll
+      for (int c = 0; c < CTH; ++c) l_part[c] += ls[c];
     }
+
+    // ------------------------------------------ values: acc += P . V'
 #pragma unroll
     for (int ww = 0; ww < kTokenGroups; ++ww) {
       h8 pa[CT];
@@ -685,7 +773,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       for (int c = 0; c < CT; ++c) pa[c] = pbuf[(ww * CT + c) * 64 + lane];
       // slots 2k, 2k+1 of this lane's chunk: tokens
       //   k < 2: 4*quad + 2k + {0,1};  k >= 2: 16 + 4*quad + 2(k-2) + {0,1}
-      u4 vmask = (u4){0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
+      u4 vmask;
       if (!full) {
         const int tb = t_step + 32 * ww;
 #pragma unroll
@@ -744,7 +832,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   for (int c = 0; c < CTH; ++c) {
     if (c >= ctn) break;
     const float l = wave_sum16(l_part[c]);
-    if (quad == 0) red[(tg * CT + ct0 + c) * 16 + col] = l;
+    if (quad == 0) red[((ct0 + c) * 16 + col) * kTokenGroups + tg] = l;
   }
   __syncthreads();
   const int64_t pbase = ((int64_t)b * p.n_split + split) * p.n_q;
@@ -754,8 +842,9 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     const int il = (ct0 + c) * 16 + col;
     if (il < nql) {
       float2* cd = p.cand + (pbase + qmap[il]) * kCand + (tg * 4 + quad) * 2;
-      cd[0] = make_float2(b1x[c], __int_as_float(t_begin + (int)(bt[c] & 0xFFFFu)));
-      cd[1] = make_float2(b2x[c], __int_as_float(t_begin + (int)(bt[c] >> 16)));
+#pragma unroll
+      for (int s = 0; s < 2; ++s)
+        cd[s] = make_float2(bx[c][s], __int_as_float(t_begin + bt[c][s] + 32 * tg + 4 * quad));
     }
   }
   if (tg == 0 && quad == 0) {
@@ -766,7 +855,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       if (il < nql) {
         float lt = 0.0f;
 #pragma unroll
-        for (int g = 0; g < kTokenGroups; ++g) lt += red[(g * CT + ct0 + c) * 16 + col];
+        for (int g = 0; g < kTokenGroups; ++g) lt += red[((ct0 + c) * 16 + col) * kTokenGroups + g];
         float* dst = p.part + (pbase + qmap[il]) * p.part_stride + p.rv;
         dst[0] = m_run[c];
         dst[1] = lt;

@@ -63,7 +63,6 @@ struct starkv_plan {
   int32_t hg_frags[STARKV_MAX_KV_HEADS];
   int32_t hg_raw[STARKV_MAX_KV_HEADS];
   int32_t hg_mid[STARKV_MAX_KV_HEADS];
-  int32_t hh_raw[STARKV_MAX_KV_HEADS][2];
   KHeadInfo kh[STARKV_MAX_KV_HEADS];      // per slot (see the decode kernel shape)
   int32_t bk_row[STARKV_MAX_KV_HEADS];    // per KV head: first row in B_k
   int32_t order[STARKV_MAX_KV_HEADS];
@@ -236,7 +235,6 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
     *raw_out = raw;
     const int nql = (g_last - g_first) * G;
     if (nql > 16 * ct) return false;
-    if (raw > kMaxLoads * 64 * 16) return false;
     return split_lds_bytes(frags, nql, D, ct, raw, L.value_groups, L.value_row_bytes) <= kLdsLimit;
   };
   int best_ct = -1;
@@ -279,8 +277,6 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
     assign(a, b, slots, &n0);
     const int mid = a + n0;          // first slot of half 1
     P->hg_mid[h] = mid;
-    P->hh_raw[h][0] = raw_of(slots, n0);
-    P->hh_raw[h][1] = raw_of(slots + n0, b - a - n0);
     int fb = 0;
     for (int sl = a; sl < b; ++sl) {
       KHeadInfo& k = P->kh[sl];
@@ -445,7 +441,6 @@ starkv_status starkv_decode_split(const starkv_plan* P, const void* cache, const
   std::memcpy(p.hg_frags, P->hg_frags, sizeof(p.hg_frags));
   std::memcpy(p.hg_raw_bytes, P->hg_raw, sizeof(p.hg_raw_bytes));
   std::memcpy(p.hg_mid, P->hg_mid, sizeof(p.hg_mid));
-  std::memcpy(p.hh_raw, P->hh_raw, sizeof(p.hh_raw));
   std::memcpy(p.kh, P->kh, sizeof(p.kh));
   std::memcpy(p.order, P->order, sizeof(p.order));
   std::memcpy(p.cls, P->cls, sizeof(p.cls));

@@ -56,7 +56,6 @@ struct DecodeParams {
   int32_t hg_mid[STARKV_MAX_KV_HEADS];       // first slot of the second half
   int32_t hg_frags[STARKV_MAX_KV_HEADS];     // fragments used by the group
   int32_t hg_raw_bytes[STARKV_MAX_KV_HEADS]; // per-wave staging bytes (max over halves)
-  int32_t hh_raw[STARKV_MAX_KV_HEADS][2];    // staging bytes of each half
   KHeadInfo kh[STARKV_MAX_KV_HEADS];         // per slot
   // slots of every half in processing order, grouped by k-block count:
   // order[cls[hg][h][k-1] .. cls[hg][h][k]) are the half's slots with k k-blocks
@@ -125,7 +124,6 @@ int split_lds_bytes(int frags, int nql, int head_dim, int ct, int raw_bytes, int
                     int v_row_bytes);
 int launch_decode_split_ntw(const DecodeParams& p, int head_dim, int qmode, int ct, int ntw,
                             size_t lds_bytes, void* stream);
-constexpr int kMaxLoads = 4;   // 16-byte key-staging loads per lane per step
 int launch_decode_combine(const CombineParams& p, void* stream);
 int launch_append_pack(const AppendParams& p, void* stream);
 int launch_downproj(const DownprojParams& p, void* stream);
