@@ -161,10 +161,10 @@ size_t        starkv_decode_workspace_bytes(const starkv_plan* plan, int32_t max
  *   x_or_latents device.  d_model > 0: hidden states [B][n_new][d_model] in x_dtype;
  *                the latents x.A_all are accumulated in fp32 and rounded to fp16
  *                (left in ws: [B][n_new][sum_r + r_v] fp16 at offset 0).
- *                d_model == 0: fp16 latents [B][n_new][sum_r + r_v] (key heads in
- *                order, then the value latent).  2-byte aligned.
+ *                16-byte aligned.  d_model == 0: fp16 latents [B][n_new][sum_r + r_v]
+ *                (key heads in order, then the value latent), 2-byte aligned.
  *   A_all        device bf16 [d_model][sum_r + r_v] (column block per key head, then
- *                values); NULL when d_model == 0.
+ *                values), 16-byte aligned; NULL when d_model == 0.
  *   pos_dev      device int32 [B]: row of the first new token of each sequence;
  *                rows pos[b] .. pos[b]+n_new-1 are written.  Rows outside
  *                [0, capacity) are not written.  The caller advances its lengths.

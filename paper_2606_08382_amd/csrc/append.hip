@@ -111,9 +111,18 @@ __global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
   uint16_t xb = 0;
   if (on) {
     if (p.partial) {
+      // the split-k partial sums in a fixed order, sixteen loads in flight
       const int64_t mn = (int64_t)n_tok * p.width;
       float acc = 0.0f;
-      for (int k = 0; k < p.k_split; ++k) acc += p.partial[k * mn + li];
+      int k = 0;
+      for (; k + 16 <= p.k_split; k += 16) {
+        float v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) v[u] = p.partial[(k + u) * mn + li];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) acc += v[u];
+      }
+      for (; k < p.k_split; ++k) acc += p.partial[k * mn + li];
       xb = __builtin_bit_cast(uint16_t, (_Float16)acc);
       p.lat_out[li] = xb;
     } else {
@@ -263,6 +272,80 @@ __global__ __launch_bounds__(256) void downproj_kernel(DownprojParams p) {
       }
 }
 
+// Down-projection for a few rows (decode appends): A_all is streamed once with
+// 16-byte loads.  Workgroup (column block of 512, k block of 64): wave w takes
+// 16 rows of k, lane l columns 8l..8l+7; the four waves' sums meet in LDS and
+// one fp32 partial per k block is written.
+constexpr int kSmallCols = 512, kSmallK = 64;
+
+__global__ __launch_bounds__(256) void downproj_small_kernel(DownprojParams p) {
+  extern __shared__ __align__(16) float dsm[];     // [4][M][kSmallCols]
+  __shared__ __align__(16) uint16_t xs[kSmallM][kSmallK];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int n0 = blockIdx.x * kSmallCols + 8 * lane;
+  const int k0 = blockIdx.y * kSmallK;
+  const int M = p.m;
+  // A rows first (clamped addresses, zeroed afterwards), then the few x values
+  u4 av[16];
+  {
+    const int nc = min(n0, p.n - 8);
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      const int k = min(k0 + 16 * w + kk, p.k - 1);
+      av[kk] = *reinterpret_cast<const u4*>(p.a + (int64_t)k * p.n + nc);
+    }
+  }
+  for (int i = tid; i < M * kSmallK; i += 256) {
+    const int m = i / kSmallK, kk = i % kSmallK;
+    xs[m][kk] = (k0 + kk < p.k) ? p.x[(int64_t)m * p.k + k0 + kk] : (uint16_t)0;
+  }
+#pragma unroll
+  for (int kk = 0; kk < 16; ++kk)
+    if (k0 + 16 * w + kk >= p.k || n0 >= p.n) av[kk] = (u4){0, 0, 0, 0};
+  __syncthreads();
+  float acc[kSmallM][8];
+#pragma unroll
+  for (int m = 0; m < kSmallM; ++m)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[m][e] = 0.0f;
+#pragma unroll
+  for (int kk = 0; kk < 16; ++kk) {
+    float a[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      a[2 * e] = __uint_as_float(av[kk][e] << 16);
+      a[2 * e + 1] = __uint_as_float(av[kk][e] & 0xFFFF0000u);
+    }
+#pragma unroll
+    for (int m = 0; m < kSmallM; ++m) {
+      if (m < M) {
+        const float xv = __uint_as_float((uint32_t)xs[m][16 * w + kk] << 16);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[m][e] = __builtin_fmaf(xv, a[e], acc[m][e]);
+      }
+    }
+  }
+#pragma unroll
+  for (int m = 0; m < kSmallM; ++m)
+    if (m < M) {
+      f4* d = reinterpret_cast<f4*>(dsm + ((w * M + m) * kSmallCols + 8 * lane));
+      d[0] = (f4){acc[m][0], acc[m][1], acc[m][2], acc[m][3]};
+      d[1] = (f4){acc[m][4], acc[m][5], acc[m][6], acc[m][7]};
+    }
+  __syncthreads();
+  float* out = p.partial + (int64_t)blockIdx.y * p.m * p.n;
+  for (int i = tid; i < M * kSmallCols; i += 256) {
+    const int m = i / kSmallCols, c = i % kSmallCols;
+    const int n = blockIdx.x * kSmallCols + c;
+    if (n < p.n) {
+      float v = 0.0f;
+#pragma unroll
+      for (int ww = 0; ww < 4; ++ww) v += dsm[(ww * M + m) * kSmallCols + c];
+      out[(int64_t)m * p.n + n] = v;
+    }
+  }
+}
+
 // ------------------------------------------------------------------ launchers
 int launch_append_pack(const AppendParams& p, void* stream) {
   const int64_t waves = (int64_t)p.batch * p.n_new * p.n_items;
@@ -272,6 +355,13 @@ int launch_append_pack(const AppendParams& p, void* stream) {
 }
 
 int launch_downproj(const DownprojParams& p, void* stream) {
+  if (p.m <= kSmallM) {
+    dim3 grid((p.n + kSmallCols - 1) / kSmallCols, p.k_split);
+    const size_t lds = (size_t)4 * p.m * kSmallCols * sizeof(float);
+    hipLaunchKernelGGL(downproj_small_kernel, grid, dim3(256), lds,
+                       static_cast<hipStream_t>(stream), p);
+    return (int)hipGetLastError();
+  }
   dim3 grid((p.n + BN - 1) / BN, (p.m + BM - 1) / BM, p.k_split);
   hipLaunchKernelGGL(downproj_kernel, grid, dim3(256), 0, static_cast<hipStream_t>(stream), p);
   return (int)hipGetLastError();

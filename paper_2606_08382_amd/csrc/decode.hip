@@ -895,7 +895,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 // reconstruction, RoPE angle reduced in fp64), and their contribution to the
 // normalizer and to the merged value latent is moved from the approximate to the
 // exact weight.
-constexpr int kCombineMaxSplits = 64;
+constexpr int kCombineMaxSplits = 64;   // one split per lane of the weight wave
 constexpr int kRescoreMax = 32;                        // tokens rescored per query head
 constexpr float kRescoreTau = 1.0f / 64.0f;
 constexpr int kCandPerThread = kCombineMaxSplits * kCand / 256;
@@ -979,30 +979,56 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   // candidates of all splits, loaded ahead of the split weights
   const int n_ent = ns * kCand;
   const float2* cand = p.cand + ((int64_t)b * p.n_split * p.n_q + i) * kCand;
+  // (every load below reads a clamped, valid address; entries beyond the
+  // sequence's splits are masked where they are used)
+  // (addresses are a per-lane base plus wave-uniform offsets; entries beyond
+  // the sequence's splits are masked where they are used)
   float2 ce[kCandPerThread];
+  {
+    const float2* cl = cand + (int64_t)(tid / kCand) * p.n_q * kCand + tid % kCand;
+    const int64_t cstep = (int64_t)(256 / kCand) * p.n_q * kCand;
 #pragma unroll
-  for (int k = 0; k < kCandPerThread; ++k) {
-    const int e = k * 256 + tid;
-    ce[k] = make_float2(-INFINITY, 0.0f);
-    if (e < n_ent) ce[k] = cand[(int64_t)(e / kCand) * p.n_q * kCand + e % kCand];
+    for (int k = 0; k < kCandPerThread; ++k) {
+      ce[k] = make_float2(-INFINITY, 0.0f);
+      if (k * 256 + tid < n_ent) ce[k] = cl[k * cstep];
+    }
   }
-  if (tid < 64) {                 // split weights: one wave, up to 64 splits per lane pass
-    float mv[kCombineMaxSplits / 64 + 1], lv[kCombineMaxSplits / 64 + 1];
-    float m = -INFINITY;
-    int k = 0;
-    for (int s = tid; s < ns; s += 64, ++k) {
-      mv[k] = part[s * sstride + p.rv];
-      lv[k] = part[s * sstride + p.rv + 1];
-      m = fmaxf(m, mv[k]);
+  // the value-latent partials of this thread's first channel and its first
+  // rows of U_V do not depend on the merge weights: load them now as well
+  const int D8 = D / 8;                  // 16 (D = 128) or 8 (D = 64)
+  const int groups = 256 / D8;           // row groups of the up-projection
+  const int j8 = tid % D8, rg = tid / D8;
+  const int64_t ldb = (int64_t)p.n_kv * D;
+  const uint16_t* bv = p.bv + (int64_t)g * D + 8 * j8;
+  // 32-bit byte offsets from the (b, head) partials: the region spans
+  // n_split * sstride floats, far below 4 GiB
+  const uint8_t* pbase = reinterpret_cast<const uint8_t*>(part);
+  const uint32_t sbytes = (uint32_t)sstride * 4u;
+  float v0[kCombineMaxSplits];
+  {
+    const uint32_t o = (uint32_t)min(tid, p.rv - 1) * 4u;
+#pragma unroll
+    for (int s = 0; s < kCombineMaxSplits; ++s)
+      v0[s] = *reinterpret_cast<const float*>(pbase + o + (uint32_t)min(s, p.n_split - 1) * sbytes);
+  }
+  u4 w0[8];
+  {
+    const uint16_t* bl = bv + (int64_t)rg * ldb;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      w0[k] = (u4){0, 0, 0, 0};
+      if (rg + k * groups < p.rv) w0[k] = *reinterpret_cast<const u4*>(bl + (int64_t)k * groups * ldb);
     }
+  }
+  if (tid < 64) {                 // split weights: one wave, one split per lane
+    const int s = min(tid, p.n_split - 1);
+    const float mv = tid < ns ? part[s * sstride + p.rv] : -INFINITY;
+    const float lv = part[s * sstride + p.rv + 1];
+    float m = mv;
     for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
-    float l = 0.0f;
-    k = 0;
-    for (int s = tid; s < ns; s += 64, ++k) {
-      const float wv = __builtin_amdgcn_exp2f(mv[k] - m);
-      wts[s] = wv;
-      l += wv * lv[k];
-    }
+    const float wv = tid < ns ? __builtin_amdgcn_exp2f(mv - m) : 0.0f;
+    wts[tid] = wv;
+    float l = tid < ns ? wv * lv : 0.0f;
     for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o);
     if (tid == 0) { misc[0] = m; misc[1] = l; }
   }
@@ -1100,15 +1126,11 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   }
   __syncthreads();
   const float inv_l = 1.0f / misc[2];
-  for (int r = tid; r < p.rv; r += 256) {
-    float v[kCombineMaxSplits];
-#pragma unroll
-    for (int s = 0; s < kCombineMaxSplits; ++s)
-      if (s < ns) v[s] = part[s * sstride + r];
+  auto merge_channel = [&](int r, const float (&v)[kCombineMaxSplits]) {
     float acc = 0.0f;
 #pragma unroll
     for (int s = 0; s < kCombineMaxSplits; ++s)
-      if (s < ns) acc += wts[s] * v[s];
+      if (s < ns) acc = __builtin_fmaf(wts[s], v[s], acc);
     for (int j0 = 0; j0 < n_sel; j0 += 8) {   // eight candidates' loads in flight
       float vl[8];
 #pragma unroll
@@ -1118,23 +1140,21 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
         if (j0 + u < n_sel) acc = __builtin_fmaf(c_d[j0 + u], vl[u], acc);
     }
     a[r] = acc * inv_l;
+  };
+  if (tid < p.rv) merge_channel(tid, v0);
+  for (int r = tid + 256; r < p.rv; r += 256) {
+    float v[kCombineMaxSplits];
+#pragma unroll
+    for (int s = 0; s < kCombineMaxSplits; ++s)
+      v[s] = *reinterpret_cast<const float*>(pbase + (uint32_t)r * 4u +
+                                             (uint32_t)min(s, p.n_split - 1) * sbytes);
+    merge_channel(r, v);
   }
   __syncthreads();
   // o = a . U_V^T restricted to KV head g's d columns (the reordering of Sec. 3.3):
-  // thread (rg, j8) covers rows rg, rg+16, .. and columns 8*j8..8*j8+7
-  const int j8n = D / 8;                 // 16 (D = 128) or 8 (D = 64)
-  const int groups = 256 / j8n;          // row groups
-  const int j8 = tid % j8n, rg = tid / j8n;
-  const int64_t ldb = (int64_t)p.n_kv * D;
-  const uint16_t* bv = p.bv + (int64_t)g * D + 8 * j8;
+  // thread (rg, j8) covers rows rg, rg + groups, .. and columns 8*j8..8*j8+7
   float o[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  for (int r0 = rg; r0 < p.rv; r0 += 8 * groups) {
-    u4 w8[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int r = r0 + k * groups;
-      if (r < p.rv) w8[k] = *reinterpret_cast<const u4*>(bv + r * ldb);
-    }
+  auto up_rows = [&](int r0, const u4 (&w8)[8]) {
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       const int r = r0 + k * groups;
@@ -1145,6 +1165,17 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
         for (int e = 0; e < 8; ++e) o[e] += ar * (float)hw[e];
       }
     }
+  };
+  up_rows(rg, w0);
+  for (int r0 = rg + 8 * groups; r0 < p.rv; r0 += 8 * groups) {
+    u4 w8[8];
+    const uint16_t* bl = bv + (int64_t)r0 * ldb;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      w8[k] = (u4){0, 0, 0, 0};
+      if (r0 + k * groups < p.rv) w8[k] = *reinterpret_cast<const u4*>(bl + (int64_t)k * groups * ldb);
+    }
+    up_rows(r0, w8);
   }
 #pragma unroll
   for (int e = 0; e < 8; ++e) red[rg * D + 8 * j8 + e] = o[e];

@@ -517,6 +517,11 @@ starkv_status starkv_decode_attn(const starkv_plan* P, const void* cache, const 
 
 static void downproj_shape(const starkv_plan* P, int32_t n_new, int* k_split, int* k_chunk) {
   const int M = P->cfg.batch * n_new, N = P->width, K = P->cfg.d_model;
+  if (M <= kSmallM) {            // streaming kernel: k blocks of 64 rows
+    *k_chunk = 64;
+    *k_split = (K + 63) / 64;
+    return;
+  }
   const int tiles = ((M + 63) / 64) * ((N + 63) / 64);
   int ks = 256 / tiles;
   if (ks < 1) ks = 1;
@@ -558,7 +563,7 @@ starkv_status starkv_append(const starkv_plan* P, void* cache, const void* x_or_
   if (c.d_model > 0) {
     if (reinterpret_cast<uintptr_t>(x_or_latents) % 16)
       return fail(STARKV_ERR_ALIGNMENT, "x not 16-byte aligned");
-    if (reinterpret_cast<uintptr_t>(A_all) % 2) return fail(STARKV_ERR_ALIGNMENT, "A_all not 2-byte aligned");
+    if (reinterpret_cast<uintptr_t>(A_all) % 16) return fail(STARKV_ERR_ALIGNMENT, "A_all not 16-byte aligned");
     int ks, kc;
     downproj_shape(P, n_new, &ks, &kc);
     const int64_t mn = (int64_t)c.batch * n_new * P->width;

@@ -126,6 +126,9 @@ int launch_decode_split_ntw(const DecodeParams& p, int head_dim, int qmode, int 
                             size_t lds_bytes, void* stream);
 int launch_decode_combine(const CombineParams& p, void* stream);
 int launch_append_pack(const AppendParams& p, void* stream);
+// rows (B * n_new) up to which the down-projection streams A_all with the
+// small-M kernel: k blocks of 64 rows, one fp32 partial per block
+constexpr int kSmallM = 7;
 int launch_downproj(const DownprojParams& p, void* stream);
 
 }  // namespace starkv
