@@ -2,7 +2,9 @@
 
 One step = starkv_append of one new token per sequence from bf16 hidden states
 (down-projection + quantize/pack) followed by starkv_decode_attn over the whole
-context (split pass + combine pass), on one layer's cache.  Five layer caches
+context (split pass + combine pass), on one layer's cache.  The timed steps
+replay the step captured in a HIP graph (one per layer cache); per-kernel times
+come from an eager pass with HIP events.  Five layer caches
 (> 1 GB together) are used in rotation so the 256 MB last-level cache cannot
 serve the latent stream.  Inputs are seeded synthetic arrays of the workload's
 shape, resident in HBM before timing starts.
@@ -96,6 +98,7 @@ def main():
     ap.add_argument("--layers", type=int, default=5)
     ap.add_argument("--cpu-sample-ctx", type=int, default=32768)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true", help="time eager launches, not graph replays")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -155,15 +158,33 @@ def main():
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
+    # eager pass: per-kernel times from HIP events on the launch stream
     t0 = time.perf_counter()
     for i in range(args.steps):
         step(i, ev[i])
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+    wall_eager = time.perf_counter() - t0
     t_app = np.array([e[0].elapsed_time(e[1]) for e in ev])
     t_split = np.array([e[1].elapsed_time(e[2]) for e in ev])
     t_comb = np.array([e[2].elapsed_time(e[3]) for e in ev])
-    ms_step = wall * 1e3 / args.steps
+    ms_eager = wall_eager * 1e3 / args.steps
+    ms_step = ms_eager
+    if not args.no_graph:
+        # the step captured once per layer cache in a HIP graph (no launch gaps)
+        graphs = []
+        for li in range(len(layers)):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                step(li)
+            graphs.append(g)
+        for i in range(args.warmup):
+            graphs[i % len(graphs)].replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            graphs[i % len(graphs)].replay()
+        torch.cuda.synchronize()
+        ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
     tokens = int(inp.ctx_len.sum())
     layout = S.starkv_cache_layout(layers[0].plan)
     per_token = (sum(layout.key_row_bytes[g] + 4 * layout.key_groups[g]
@@ -174,7 +195,7 @@ def main():
     achieved = alg_bytes / split_s / 1e9
     log(f"append {t_app.mean() * 1e3:.1f} us  split {t_split.mean() * 1e3:.1f} us "
         f"(median {np.median(t_split) * 1e3:.1f})  combine {t_comb.mean() * 1e3:.1f} us  "
-        f"wall/step {ms_step * 1e3:.1f} us")
+        f"wall/step {ms_step * 1e3:.1f} us (eager {ms_eager * 1e3:.1f} us)")
     copy = copy_stream(torch, stream)
     log(f"device copy {copy['GBps']:.0f} GB/s (read + write)")
     traffic, tsum = measured_traffic(w.name)
@@ -191,7 +212,9 @@ def main():
                    "kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
                    "key_ranks": inp.key_rank, "value_rank": w.value_rank,
                    "cache": "int8/int4 mixed, 32-channel groups", "layers_rotated": args.layers,
-                   "append": f"{w.append_tokens} token/seq from bf16 hidden {w.d_model}"},
+                   "append": f"{w.append_tokens} token/seq from bf16 hidden {w.d_model}",
+                   "launch": "eager" if args.no_graph else "hip graph per layer",
+                   "ms_per_step_eager": ms_eager},
         "kernels_us": {"append": float(t_app.mean() * 1e3), "decode_split": float(t_split.mean() * 1e3),
                        "decode_combine": float(t_comb.mean() * 1e3)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,

@@ -111,10 +111,17 @@ __global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
   uint16_t xb = 0;
   if (on) {
     if (p.partial) {
-      // the split-k partial sums in a fixed order, sixteen loads in flight
+      // the split-k partial sums in a fixed order, up to 64 loads in flight
       const int64_t mn = (int64_t)n_tok * p.width;
       float acc = 0.0f;
       int k = 0;
+      for (; k + 64 <= p.k_split; k += 64) {
+        float v[64];
+#pragma unroll
+        for (int u = 0; u < 64; ++u) v[u] = p.partial[(k + u) * mn + li];
+#pragma unroll
+        for (int u = 0; u < 64; ++u) acc += v[u];
+      }
       for (; k + 16 <= p.k_split; k += 16) {
         float v[16];
 #pragma unroll
@@ -273,26 +280,26 @@ __global__ __launch_bounds__(256) void downproj_kernel(DownprojParams p) {
 }
 
 // Down-projection for a few rows (decode appends): A_all is streamed once with
-// 16-byte loads.  Workgroup (column block of 512, k block of 64): wave w takes
-// 16 rows of k, lane l columns 8l..8l+7; the four waves' sums meet in LDS and
-// one fp32 partial per k block is written.
-constexpr int kSmallCols = 512, kSmallK = 64;
+// 16-byte loads.  Workgroup = (128 columns, 64 rows of k): thread (kg, cg)
+// takes rows 4*kg..4*kg+3 and columns 8*cg..8*cg+7; the sixteen k groups meet
+// in LDS and one fp32 partial per k block is written.
+constexpr int kSmallCols = 128, kSmallK = 64;
 
 __global__ __launch_bounds__(256) void downproj_small_kernel(DownprojParams p) {
-  extern __shared__ __align__(16) float dsm[];     // [4][M][kSmallCols]
+  extern __shared__ __align__(16) float dsm[];     // [16][M][kSmallCols]
   __shared__ __align__(16) uint16_t xs[kSmallM][kSmallK];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int n0 = blockIdx.x * kSmallCols + 8 * lane;
+  const int tid = threadIdx.x, cg = tid % 16, kg = tid / 16;
+  const int n0 = blockIdx.x * kSmallCols + 8 * cg;
   const int k0 = blockIdx.y * kSmallK;
   const int M = p.m;
   // A rows first (clamped addresses, zeroed afterwards), then the few x values
-  u4 av[16];
+  u4 av[4];
   {
     const int nc = min(n0, p.n - 8);
 #pragma unroll
-    for (int kk = 0; kk < 16; ++kk) {
-      const int k = min(k0 + 16 * w + kk, p.k - 1);
-      av[kk] = *reinterpret_cast<const u4*>(p.a + (int64_t)k * p.n + nc);
+    for (int i = 0; i < 4; ++i) {
+      const int k = min(k0 + 4 * kg + i, p.k - 1);
+      av[i] = *reinterpret_cast<const u4*>(p.a + (int64_t)k * p.n + nc);
     }
   }
   for (int i = tid; i < M * kSmallK; i += 256) {
@@ -300,8 +307,8 @@ __global__ __launch_bounds__(256) void downproj_small_kernel(DownprojParams p) {
     xs[m][kk] = (k0 + kk < p.k) ? p.x[(int64_t)m * p.k + k0 + kk] : (uint16_t)0;
   }
 #pragma unroll
-  for (int kk = 0; kk < 16; ++kk)
-    if (k0 + 16 * w + kk >= p.k || n0 >= p.n) av[kk] = (u4){0, 0, 0, 0};
+  for (int i = 0; i < 4; ++i)
+    if (k0 + 4 * kg + i >= p.k || n0 >= p.n) av[i] = (u4){0, 0, 0, 0};
   __syncthreads();
   float acc[kSmallM][8];
 #pragma unroll
@@ -309,17 +316,17 @@ __global__ __launch_bounds__(256) void downproj_small_kernel(DownprojParams p) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[m][e] = 0.0f;
 #pragma unroll
-  for (int kk = 0; kk < 16; ++kk) {
+  for (int i = 0; i < 4; ++i) {
     float a[8];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      a[2 * e] = __uint_as_float(av[kk][e] << 16);
-      a[2 * e + 1] = __uint_as_float(av[kk][e] & 0xFFFF0000u);
+      a[2 * e] = __uint_as_float(av[i][e] << 16);
+      a[2 * e + 1] = __uint_as_float(av[i][e] & 0xFFFF0000u);
     }
 #pragma unroll
     for (int m = 0; m < kSmallM; ++m) {
       if (m < M) {
-        const float xv = __uint_as_float((uint32_t)xs[m][16 * w + kk] << 16);
+        const float xv = __uint_as_float((uint32_t)xs[m][4 * kg + i] << 16);
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[m][e] = __builtin_fmaf(xv, a[e], acc[m][e]);
       }
@@ -328,7 +335,7 @@ __global__ __launch_bounds__(256) void downproj_small_kernel(DownprojParams p) {
 #pragma unroll
   for (int m = 0; m < kSmallM; ++m)
     if (m < M) {
-      f4* d = reinterpret_cast<f4*>(dsm + ((w * M + m) * kSmallCols + 8 * lane));
+      f4* d = reinterpret_cast<f4*>(dsm + ((kg * M + m) * kSmallCols + 8 * cg));
       d[0] = (f4){acc[m][0], acc[m][1], acc[m][2], acc[m][3]};
       d[1] = (f4){acc[m][4], acc[m][5], acc[m][6], acc[m][7]};
     }
@@ -340,7 +347,7 @@ __global__ __launch_bounds__(256) void downproj_small_kernel(DownprojParams p) {
     if (n < p.n) {
       float v = 0.0f;
 #pragma unroll
-      for (int ww = 0; ww < 4; ++ww) v += dsm[(ww * M + m) * kSmallCols + c];
+      for (int g = 0; g < 16; ++g) v += dsm[(g * M + m) * kSmallCols + c];
       out[(int64_t)m * p.n + n] = v;
     }
   }
@@ -357,7 +364,7 @@ int launch_append_pack(const AppendParams& p, void* stream) {
 int launch_downproj(const DownprojParams& p, void* stream) {
   if (p.m <= kSmallM) {
     dim3 grid((p.n + kSmallCols - 1) / kSmallCols, p.k_split);
-    const size_t lds = (size_t)4 * p.m * kSmallCols * sizeof(float);
+    const size_t lds = (size_t)16 * p.m * kSmallCols * sizeof(float);
     hipLaunchKernelGGL(downproj_small_kernel, grid, dim3(256), lds,
                        static_cast<hipStream_t>(stream), p);
     return (int)hipGetLastError();
