@@ -107,7 +107,7 @@ __host__ __device__ inline SplitLds split_lds(int frags, int nql, int head_dim, 
   SplitLds L;
   L.frag = 0;
   L.qc = frags * 1024;
-  L.red = L.qc + ((nql * (head_dim + 8) * 2 + 16 + 15) / 16) * 16;
+  L.red = L.qc + ((nql * (head_dim + 8) * 2 + 256 + 15) / 16) * 16;
   L.alpha = L.red + kTokenGroups * ct * 16 * 4;
   L.flag = L.alpha + ct * 16 * 4;
   L.rot = L.flag + kWaves * 4;
@@ -136,7 +136,8 @@ __device__ __forceinline__ void copy_to_lds(uint8_t* lds, const uint8_t* src, in
 }
 
 // Wait until at most n (wave-uniform) vector memory operations of this wave are
-// outstanding; they complete in issue order.
+// outstanding; they complete in issue order.  Counts above 15 wait for all
+// (conservative).
 __device__ __forceinline__ void wait_vm(int n) {
   switch (__builtin_amdgcn_readfirstlane(n)) {
     case 1: __builtin_amdgcn_s_waitcnt(0x0F71); break;
@@ -282,7 +283,9 @@ __device__ __forceinline__ void key_head(const HeadRt& kh, const uint8_t* raw, c
   const int ct_g = (gl * G) / 16 - ct0;      // score tile of this head within the half
   const int c_lo = (gl * G) % 16;
   const bool mine = col >= c_lo && col < c_lo + G;
-  const int qrow = (((gl * G) / 16) * 16 + col) * QS;
+  // the lane's query vectors of k-blocks 0.. are 32 halves apart; lanes whose
+  // column is not one of the head's queries read a zero area laid out alike
+  const _Float16* qb = qc + (mine ? (((gl * G) / 16) * 16 + col) * QS : qzero) + quad * 8;
   const int fb = kh.frag_base;
   f4 klo[2][2], khi[2][2];   // [buffer][subtile]
 #pragma unroll
@@ -304,7 +307,7 @@ __device__ __forceinline__ void key_head(const HeadRt& kh, const uint8_t* raw, c
     }
     if (kbs > 0) {           // rotate and score k-block kbs-1 (packed fp16)
       const int kq = kbs - 1, buf = kq & 1;
-      const h8 qf = *reinterpret_cast<const h8*>(qc + (mine ? qrow + (kq * 4 + quad) * 8 : qzero));
+      const h8 qf = *reinterpret_cast<const h8*>(qb + kq * 32);
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
         const CS4& r = cs[s][kq];
@@ -419,7 +422,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     for (int i = tid; i < n; i += kThreads) f[i] = (u4){0, 0, 0, 0};
   }
   if (tid < nql) qmap[tid] = p.kh[g0 + tid / G].head * G + tid % G;
-  if (tid < 8) qc[qzero + tid] = (_Float16)0.0f;
+  if (tid < 128) qc[qzero + tid] = (_Float16)0.0f;
   // RoPE tables: the lane's in-step offset u = 32*tg + 16*s + col composed as
   // the subtile rotation (16*(2*tg + s)) times the column rotation (col), and
   // the rotation by one step (kStepTokens) for the query's base position.
@@ -543,9 +546,11 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 #pragma unroll
   for (int k = 0; k <= NKBS; ++k) cls_end[k] = p.cls[hg][hh][k] - c0;
   const int n_h = cls_end[NKBS];
-  int t_raw_code = 0, t_raw_meta = 0, t_rb = 0, t_rank = 0, t_n8 = 0, t_ng8 = 0, t_ng = 0,
-      t_fb = 0, t_gl = 0;
-  int64_t t_code = 0, t_meta = 0;
+  // Packed fields: staging offsets (16 bits each; a wave's staging is far
+  // below 64 KiB); row bytes (9 bits), rank (8), 8-bit chunks (3), 8-bit groups
+  // (2), groups (3), slot in the group (4); fragment base; plane offsets / 256
+  // (planes are 256-byte aligned).
+  uint32_t t_raw = 0, t_geo = 0, t_fb = 0, t_code = 0, t_meta = 0;
   int n_kw = 0;
   for (int i = 0; i < n_h; ++i) {
     const int gg = p.order[c0 + i];
@@ -553,29 +558,29 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     n_kw += (32 * kh.row_bytes + 1023) / 1024;
     if (QM != STARKV_Q_F16) n_kw += (2 * kh.ngroups * 64 + 1023) / 1024;
     if (lane == i) {
-      t_raw_code = kh.raw_code; t_raw_meta = kh.raw_meta; t_rb = kh.row_bytes;
-      t_rank = kh.rank; t_n8 = kh.n8; t_ng8 = kh.ng8; t_ng = kh.ngroups;
-      t_fb = kh.frag_base; t_gl = gg - g0;
-      t_code = kh.code_off; t_meta = kh.meta_off;
+      t_raw = (uint32_t)kh.raw_code | ((uint32_t)kh.raw_meta << 16);
+      t_geo = (uint32_t)kh.row_bytes | ((uint32_t)kh.rank << 9) | ((uint32_t)kh.n8 << 17) |
+              ((uint32_t)kh.ng8 << 20) | ((uint32_t)kh.ngroups << 22) | ((uint32_t)(gg - g0) << 25);
+      t_fb = (uint32_t)kh.frag_base;
+      t_code = (uint32_t)(kh.code_off >> 8);
+      t_meta = (uint32_t)(kh.meta_off >> 8);
     }
   }
   auto head_rt = [&](int i) {
     HeadRt h;
-    h.raw_code = __builtin_amdgcn_readlane(t_raw_code, i);
-    h.raw_meta = __builtin_amdgcn_readlane(t_raw_meta, i);
-    h.row_bytes = __builtin_amdgcn_readlane(t_rb, i);
-    h.rank = __builtin_amdgcn_readlane(t_rank, i);
-    h.n8 = __builtin_amdgcn_readlane(t_n8, i);
-    h.ng8 = __builtin_amdgcn_readlane(t_ng8, i);
-    h.ngroups = __builtin_amdgcn_readlane(t_ng, i);
-    h.frag_base = __builtin_amdgcn_readlane(t_fb, i);
-    h.gl = __builtin_amdgcn_readlane(t_gl, i);
-    const uint32_t clo = __builtin_amdgcn_readlane((uint32_t)t_code, i);
-    const uint32_t chi = __builtin_amdgcn_readlane((uint32_t)(t_code >> 32), i);
-    const uint32_t mlo = __builtin_amdgcn_readlane((uint32_t)t_meta, i);
-    const uint32_t mhi = __builtin_amdgcn_readlane((uint32_t)(t_meta >> 32), i);
-    h.code_off = (int64_t)(((uint64_t)chi << 32) | clo);
-    h.meta_off = (int64_t)(((uint64_t)mhi << 32) | mlo);
+    const uint32_t raw_ = __builtin_amdgcn_readlane(t_raw, i);
+    const uint32_t geo = __builtin_amdgcn_readlane(t_geo, i);
+    h.raw_code = (int)(raw_ & 0xFFFFu);
+    h.raw_meta = (int)(raw_ >> 16);
+    h.row_bytes = (int)(geo & 0x1FFu);
+    h.rank = (int)((geo >> 9) & 0xFFu);
+    h.n8 = (int)((geo >> 17) & 7u);
+    h.ng8 = (int)((geo >> 20) & 3u);
+    h.ngroups = (int)((geo >> 22) & 7u);
+    h.gl = (int)((geo >> 25) & 15u);
+    h.frag_base = (int)__builtin_amdgcn_readlane(t_fb, i);
+    h.code_off = (int64_t)__builtin_amdgcn_readlane(t_code, i) << 8;
+    h.meta_off = (int64_t)__builtin_amdgcn_readlane(t_meta, i) << 8;
     return h;
   };
   // value codes and meta of one step are copied into LDS ahead of use; per-lane
@@ -645,6 +650,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     for (int s = 0; s < 2; ++s)
 #pragma unroll
       for (int c = 0; c < CTH; ++c) acc_s[s][c] = (f4){0, 0, 0, 0};
+
 #pragma unroll
     for (int k = 1; k <= NKBS; ++k) {
       for (int i = cls_end[k - 1]; i < cls_end[k]; ++i) {
