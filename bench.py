@@ -37,7 +37,7 @@ def log(*a):
 
 def cpu_baseline(w, inp, sample_ctx: int):
     """The fp64 oracle on one sequence (all heads) over the first sample_ctx tokens, scaled
-    linearly to the full context."""
+    linearly to the full context when the sample is shorter."""
     from oracle import oracle as O
     cfg = O.make_cfg(1, w.n_q_heads, w.n_kv_heads, w.head_dim, sample_ctx, inp.key_rank,
                      w.value_rank, w.qmode, w.rope_theta)
@@ -48,9 +48,11 @@ def cpu_baseline(w, inp, sample_ctx: int):
                                inp.Bv, np.array([sample_ctx], np.int32))
     dt = time.perf_counter() - t0
     full = dt * (w.ctx / sample_ctx)            # seconds for one decode token at full context
+    span = (f"all {w.ctx} tokens" if sample_ctx == w.ctx else
+            f"the first {sample_ctx} of {w.ctx} tokens (scaled linearly in context length)")
     return {"value": 1.0 / full, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": (f"1 sequence x {w.n_q_heads} query heads over the first {sample_ctx} of "
-                       f"{w.ctx} tokens took {dt:.2f} s; scaled linearly in context length")}
+            "sample": (f"one decode token: 1 sequence x {w.n_q_heads} query heads over {span} "
+                       f"took {dt:.2f} s")}
 
 
 def measured_traffic(workload_name):
@@ -96,7 +98,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="c3")
     ap.add_argument("--layers", type=int, default=5)
-    ap.add_argument("--cpu-sample-ctx", type=int, default=32768)
+    ap.add_argument("--cpu-sample-ctx", type=int, default=0,
+                    help="context tokens of the oracle sample (0: the full context)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches, not graph replays")
     args = ap.parse_args()
@@ -229,7 +232,7 @@ def main():
                                  "fetch_scale", "write_scale") if k in tsum}
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
-        result["cpu_baseline"] = cpu_baseline(w, inp, min(args.cpu_sample_ctx, L))
+        result["cpu_baseline"] = cpu_baseline(w, inp, min(args.cpu_sample_ctx or L, L))
     print(json.dumps(result), flush=True)
 
 
