@@ -25,6 +25,8 @@
 //   query head (Sec. 3.3), casting to the output type.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "starkv_internal.h"
 
 namespace starkv {
@@ -54,6 +56,9 @@ __device__ __forceinline__ uint32_t deq_pair(uint32_t magic_pair, h2 s, h2 z) {
 // Scores may exceed the shared softmax reference by this much (log2 units)
 // before it is raised: probabilities stay below 2^8 in fp16.
 constexpr float kLazyMargin = 8.0f;
+
+// value-tile precision variants of the split kernel's p.V' phase
+constexpr int kValues8 = 0, kValues4 = 1, kValuesMixed = 2;
 
 __device__ __forceinline__ float wave_max16(float v) {
   v = fmaxf(v, __shfl_xor(v, 16));
@@ -587,15 +592,32 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   // offsets of this wave's channel tiles inside a 32-token block
   const int NT = p.rv / 16;
   int v_off[NTW], v_gi[NTW];
+  bool v_is8[NTW];
 #pragma unroll
   for (int t = 0; t < NTW; ++t) {
-    const int nt = w * NTW + t;
+    // a wave's tiles beyond the value rank read tile NT-1 (their results are
+    // not stored), so the step loop needs no per-tile branch
+    const int nt = min(w * NTW + t, NT - 1);
     const int rho = 16 * nt + col;
     const bool is8 = rho < p.v_ro;
     if (QM == STARKV_Q_F16) v_off[t] = (rho * 4 + quad) * 16;
     else if (is8) v_off[t] = (rho * 4 + quad) * 8;
     else v_off[t] = 32 * p.v_ro + ((rho - p.v_ro) * 4 + quad) * 4;
     v_gi[t] = is8 ? rho / 32 : p.v_ng8 + (rho - p.v_ro) / 32;
+    v_is8[t] = is8;
+  }
+  // precision of this wave's value tiles: all 8-bit, all 4-bit (also every
+  // INT4 cache), or mixed (only when the 8-bit channel count is not a multiple
+  // of 16, or a wave's tiles straddle it); fp16 caches take the first branch
+  int vmode = kValues8;
+  if (QM != STARKV_Q_F16) {
+    bool any8 = false, any4 = false;
+    for (int t = 0; t < NTW; ++t) {
+      const int nt = min(w * NTW + t, NT - 1);   // the tile the step loop reads
+      any8 |= QM == STARKV_Q_MIX8_4 && 16 * nt < p.v_ro;
+      any4 |= QM != STARKV_Q_MIX8_4 || 16 * nt + 16 > p.v_ro;
+    }
+    vmode = any8 && any4 ? kValuesMixed : any8 ? kValues8 : kValues4;
   }
   const int64_t vblk0 = (int64_t)b * (p.cap_pad / 32) + t_begin / 32;
   const int vmeta_bytes = 4 * p.v_ng * 128;
@@ -772,61 +794,71 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     }
 
     // ------------------------------------------ values: acc += P . V'
+    // The precision of a wave's value tiles does not change between steps, so
+    // the wave runs one branch-free variant (see vmode) and the loads of all
+    // token groups can be issued ahead of the dequantization.
+    auto values = [&](auto vm_tag, auto full_tag) {
+      constexpr int VM = decltype(vm_tag)::value;
+      constexpr bool FULL = decltype(full_tag)::value;
 #pragma unroll
-    for (int ww = 0; ww < kTokenGroups; ++ww) {
-      h8 pa[CT];
+      for (int ww = 0; ww < kTokenGroups; ++ww) {
+        h8 pa[CT];
 #pragma unroll
-      for (int c = 0; c < CT; ++c) pa[c] = pbuf[(ww * CT + c) * 64 + lane];
-      // slots 2k, 2k+1 of this lane's chunk: tokens
-      //   k < 2: 4*quad + 2k + {0,1};  k >= 2: 16 + 4*quad + 2(k-2) + {0,1}
-      u4 vmask;
-      if (!full) {
-        const int tb = t_step + 32 * ww;
+        for (int c = 0; c < CT; ++c) pa[c] = pbuf[(ww * CT + c) * 64 + lane];
+        // slots 2k, 2k+1 of this lane's chunk: tokens
+        //   k < 2: 4*quad + 2k + {0,1};  k >= 2: 16 + 4*quad + 2(k-2) + {0,1}
+        u4 vmask;
+        if (!FULL) {
+          const int tb = t_step + 32 * ww;
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const int t0 = tb + (k < 2 ? 4 * quad + 2 * k : 16 + 4 * quad + 2 * (k - 2));
-          vmask[k] = (t0 < t_end ? 0x0000FFFFu : 0u) | (t0 + 1 < t_end ? 0xFFFF0000u : 0u);
-        }
-      }
-      const uint8_t* vb = vcode + ww * 32 * p.v_row_bytes;
-#pragma unroll
-      for (int t = 0; t < NTW; ++t) {
-        const int nt = w * NTW + t;
-        if (nt >= NT) continue;
-        u4 v;
-        if (QM == STARKV_Q_F16) {
-          v = *reinterpret_cast<const u4*>(vb + v_off[t]);
-        } else {
-          const uint8_t* mb = vmeta + ((ww * p.v_ng + v_gi[t]) * 4 + quad) * 32;
-          const u4 sv = *reinterpret_cast<const u4*>(mb);
-          const u4 zv = *reinterpret_cast<const u4*>(mb + 16);
-          // a 16-channel tile is all 8-bit, all 4-bit, or (only when the outlier
-          // count is not a multiple of 16) mixed across lanes
-          const int lo_ch = 16 * nt, hi_ch = 16 * nt + 16;
-          if (QM == STARKV_Q_MIX8_4 && hi_ch <= p.v_ro) {
-            const u2 d = *reinterpret_cast<const u2*>(vb + v_off[t]);
-            v = deq_int8p(d, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y), as_h2(sv.z),
-                          as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
-          } else if (lo_ch >= p.v_ro) {
-            const uint32_t d = *reinterpret_cast<const uint32_t*>(vb + v_off[t]);
-            v = deq_int4m(d, nib_mask, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y),
-                          as_h2(sv.z), as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
-          } else if (16 * nt + col < p.v_ro) {
-            const u2 d = *reinterpret_cast<const u2*>(vb + v_off[t]);
-            v = deq_int8p(d, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y), as_h2(sv.z),
-                          as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
-          } else {
-            const uint32_t d = *reinterpret_cast<const uint32_t*>(vb + v_off[t]);
-            v = deq_int4m(d, nib_mask, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y),
-                          as_h2(sv.z), as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
+          for (int k = 0; k < 4; ++k) {
+            const int t0 = tb + (k < 2 ? 4 * quad + 2 * k : 16 + 4 * quad + 2 * (k - 2));
+            vmask[k] = (t0 < t_end ? 0x0000FFFFu : 0u) | (t0 + 1 < t_end ? 0xFFFF0000u : 0u);
           }
         }
-        if (!full) v &= vmask;
-        const h8 vop = __builtin_bit_cast(h8, v);
+        const uint8_t* vb = vcode + ww * 32 * p.v_row_bytes;
 #pragma unroll
-        for (int c = 0; c < CT; ++c) acc_v[c][t] = mfma16(pa[c], vop, acc_v[c][t]);
+        for (int t = 0; t < NTW; ++t) {
+          u4 v;
+          if (QM == STARKV_Q_F16) {
+            v = *reinterpret_cast<const u4*>(vb + v_off[t]);
+          } else {
+            const uint8_t* mb = vmeta + ((ww * p.v_ng + v_gi[t]) * 4 + quad) * 32;
+            const u4 sv = *reinterpret_cast<const u4*>(mb);
+            const u4 zv = *reinterpret_cast<const u4*>(mb + 16);
+            if (VM == kValues8) {
+              const u2 d = *reinterpret_cast<const u2*>(vb + v_off[t]);
+              v = deq_int8p(d, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y), as_h2(sv.z),
+                            as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
+            } else if (VM == kValues4) {
+              const uint32_t d = *reinterpret_cast<const uint32_t*>(vb + v_off[t]);
+              v = deq_int4m(d, nib_mask, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y),
+                            as_h2(sv.z), as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
+            } else {
+              // 8-bit and 4-bit lanes in one wave: an aligned 8-byte read
+              // serves both (a 4-bit lane takes the half holding its word)
+              const u2 d = *reinterpret_cast<const u2*>(vb + (v_off[t] & ~7));
+              const uint32_t d4 = (v_off[t] & 4) ? d.y : d.x;
+              const u4 v8 = deq_int8p(d, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y),
+                                      as_h2(sv.z), as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
+              const u4 v4 = deq_int4m(d4, nib_mask, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y),
+                                      as_h2(zv.y), as_h2(sv.z), as_h2(zv.z), as_h2(sv.w),
+                                      as_h2(zv.w));
+              v = v_is8[t] ? v8 : v4;
+            }
+          }
+          if (!FULL) v &= vmask;
+          const h8 vop = __builtin_bit_cast(h8, v);
+#pragma unroll
+          for (int c = 0; c < CT; ++c) acc_v[c][t] = mfma16(pa[c], vop, acc_v[c][t]);
+        }
       }
-    }
+    };
+    using Full = std::true_type;
+    if (!full) values(std::integral_constant<int, kValuesMixed>{}, std::false_type{});
+    else if (vmode == kValues8) values(std::integral_constant<int, kValues8>{}, Full{});
+    else if (vmode == kValues4) values(std::integral_constant<int, kValues4>{}, Full{});
+    else values(std::integral_constant<int, kValuesMixed>{}, Full{});
     if (step + 1 < n_steps) {
       __syncthreads();   // every wave is done reading this step's values
       load_v(step + 1);
