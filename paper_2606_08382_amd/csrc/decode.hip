@@ -421,11 +421,6 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   const int qzero = nql * QS;
 
   // ---------------------------------------------------------------- prologue
-  {
-    u4* f = reinterpret_cast<u4*>(smem + LL.frag);
-    const int n = p.hg_frags[hg] * 64;
-    for (int i = tid; i < n; i += kThreads) f[i] = (u4){0, 0, 0, 0};
-  }
   if (tid < nql) qmap[tid] = p.kh[g0 + tid / G].head * G + tid % G;
   if (tid < 128) qc[qzero + tid] = (_Float16)0.0f;
   // RoPE tables: the lane's in-step offset u = 32*tg + 16*s + col composed as
@@ -487,24 +482,61 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   // Up-projection fragments.  Fragment (slot, m-tile mt, k-block kb), lane
   // (jj, kq): 8 halves = B_k[row][16*mt + jj] for the 8 channels of chunk
   // 4*kb + kq, in the order the key operand delivers them (4-bit chunks:
-  // channels 0,2,4,6,1,3,5,7; 8-bit and fp16 chunks in order).
-  for (int gg = g0; gg < g1; ++gg) {
-    const KHeadInfo& kh = p.kh[gg];
-    const int nvec = kh.rank * (D / 8);
-    for (int i = tid; i < nvec; i += kThreads) {
-      const int row = i / (D / 8), j8 = i % (D / 8);
-      const u4 v = *reinterpret_cast<const u4*>(p.bk + (int64_t)(kh.bk_row + row) * D + 8 * j8);
-      const _Float16* hv = reinterpret_cast<const _Float16*>(&v);
-      const int c = row / 8, wi = row % 8;
-      const int kb = c / 4, kq = c % 4;
-      int e = wi;
-      if (QM != STARKV_Q_F16 && c >= kh.n8) e = (wi % 2 == 0) ? wi / 2 : 4 + wi / 2;
-      for (int u = 0; u < 8; ++u) {
-        const int j = 8 * j8 + u;
-        const int mt = j / 16, jj = j % 16;
-        _Float16* f = reinterpret_cast<_Float16*>(frag + (kh.frag_base + mt * kh.nkb + kb) * 64 +
-                                                  jj + 16 * kq);
-        f[e] = hv[u];
+  // channels 0,2,4,6,1,3,5,7; 8-bit and fp16 chunks in order); channels at or
+  // beyond the rank are zero.  Wave w gathers fragments w, w + 8, ... in
+  // batches whose loads are all issued before the first 16-byte LDS store.
+  {
+    constexpr int kBatch = 5;
+    const int n_fr = p.hg_frags[hg];
+    const int jj = lane & 15, kq = lane >> 4;
+    // lane i holds slot g0 + i: first fragment, k-blocks, 8-bit chunks, rank, B_k row
+    int l_fb = 0x7FFFFFFF, l_nkb = 1, l_n8 = 0, l_rank = 1, l_row = 0;
+    if (lane < g1 - g0) {
+      const KHeadInfo& k = p.kh[g0 + lane];
+      l_fb = k.frag_base;
+      l_nkb = k.nkb;
+      l_n8 = k.n8;
+      l_rank = k.rank;
+      l_row = k.bk_row;
+    }
+    for (int f0 = w; f0 < n_fr; f0 += kBatch * kWaves) {
+      // rows beyond the rank (and fragments beyond the group) load a valid
+      // element and are zeroed afterwards, so no load sits behind a branch
+      uint16_t ld[kBatch][8];
+      uint32_t live[kBatch];   // bit e: element e is a channel below the rank
+#pragma unroll
+      for (int k = 0; k < kBatch; ++k) {
+        const int f = min(f0 + k * kWaves, n_fr - 1);
+        // the fragment's slot: the last one whose first fragment is <= f
+        const int hs = __builtin_popcountll(__ballot(l_fb <= f)) - 1;
+        const int fb = __builtin_amdgcn_readlane(l_fb, hs);
+        const int nkb = __builtin_amdgcn_readlane(l_nkb, hs);
+        const int n8 = __builtin_amdgcn_readlane(l_n8, hs);
+        const int rank = __builtin_amdgcn_readlane(l_rank, hs);
+        const int bk_row = __builtin_amdgcn_readlane(l_row, hs);
+        const int fl = f - fb;
+        const int mt = fl / nkb, kb = fl % nkb;
+        const int c = 4 * kb + kq;
+        const bool four = QM != STARKV_Q_F16 && c >= n8;
+        const uint16_t* src = p.bk + (int64_t)bk_row * D + 16 * mt + jj;
+        live[k] = 0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int wi = four ? (e < 4 ? 2 * e : 2 * (e - 4) + 1) : e;
+          const int row = 8 * c + wi;
+          live[k] |= row < rank ? 1u << e : 0u;
+          ld[k][e] = src[(int64_t)min(row, rank - 1) * D];
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < kBatch; ++k) {
+        const int f = f0 + k * kWaves;
+        u4 v;
+#pragma unroll
+        for (int h = 0; h < 4; ++h)
+          v[h] = ((live[k] >> (2 * h)) & 1u ? (uint32_t)ld[k][2 * h] : 0u) |
+                 ((live[k] >> (2 * h + 1)) & 1u ? (uint32_t)ld[k][2 * h + 1] << 16 : 0u);
+        if (f < n_fr) frag[f * 64 + lane] = __builtin_bit_cast(h8, v);
       }
     }
   }
@@ -555,22 +587,23 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   // below 64 KiB); row bytes (9 bits), rank (8), 8-bit chunks (3), 8-bit groups
   // (2), groups (3), slot in the group (4); fragment base; plane offsets / 256
   // (planes are 256-byte aligned).
+  // Lane i reads the i-th head's parameters (one round of loads for all heads).
   uint32_t t_raw = 0, t_geo = 0, t_fb = 0, t_code = 0, t_meta = 0;
-  int n_kw = 0;
-  for (int i = 0; i < n_h; ++i) {
-    const int gg = p.order[c0 + i];
+  int l_kw = 0;   // this lane's head: copies per step
+  if (lane < n_h) {
+    const int gg = p.order[c0 + lane];
     const KHeadInfo& kh = p.kh[gg];
-    n_kw += (32 * kh.row_bytes + 1023) / 1024;
-    if (QM != STARKV_Q_F16) n_kw += (2 * kh.ngroups * 64 + 1023) / 1024;
-    if (lane == i) {
-      t_raw = (uint32_t)kh.raw_code | ((uint32_t)kh.raw_meta << 16);
-      t_geo = (uint32_t)kh.row_bytes | ((uint32_t)kh.rank << 9) | ((uint32_t)kh.n8 << 17) |
-              ((uint32_t)kh.ng8 << 20) | ((uint32_t)kh.ngroups << 22) | ((uint32_t)(gg - g0) << 25);
-      t_fb = (uint32_t)kh.frag_base;
-      t_code = (uint32_t)(kh.code_off >> 8);
-      t_meta = (uint32_t)(kh.meta_off >> 8);
-    }
+    l_kw = (32 * kh.row_bytes + 1023) / 1024;
+    if (QM != STARKV_Q_F16) l_kw += (2 * kh.ngroups * 64 + 1023) / 1024;
+    t_raw = (uint32_t)kh.raw_code | ((uint32_t)kh.raw_meta << 16);
+    t_geo = (uint32_t)kh.row_bytes | ((uint32_t)kh.rank << 9) | ((uint32_t)kh.n8 << 17) |
+            ((uint32_t)kh.ng8 << 20) | ((uint32_t)kh.ngroups << 22) | ((uint32_t)(gg - g0) << 25);
+    t_fb = (uint32_t)kh.frag_base;
+    t_code = (uint32_t)(kh.code_off >> 8);
+    t_meta = (uint32_t)(kh.meta_off >> 8);
   }
+  int n_kw = 0;
+  for (int i = 0; i < n_h; ++i) n_kw += __builtin_amdgcn_readlane(l_kw, i);
   auto head_rt = [&](int i) {
     HeadRt h;
     const uint32_t raw_ = __builtin_amdgcn_readlane(t_raw, i);
