@@ -103,7 +103,7 @@ __device__ __forceinline__ u4 deq_int4m(uint32_t w, uint32_t mask, h2 s0, h2 z0,
 
 // LDS layout of the split kernel (byte offsets); identical on the host.
 struct SplitLds {
-  int frag, qc, red, alpha, flag, rot, qmap, loop, raw, vcode, vmeta, pbuf, rope, total;
+  int frag, qc, red, alpha, flag, prog, rot, qmap, loop, raw, vcode, vmeta, pbuf, rope, total;
 };
 
 // vcode_bytes: value codes of one step (kStepTokens tokens), a multiple of 16.
@@ -115,7 +115,8 @@ __host__ __device__ inline SplitLds split_lds(int frags, int nql, int head_dim, 
   L.red = L.qc + ((nql * (head_dim + 8) * 2 + 256 + 15) / 16) * 16;
   L.alpha = L.red + kTokenGroups * ct * 16 * 4;
   L.flag = L.alpha + ct * 16 * 4;
-  L.rot = L.flag + kWaves * 4;
+  L.prog = L.flag + kWaves * 4;
+  L.rot = L.prog + kWaves * 4;
   L.qmap = L.rot + 64 * 8;
   L.loop = L.qmap + 64 * 4;
   L.raw = L.loop;
@@ -410,6 +411,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   float* red = reinterpret_cast<float*>(smem + LL.red);
   float* alpha_s = reinterpret_cast<float*>(smem + LL.alpha);
   int* flag_s = reinterpret_cast<int*>(smem + LL.flag);
+  int* prog_s = reinterpret_cast<int*>(smem + LL.prog);   // key-phase progress per wave
   float2* rot_s = reinterpret_cast<float2*>(smem + LL.rot);        // [64] step rotations
   int* qmap = reinterpret_cast<int*>(smem + LL.qmap);             // slot-local -> query head
   uint8_t* raw = smem + LL.raw + w * raw_bytes;
@@ -687,6 +689,16 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 #pragma unroll
     for (int t = 0; t < NTW; ++t) acc_v[c][t] = (f4){0, 0, 0, 0};
 
+  // key cost per step of this wave's half and of the other half (units of
+  // 2 + k-blocks per head, as the host balances them)
+  int cost_me = 0, cost_other = 0;
+#pragma unroll
+  for (int k = 1; k <= NKBS; ++k) {
+    cost_me += (p.cls[hg][hh][k] - p.cls[hg][hh][k - 1]) * (2 + k);
+    cost_other += (p.cls[hg][1 - hh][k] - p.cls[hg][1 - hh][k - 1]) * (2 + k);
+  }
+  int prog = 0;
+  if (lane == 0) prog_s[w] = 0;
   for (int i = 0; i < n_h; ++i) copy_head(head_rt(i), 0);
   load_v(0);
   __syncthreads();   // rotated queries of step 0 and the fragments visible
@@ -706,9 +718,16 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 #pragma unroll
       for (int c = 0; c < CTH; ++c) acc_s[s][c] = (f4){0, 0, 0, 0};
 
+    // The two waves sharing a SIMD (w and w ^ 4, one per head half) split its
+    // issue slots unevenly: at equal priority the older wave (w < 4) wins, and
+    // the younger ends up running its last heads alone.  After every head a
+    // wave compares its share of the key work done (cumulative cost over the
+    // half's cost per step) with its partner's and takes the higher priority
+    // while it is behind; the younger also takes it on a tie.
 #pragma unroll
     for (int k = 1; k <= NKBS; ++k) {
       for (int i = cls_end[k - 1]; i < cls_end[k]; ++i) {
+        const int partner = prog_s[w ^ 4];
         const HeadRt kh = head_rt(i);
         if (k == 1) key_head<D, QM, CTH, 1>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, quad, cs, acc_s);
         if (k == 2) key_head<D, QM, CTH, 2>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, quad, cs, acc_s);
@@ -717,8 +736,14 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
         // the head's staging has been read (its values are consumed): copy
         // the next step's codes and meta of this head into it
         if (step + 1 < n_steps) copy_head(kh, step + 1);
+        prog += 2 + k;
+        if (lane == 0) prog_s[w] = prog;
+        const int mine_n = prog * cost_other, part_n = partner * cost_me;
+        if (part_n > mine_n || (hh == 1 && part_n == mine_n)) __builtin_amdgcn_s_setprio(1);
+        else __builtin_amdgcn_s_setprio(0);
       }
     }
+    __builtin_amdgcn_s_setprio(0);
 
     // ------------------------------------------ online softmax (log2 domain)
     // scores are already in log2 units (the query carries log2(e)/sqrt(d))
