@@ -124,8 +124,8 @@ __host__ __device__ inline SplitLds split_lds(int frags, int nql, int head_dim, 
   L.vmeta = L.vcode + vcode_bytes;
   L.pbuf = L.vmeta + 4 * v_ng * 128;
   int loop_end = L.pbuf + kTokenGroups * ct * 1024;
-  L.rope = L.loop;   // RoPE tables (prologue only) alias the loop area
-  int rope_end = L.rope + (16 * 64 + 8 * 64) * 8;
+  L.rope = L.vcode;   // RoPE tables (prologue only) alias the value staging
+  int rope_end = L.rope + (16 * 65 + 8 * 64) * 8;
   L.total = loop_end > rope_end ? loop_end : rope_end;
   return L;
 }
@@ -396,7 +396,49 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   const int ct0 = hh ? ct_half : 0;                        // first score tile of this half
   const int ctn = hh ? (nql + 15) / 16 - ct_half : ct_half; // its tile count
 
+  // ---------------------------------------------------------------- prologue
+  // Every load whose address is known at entry is issued first (context
+  // length, this half's head table, the fragment table, the query heads of
+  // this thread's query vectors); the key copies of step 0, the fragment and
+  // query loads follow, and the RoPE tables are computed while they are in
+  // flight.  The prologue then costs about two memory round trips.
   int L = p.ctx_len[b];
+  // The half's heads in processing order (grouped by k-block count): lane i
+  // of the head table holds the i-th head's packed fields (staging offsets;
+  // row bytes, rank, 8-bit chunks, 8-bit groups, groups, slot; fragment base;
+  // plane offsets / 256).
+  const int c0 = p.cls[hg][hh][0];
+  int cls_end[NKBS + 1];
+#pragma unroll
+  for (int k = 0; k <= NKBS; ++k) cls_end[k] = p.cls[hg][hh][k] - c0;
+  const int n_h = cls_end[NKBS];
+  uint32_t t_raw = 0, t_geo = 0, t_fb = 0, t_code = 0, t_meta = 0;
+  if (lane < n_h) {
+    t_raw = p.o_raw[c0 + lane];
+    t_geo = p.o_geo[c0 + lane];
+    t_fb = p.o_fb[c0 + lane];
+    t_code = p.o_code[c0 + lane];
+    t_meta = p.o_meta[c0 + lane];
+  }
+  // fragment table: lane i holds slot g0 + i (first fragment, k-blocks,
+  // 8-bit chunks, rank, first B_k row)
+  int l_fb = 0x7FFFFFFF, l_nkb = 1, l_n8 = 0, l_rank = 1, l_row = 0;
+  if (lane < g1 - g0) {
+    const KHeadInfo& k = p.kh[g0 + lane];
+    l_fb = k.frag_base;
+    l_nkb = k.nkb;
+    l_n8 = k.n8;
+    l_rank = k.rank;
+    l_row = k.bk_row;
+  }
+  // query head of each of this thread's query vectors
+  int qh[NQV];
+#pragma unroll
+  for (int v = 0; v < NQV; ++v) {
+    const int il = (tid + v * kThreads) / (D / 8);
+    qh[v] = il < nql ? p.kh[g0 + il / G].head * G + il % G : 0;
+  }
+  const int qm = tid < nql ? p.kh[g0 + tid / G].head * G + tid % G : 0;
   L = L < 0 ? 0 : (L > p.max_ctx ? p.max_ctx : L);
   const int t_begin = split * p.split_len;
   if (t_begin >= L) return;
@@ -418,40 +460,112 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   uint8_t* vcode = smem + LL.vcode;
   uint8_t* vmeta = smem + LL.vmeta;
   h8* pbuf = reinterpret_cast<h8*>(smem + LL.pbuf);
-  float2* rope_col = reinterpret_cast<float2*>(smem + LL.rope);   // [16][64]
-  float2* rope_ws = rope_col + 16 * 64;                           // [8][64]
+  float2* rope_col = reinterpret_cast<float2*>(smem + LL.rope);   // [16][65]
+  float2* rope_ws = rope_col + 16 * 65;   // [8][64]; rope_col rows are padded to 65 (banks)
   const int qzero = nql * QS;
 
-  // ---------------------------------------------------------------- prologue
-  if (tid < nql) qmap[tid] = p.kh[g0 + tid / G].head * G + tid % G;
+  if (tid < nql) qmap[tid] = qm;
   if (tid < 128) qc[qzero + tid] = (_Float16)0.0f;
-  // RoPE tables: the lane's in-step offset u = 32*tg + 16*s + col composed as
-  // the subtile rotation (16*(2*tg + s)) times the column rotation (col), and
-  // the rotation by one step (kStepTokens) for the query's base position.
+  // Key staging: the wave's 32 tokens of every key head of its half, codes then
+  // meta per head, copied straight into the wave's LDS area.  A head's copy for
+  // the next step is issued as soon as the head has been processed, so the
+  // copies have most of a step to land.  Lane 0 of every issued copy is active,
+  // so the wave issues exactly n_kw copies per step.
+  const int64_t blk16 = (int64_t)b * (p.cap_pad / 16) + (t_begin + 32 * tg) / 16;
+  auto copy_head = [&](const HeadRt& kh, int step) {
+    const int64_t blk = blk16 + (int64_t)step * (kStepTokens / 16);
+    copy_to_lds_wave(raw + kh.raw_code, p.cache + kh.code_off + blk * 16 * kh.row_bytes,
+                     32 * kh.row_bytes, lane);
+    if (QM != STARKV_Q_F16)
+      copy_to_lds_wave(raw + kh.raw_meta, p.cache + kh.meta_off + blk * kh.ngroups * 64,
+                       2 * kh.ngroups * 64, lane);
+  };
+  auto head_rt = [&](int i) {
+    HeadRt h;
+    const uint32_t raw_ = __builtin_amdgcn_readlane(t_raw, i);
+    const uint32_t geo = __builtin_amdgcn_readlane(t_geo, i);
+    h.raw_code = (int)(raw_ & 0xFFFFu);
+    h.raw_meta = (int)(raw_ >> 16);
+    h.row_bytes = (int)(geo & 0x1FFu);
+    h.rank = (int)((geo >> 9) & 0xFFu);
+    h.n8 = (int)((geo >> 17) & 7u);
+    h.ng8 = (int)((geo >> 20) & 3u);
+    h.ngroups = (int)((geo >> 22) & 7u);
+    h.gl = (int)((geo >> 25) & 15u);
+    h.frag_base = (int)__builtin_amdgcn_readlane(t_fb, i);
+    h.code_off = (int64_t)__builtin_amdgcn_readlane(t_code, i) << 8;
+    h.meta_off = (int64_t)__builtin_amdgcn_readlane(t_meta, i) << 8;
+    return h;
+  };
+  int n_kw = 0;   // key copies per step
   {
-    const double l2t = p.log2_theta;
-    for (int i = tid; i < HALF; i += kThreads) {
-      const double om = exp2(-(2.0 * i / D) * l2t);
-      float ss, cs;
-      sincosf((float)(kStepTokens * om), &ss, &cs);
-      rot_s[i] = make_float2(cs, ss);
+    int l_kw = 0;
+    if (lane < n_h) {
+      const int rb = (int)(t_geo & 0x1FFu), ng = (int)((t_geo >> 22) & 7u);
+      l_kw = (32 * rb + 1023) / 1024;
+      if (QM != STARKV_Q_F16) l_kw += (2 * ng * 64 + 1023) / 1024;
     }
-    for (int i = tid; i < 16 * HALF; i += kThreads) {
-      const int c = i / HALF, j = i % HALF;
-      const float om = (float)exp2(-(2.0 * j / D) * l2t);
-      float ss, cs;
-      sincosf((float)c * om, &ss, &cs);
-      rope_col[c * 64 + j] = make_float2(cs, ss);
-    }
-    for (int i = tid; i < 8 * HALF; i += kThreads) {
-      const int k = i / HALF, j = i % HALF;
-      const double om = exp2(-(2.0 * j / D) * l2t);
-      float ss, cs;
-      sincosf((float)(16.0 * k * om), &ss, &cs);
-      rope_ws[k * 64 + j] = make_float2(cs, ss);
-    }
+    for (int i = 0; i < n_h; ++i) n_kw += __builtin_amdgcn_readlane(l_kw, i);
   }
-  __syncthreads();   // qmap, tables
+  // step 0's key copies (the key staging is not used by the prologue)
+  for (int i = 0; i < n_h; ++i) copy_head(head_rt(i), 0);
+
+  // Up-projection fragments.  Fragment (slot, m-tile mt, k-block kb), lane
+  // (jj, kq): 8 halves = B_k[row][16*mt + jj] for the 8 channels of chunk
+  // 4*kb + kq, in the order the key operand delivers them (4-bit chunks:
+  // channels 0,2,4,6,1,3,5,7; 8-bit and fp16 chunks in order); channels at or
+  // beyond the rank are zero.  Wave w gathers fragments w, w + 8, ... in
+  // batches whose loads are all issued before the first 16-byte LDS store.
+  constexpr int kBatch = 5;
+  const int n_fr = p.hg_frags[hg];
+  // rows beyond the rank (and fragments beyond the group) load a valid
+  // element and are zeroed when stored, so no load sits behind a branch
+  auto frag_load = [&](int f0, uint16_t (&ld)[kBatch][8], uint32_t (&live)[kBatch]) {
+    const int jj = lane & 15, kq = lane >> 4;
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const int f = min(f0 + k * kWaves, n_fr - 1);
+      // the fragment's slot: the last one whose first fragment is <= f
+      const int hs = __builtin_popcountll(__ballot(l_fb <= f)) - 1;
+      const int fb = __builtin_amdgcn_readlane(l_fb, hs);
+      const int nkb = __builtin_amdgcn_readlane(l_nkb, hs);
+      const int n8 = __builtin_amdgcn_readlane(l_n8, hs);
+      const int rank = __builtin_amdgcn_readlane(l_rank, hs);
+      const int bk_row = __builtin_amdgcn_readlane(l_row, hs);
+      const int fl = f - fb;
+      const int mt = fl / nkb, kb = fl % nkb;
+      const int c = 4 * kb + kq;
+      const bool four = QM != STARKV_Q_F16 && c >= n8;
+      const uint16_t* src = p.bk + (int64_t)bk_row * D + 16 * mt + jj;
+      live[k] = 0;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int wi = four ? (e < 4 ? 2 * e : 2 * (e - 4) + 1) : e;
+        const int row = 8 * c + wi;
+        live[k] |= row < rank ? 1u << e : 0u;
+        ld[k][e] = src[(int64_t)min(row, rank - 1) * D];
+      }
+    }
+  };
+  auto frag_store = [&](int f0, const uint16_t (&ld)[kBatch][8], const uint32_t (&live)[kBatch]) {
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const int f = f0 + k * kWaves;
+      u4 v;
+#pragma unroll
+      for (int h = 0; h < 4; ++h)
+        v[h] = ((live[k] >> (2 * h)) & 1u ? (uint32_t)ld[k][2 * h] : 0u) |
+               ((live[k] >> (2 * h + 1)) & 1u ? (uint32_t)ld[k][2 * h + 1] << 16 : 0u);
+      if (f < n_fr) frag[f * 64 + lane] = __builtin_bit_cast(h8, v);
+    }
+  };
+  // the fragment area is free from the start: batch 0 is loaded here and
+  // stored after the RoPE tables are computed, batch 1 is loaded then and
+  // stored after the key rotations, and any further batches follow
+  uint16_t ld0[kBatch][8], ld1[kBatch][8];
+  uint32_t live0[kBatch], live1[kBatch];
+  frag_load(w, ld0, live0);
+
   // this thread's query vectors (fp32) and the base rotation of its four
   // frequencies at t_begin (angle reduced in fp64)
   float qo[NQV][8];
@@ -470,9 +584,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     }
 #pragma unroll
     for (int v = 0; v < NQV; ++v) {
-      const int il = (tid + v * kThreads) / (D / 8);
-      const int qh = il < nql ? qmap[il] : 0;
-      const uint16_t* qs = static_cast<const uint16_t*>(p.q) + ((int64_t)b * p.n_q + qh) * D;
+      const uint16_t* qs = static_cast<const uint16_t*>(p.q) + ((int64_t)b * p.n_q + qh[v]) * D;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         qo[v][e] = load_qf(qs, j0 + e, p.q_bf16) * p.score_scale;
@@ -480,68 +592,36 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       }
     }
   }
-  store_rotated_q<D, NQV>(qc, nql, tid, qo, bs);
-  // Up-projection fragments.  Fragment (slot, m-tile mt, k-block kb), lane
-  // (jj, kq): 8 halves = B_k[row][16*mt + jj] for the 8 channels of chunk
-  // 4*kb + kq, in the order the key operand delivers them (4-bit chunks:
-  // channels 0,2,4,6,1,3,5,7; 8-bit and fp16 chunks in order); channels at or
-  // beyond the rank are zero.  Wave w gathers fragments w, w + 8, ... in
-  // batches whose loads are all issued before the first 16-byte LDS store.
+  // RoPE tables: the lane's in-step offset u = 32*tg + 16*s + col composed as
+  // the subtile rotation (16*(2*tg + s)) times the column rotation (col), and
+  // the rotation by one step (kStepTokens) for the query's base position.
   {
-    constexpr int kBatch = 5;
-    const int n_fr = p.hg_frags[hg];
-    const int jj = lane & 15, kq = lane >> 4;
-    // lane i holds slot g0 + i: first fragment, k-blocks, 8-bit chunks, rank, B_k row
-    int l_fb = 0x7FFFFFFF, l_nkb = 1, l_n8 = 0, l_rank = 1, l_row = 0;
-    if (lane < g1 - g0) {
-      const KHeadInfo& k = p.kh[g0 + lane];
-      l_fb = k.frag_base;
-      l_nkb = k.nkb;
-      l_n8 = k.n8;
-      l_rank = k.rank;
-      l_row = k.bk_row;
+    const double l2t = p.log2_theta;
+    for (int i = tid; i < HALF; i += kThreads) {
+      const double om = exp2(-(2.0 * i / D) * l2t);
+      float ss, cs;
+      sincosf((float)(kStepTokens * om), &ss, &cs);
+      rot_s[i] = make_float2(cs, ss);
     }
-    for (int f0 = w; f0 < n_fr; f0 += kBatch * kWaves) {
-      // rows beyond the rank (and fragments beyond the group) load a valid
-      // element and are zeroed afterwards, so no load sits behind a branch
-      uint16_t ld[kBatch][8];
-      uint32_t live[kBatch];   // bit e: element e is a channel below the rank
-#pragma unroll
-      for (int k = 0; k < kBatch; ++k) {
-        const int f = min(f0 + k * kWaves, n_fr - 1);
-        // the fragment's slot: the last one whose first fragment is <= f
-        const int hs = __builtin_popcountll(__ballot(l_fb <= f)) - 1;
-        const int fb = __builtin_amdgcn_readlane(l_fb, hs);
-        const int nkb = __builtin_amdgcn_readlane(l_nkb, hs);
-        const int n8 = __builtin_amdgcn_readlane(l_n8, hs);
-        const int rank = __builtin_amdgcn_readlane(l_rank, hs);
-        const int bk_row = __builtin_amdgcn_readlane(l_row, hs);
-        const int fl = f - fb;
-        const int mt = fl / nkb, kb = fl % nkb;
-        const int c = 4 * kb + kq;
-        const bool four = QM != STARKV_Q_F16 && c >= n8;
-        const uint16_t* src = p.bk + (int64_t)bk_row * D + 16 * mt + jj;
-        live[k] = 0;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int wi = four ? (e < 4 ? 2 * e : 2 * (e - 4) + 1) : e;
-          const int row = 8 * c + wi;
-          live[k] |= row < rank ? 1u << e : 0u;
-          ld[k][e] = src[(int64_t)min(row, rank - 1) * D];
-        }
-      }
-#pragma unroll
-      for (int k = 0; k < kBatch; ++k) {
-        const int f = f0 + k * kWaves;
-        u4 v;
-#pragma unroll
-        for (int h = 0; h < 4; ++h)
-          v[h] = ((live[k] >> (2 * h)) & 1u ? (uint32_t)ld[k][2 * h] : 0u) |
-                 ((live[k] >> (2 * h + 1)) & 1u ? (uint32_t)ld[k][2 * h + 1] << 16 : 0u);
-        if (f < n_fr) frag[f * 64 + lane] = __builtin_bit_cast(h8, v);
-      }
+    for (int i = tid; i < 16 * HALF; i += kThreads) {
+      const int c = i / HALF, j = i % HALF;
+      const float om = (float)exp2(-(2.0 * j / D) * l2t);
+      float ss, cs;
+      sincosf((float)c * om, &ss, &cs);
+      rope_col[c * 65 + j] = make_float2(cs, ss);
+    }
+    for (int i = tid; i < 8 * HALF; i += kThreads) {
+      const int k = i / HALF, j = i % HALF;
+      const double om = exp2(-(2.0 * j / D) * l2t);
+      float ss, cs;
+      sincosf((float)(16.0 * k * om), &ss, &cs);
+      rope_ws[k * 64 + j] = make_float2(cs, ss);
     }
   }
+  frag_store(w, ld0, live0);
+  frag_load(w + kBatch * kWaves, ld1, live1);
+  __syncthreads();   // query map, tables
+  store_rotated_q<D, NQV>(qc, nql, tid, qo, bs);
   // the lane's fixed key rotations, packed fp16
   CS4 cs[2][NKBS];
 #pragma unroll
@@ -552,7 +632,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int j = 16 * kq + 4 * quad + e;
-        const float2 r = cmul(rope_ws[(2 * tg + s) * 64 + j], rope_col[col * 64 + j]);
+        const float2 r = cmul(rope_ws[(2 * tg + s) * 64 + j], rope_col[col * 65 + j]);
         cc[e] = r.x;
         ss[e] = r.y;
       }
@@ -561,68 +641,15 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       cs[s][kq].s01 = __builtin_convertvector((f2){ss[0], ss[1]}, h2);
       cs[s][kq].s23 = __builtin_convertvector((f2){ss[2], ss[3]}, h2);
     }
-  __syncthreads();   // RoPE tables are dead from here on (the loop area reuses them)
-
-  // ---------------------------------------------------------------- prefetch setup
-  // Key staging: the wave's 32 tokens of every key head of its half, codes then
-  // meta per head, copied straight into the wave's LDS area.  A head's copy for
-  // the next step is issued as soon as the head has been processed, so the
-  // copies have most of a step to land.  Lane 0 of every issued copy is active,
-  // so the wave issues exactly n_kw copies per step.
-  const int64_t blk16 = (int64_t)b * (p.cap_pad / 16) + (t_begin + 32 * tg) / 16;
-  auto copy_head = [&](const HeadRt& kh, int step) {
-    const int64_t blk = blk16 + (int64_t)step * (kStepTokens / 16);
-    copy_to_lds_wave(raw + kh.raw_code, p.cache + kh.code_off + blk * 16 * kh.row_bytes,
-                     32 * kh.row_bytes, lane);
-    if (QM != STARKV_Q_F16)
-      copy_to_lds_wave(raw + kh.raw_meta, p.cache + kh.meta_off + blk * kh.ngroups * 64,
-                       2 * kh.ngroups * 64, lane);
-  };
-  // The half's heads in processing order (grouped by k-block count): lane i
-  // of the head table holds the i-th head's values.
-  const int c0 = p.cls[hg][hh][0];
-  int cls_end[NKBS + 1];
-#pragma unroll
-  for (int k = 0; k <= NKBS; ++k) cls_end[k] = p.cls[hg][hh][k] - c0;
-  const int n_h = cls_end[NKBS];
-  // Packed fields: staging offsets (16 bits each; a wave's staging is far
-  // below 64 KiB); row bytes (9 bits), rank (8), 8-bit chunks (3), 8-bit groups
-  // (2), groups (3), slot in the group (4); fragment base; plane offsets / 256
-  // (planes are 256-byte aligned).
-  // Lane i reads the i-th head's parameters (one round of loads for all heads).
-  uint32_t t_raw = 0, t_geo = 0, t_fb = 0, t_code = 0, t_meta = 0;
-  int l_kw = 0;   // this lane's head: copies per step
-  if (lane < n_h) {
-    const int gg = p.order[c0 + lane];
-    const KHeadInfo& kh = p.kh[gg];
-    l_kw = (32 * kh.row_bytes + 1023) / 1024;
-    if (QM != STARKV_Q_F16) l_kw += (2 * kh.ngroups * 64 + 1023) / 1024;
-    t_raw = (uint32_t)kh.raw_code | ((uint32_t)kh.raw_meta << 16);
-    t_geo = (uint32_t)kh.row_bytes | ((uint32_t)kh.rank << 9) | ((uint32_t)kh.n8 << 17) |
-            ((uint32_t)kh.ng8 << 20) | ((uint32_t)kh.ngroups << 22) | ((uint32_t)(gg - g0) << 25);
-    t_fb = (uint32_t)kh.frag_base;
-    t_code = (uint32_t)(kh.code_off >> 8);
-    t_meta = (uint32_t)(kh.meta_off >> 8);
+  frag_store(w + kBatch * kWaves, ld1, live1);
+  __syncthreads();   // RoPE tables are dead from here on (the value staging reuses them)
+  for (int f0 = w + 2 * kBatch * kWaves; f0 < n_fr; f0 += kBatch * kWaves) {
+    uint16_t ld[kBatch][8];
+    uint32_t live[kBatch];
+    frag_load(f0, ld, live);
+    frag_store(f0, ld, live);
   }
-  int n_kw = 0;
-  for (int i = 0; i < n_h; ++i) n_kw += __builtin_amdgcn_readlane(l_kw, i);
-  auto head_rt = [&](int i) {
-    HeadRt h;
-    const uint32_t raw_ = __builtin_amdgcn_readlane(t_raw, i);
-    const uint32_t geo = __builtin_amdgcn_readlane(t_geo, i);
-    h.raw_code = (int)(raw_ & 0xFFFFu);
-    h.raw_meta = (int)(raw_ >> 16);
-    h.row_bytes = (int)(geo & 0x1FFu);
-    h.rank = (int)((geo >> 9) & 0xFFu);
-    h.n8 = (int)((geo >> 17) & 7u);
-    h.ng8 = (int)((geo >> 20) & 3u);
-    h.ngroups = (int)((geo >> 22) & 7u);
-    h.gl = (int)((geo >> 25) & 15u);
-    h.frag_base = (int)__builtin_amdgcn_readlane(t_fb, i);
-    h.code_off = (int64_t)__builtin_amdgcn_readlane(t_code, i) << 8;
-    h.meta_off = (int64_t)__builtin_amdgcn_readlane(t_meta, i) << 8;
-    return h;
-  };
+
   // value codes and meta of one step are copied into LDS ahead of use; per-lane
   // offsets of this wave's channel tiles inside a 32-token block
   const int NT = p.rv / 16;
@@ -699,7 +726,6 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   }
   int prog = 0;
   if (lane == 0) prog_s[w] = 0;
-  for (int i = 0; i < n_h; ++i) copy_head(head_rt(i), 0);
   load_v(0);
   __syncthreads();   // rotated queries of step 0 and the fragments visible
 

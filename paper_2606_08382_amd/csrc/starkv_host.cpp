@@ -65,8 +65,10 @@ struct starkv_plan {
   int32_t hg_mid[STARKV_MAX_KV_HEADS];
   KHeadInfo kh[STARKV_MAX_KV_HEADS];      // per slot (see the decode kernel shape)
   int32_t bk_row[STARKV_MAX_KV_HEADS];    // per KV head: first row in B_k
-  int32_t order[STARKV_MAX_KV_HEADS];
   int32_t cls[STARKV_MAX_KV_HEADS][2][5];
+  // per processing position: the head's fields packed for the split kernel
+  uint32_t o_raw[STARKV_MAX_KV_HEADS], o_geo[STARKV_MAX_KV_HEADS], o_fb[STARKV_MAX_KV_HEADS];
+  uint32_t o_code[STARKV_MAX_KV_HEADS], o_meta[STARKV_MAX_KV_HEADS];
   int32_t lds_bytes;
 };
 
@@ -297,8 +299,29 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
       // processing order inside the half: slots sorted by k-block count
       for (int kk = 1; kk <= 4; ++kk) {
         P->cls[h][half][kk - 1] = pos;
-        for (int sl = ha; sl < hb; ++sl)
-          if (P->kh[sl].nkb == kk) P->order[pos++] = sl;
+        for (int sl = ha; sl < hb; ++sl) {
+          if (P->kh[sl].nkb != kk) continue;
+          const KHeadInfo& k = P->kh[sl];
+          // field widths: staging offsets < 64 KiB, row bytes < 512, rank < 256,
+          // 8-bit chunks < 8, 8-bit groups < 4, groups < 8, slot < 16, planes
+          // 256-byte aligned below 2^40 bytes
+          const bool fits = k.raw_meta < 65536 && k.raw_code < 65536 && k.row_bytes < 512 &&
+                            k.rank < 256 && k.n8 < 8 && k.ng8 < 4 && k.ngroups < 8 &&
+                            sl - a < 16 && (k.code_off >> 40) == 0 && (k.meta_off >> 40) == 0 &&
+                            k.code_off % 256 == 0 && k.meta_off % 256 == 0;
+          if (!fits) {
+            delete P;
+            return fail(STARKV_ERR_UNSUPPORTED, "head parameters exceed the split kernel's table");
+          }
+          P->o_raw[pos] = (uint32_t)k.raw_code | ((uint32_t)k.raw_meta << 16);
+          P->o_geo[pos] = (uint32_t)k.row_bytes | ((uint32_t)k.rank << 9) | ((uint32_t)k.n8 << 17) |
+                          ((uint32_t)k.ng8 << 20) | ((uint32_t)k.ngroups << 22) |
+                          ((uint32_t)(sl - a) << 25);
+          P->o_fb[pos] = (uint32_t)k.frag_base;
+          P->o_code[pos] = (uint32_t)(k.code_off >> 8);
+          P->o_meta[pos] = (uint32_t)(k.meta_off >> 8);
+          ++pos;
+        }
       }
       P->cls[h][half][4] = pos;
     }
@@ -442,7 +465,11 @@ starkv_status starkv_decode_split(const starkv_plan* P, const void* cache, const
   std::memcpy(p.hg_raw_bytes, P->hg_raw, sizeof(p.hg_raw_bytes));
   std::memcpy(p.hg_mid, P->hg_mid, sizeof(p.hg_mid));
   std::memcpy(p.kh, P->kh, sizeof(p.kh));
-  std::memcpy(p.order, P->order, sizeof(p.order));
+  std::memcpy(p.o_raw, P->o_raw, sizeof(p.o_raw));
+  std::memcpy(p.o_geo, P->o_geo, sizeof(p.o_geo));
+  std::memcpy(p.o_fb, P->o_fb, sizeof(p.o_fb));
+  std::memcpy(p.o_code, P->o_code, sizeof(p.o_code));
+  std::memcpy(p.o_meta, P->o_meta, sizeof(p.o_meta));
   std::memcpy(p.cls, P->cls, sizeof(p.cls));
   const int e = launch_decode_split_ntw(p, c.head_dim, c.qmode, P->ct, P->ntw, P->lds_bytes,
                                         static_cast<void*>(stream));

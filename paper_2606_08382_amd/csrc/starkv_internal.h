@@ -57,10 +57,17 @@ struct DecodeParams {
   int32_t hg_frags[STARKV_MAX_KV_HEADS];     // fragments used by the group
   int32_t hg_raw_bytes[STARKV_MAX_KV_HEADS]; // per-wave staging bytes (max over halves)
   KHeadInfo kh[STARKV_MAX_KV_HEADS];         // per slot
-  // slots of every half in processing order, grouped by k-block count:
-  // order[cls[hg][h][k-1] .. cls[hg][h][k]) are the half's slots with k k-blocks
-  int32_t order[STARKV_MAX_KV_HEADS];
+  // The heads of every half in processing order, grouped by k-block count:
+  // positions cls[hg][h][k-1] .. cls[hg][h][k]-1 are the half's heads with k
+  // k-blocks.  Per position, the head's fields packed for the kernel:
+  //   o_raw:  staging offset of the codes | staging offset of the meta << 16
+  //   o_geo:  row bytes | rank << 9 | 8-bit chunks << 17 | 8-bit groups << 20 |
+  //           groups << 22 | slot within the group << 25
+  //   o_fb:   first up-projection fragment
+  //   o_code, o_meta: plane offsets / 256
   int32_t cls[STARKV_MAX_KV_HEADS][2][5];
+  uint32_t o_raw[STARKV_MAX_KV_HEADS], o_geo[STARKV_MAX_KV_HEADS], o_fb[STARKV_MAX_KV_HEADS];
+  uint32_t o_code[STARKV_MAX_KV_HEADS], o_meta[STARKV_MAX_KV_HEADS];
 };
 
 constexpr int kCand = 32;      // rescoring candidates per (sequence, split, query head)
