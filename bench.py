@@ -26,6 +26,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_F16_PEAK_TFLOPS = 2500.0   # dense fp16 matrix peak
 COPY_BYTES = 256 << 20           # the plain device-to-device copy timed beside the path
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_split_c3_traffic.json")
 SPLIT_SOURCE = os.path.join(ROOT, "paper_2606_08382_amd", "csrc", "decode.hip")
@@ -89,6 +90,22 @@ def copy_stream(torch, stream, reps=5):
     ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
     return {"bytes_read": COPY_BYTES, "bytes_written": COPY_BYTES, "us": ms * 1e3,
             "GBps": 2 * COPY_BYTES / (ms / 1e3) / 1e9}
+
+
+def read_stream(torch, stream, n_bytes=1 << 30, reps=5):
+    """Bandwidth of a plain read-only stream: torch's sum over n_bytes of fp32, for context."""
+    x = torch.ones(n_bytes // 4, dtype=torch.float32, device="cuda")
+    torch.sum(x)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(reps)]
+    for a, b in evs:
+        a.record(stream)
+        torch.sum(x)
+        b.record(stream)
+    torch.cuda.synchronize()
+    ms = float(np.median([a.elapsed_time(b) for a, b in evs]))
+    del x
+    return {"bytes_read": n_bytes, "us": ms * 1e3, "GBps": n_bytes / (ms / 1e3) / 1e9}
 
 
 def main():
@@ -194,12 +211,19 @@ def main():
                      for g in range(w.n_kv_heads))
                  + layout.value_row_bytes + 4 * layout.value_groups)
     alg_bytes = per_token * tokens
+    # useful flops per cached token: key reconstruction 2*sum(r)*d, scores 2*H_q*d,
+    # value latents 2*H_q*r_v
+    flops_token = (2 * sum(inp.key_rank) * w.head_dim + 2 * w.n_q_heads * w.head_dim
+                   + 2 * w.n_q_heads * w.value_rank)
+    alg_flops = flops_token * tokens
     split_s = float(t_split.mean()) / 1e3
     achieved = alg_bytes / split_s / 1e9
     log(f"append {t_app.mean() * 1e3:.1f} us  split {t_split.mean() * 1e3:.1f} us "
         f"(median {np.median(t_split) * 1e3:.1f})  combine {t_comb.mean() * 1e3:.1f} us  "
         f"wall/step {ms_step * 1e3:.1f} us (eager {ms_eager * 1e3:.1f} us)")
     copy = copy_stream(torch, stream)
+    rstream = read_stream(torch, stream)
+    log(f"read stream {rstream['GBps']:.0f} GB/s")
     log(f"device copy {copy['GBps']:.0f} GB/s (read + write)")
     traffic, tsum = measured_traffic(w.name)
     result = {
@@ -223,8 +247,16 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": "decode_split", "alg_bytes_per_launch": alg_bytes,
-                     "bytes_per_token": per_token},
+                     "bytes_per_token": per_token,
+                     "frac_of_read_stream": achieved / rstream["GBps"]},
+        "roofline_mfma": {"achieved": alg_flops / split_s / 1e12, "peak": MFMA_F16_PEAK_TFLOPS,
+                          "unit": "TFLOP/s", "frac": alg_flops / split_s / 1e12 / MFMA_F16_PEAK_TFLOPS,
+                          "flops_per_token": flops_token,
+                          "note": "useful fp16 MFMA work: key reconstruction, scores, p.V'"},
+        "decode_split_us_median": float(np.median(t_split) * 1e3),
+        "context_tokens_per_s": tokens / (ms_step / 1e3),
         "copy_stream": copy,
+        "read_stream": rstream,
     }
     if tsum is not None:
         result["roofline"]["traffic_detail"] = {
