@@ -81,9 +81,22 @@ double orc_bf16_to_double(uint16_t b) {
 
 #define GROUP 32
 
+/* Bit widths of the two regions of a latent block: the outlier region takes
+ * the leading channels (largest singular values), the inlier region the rest.
+ * MIX8_4: 8 / 4 bits.  MIX4_3: the paper's own split, 4-bit outliers and
+ * 3-bit inliers.  INT4: a single 4-bit region. */
+static int hi_bits(int qmode) { return qmode == ORC_Q_MIX8_4 ? 8 : 4; }
+static int lo_bits(int qmode) { return qmode == ORC_Q_MIX4_3 ? 3 : 4; }
+
 int orc_outlier_channels(int qmode, int r) {
-  if (qmode != ORC_Q_MIX8_4) return 0;
-  return 8 * ((r + 31) / 32);                  /* 25 % of r, rounded up to 8 */
+  if (qmode == ORC_Q_MIX8_4) return 8 * ((r + 31) / 32);   /* 25 % of r, rounded up to 8 */
+  if (qmode == ORC_Q_MIX4_3) {
+    /* 20 % of r to the nearest multiple of 8 (halves up), at least 8 */
+    int ro = 8 * ((r + 20) / 40);
+    if (ro < 8) ro = 8;
+    return ro < r ? ro : r;
+  }
+  return 0;
 }
 
 int orc_n_groups(int qmode, int r) {
@@ -95,8 +108,8 @@ int orc_n_groups(int qmode, int r) {
 int orc_channel_group(int qmode, int r, int c, int* bits) {
   if (qmode == ORC_Q_F16) { *bits = 16; return -1; }
   int ro = orc_outlier_channels(qmode, r);
-  if (c < ro) { *bits = 8; return c / GROUP; }
-  *bits = 4;
+  if (c < ro) { *bits = hi_bits(qmode); return c / GROUP; }
+  *bits = lo_bits(qmode);
   return (ro + GROUP - 1) / GROUP + (c - ro) / GROUP;
 }
 
@@ -149,7 +162,7 @@ static int64_t align256(int64_t x) { return (x + 255) / 256 * 256; }
 static int row_bytes(int qmode, int r) {
   if (qmode == ORC_Q_F16) return 2 * r;
   int ro = orc_outlier_channels(qmode, r);
-  return ro + (r - ro) / 2;
+  return ro * hi_bits(qmode) / 8 + (r - ro) * lo_bits(qmode) / 8;
 }
 
 int64_t orc_plane_offset(const orc_cfg* cfg, int which, int head) {
@@ -171,21 +184,32 @@ int64_t orc_plane_offset(const orc_cfg* cfg, int which, int head) {
 
 int64_t orc_cache_bytes(const orc_cfg* cfg) { return orc_plane_offset(cfg, 4, 0); }
 
-/* Key code of channel c of head g at token t: returns the byte offset and, for
- * 4-bit codes, which nibble (0 = low).  Within a 16-token block the channels are
- * taken in chunks of 8; each chunk stores its 16 tokens contiguously. */
-static int64_t key_code_at(const orc_cfg* cfg, int g, int b, int t, int c, int* nib) {
+/* Key code of channel c of head g at token t.  Returns the byte offset of the
+ * code's container and, in *bit, the code's first bit in it (containers: one
+ * byte for 8-bit and 4-bit codes, two for fp16, three for 3-bit codes read as
+ * a little-endian 24-bit word).  Within a 16-token block the channels are
+ * taken in chunks of 8, outlier chunks first; each chunk stores its 16 tokens
+ * contiguously, a token's 8 codes in b bytes (b = bits per code):
+ *   8-bit: channel w in byte w;  4-bit: channel w in byte w/2, low nibble for
+ *   even w;  3-bit: channel w at bits 3w..3w+2 of the token's 24-bit word. */
+static int64_t key_code_at(const orc_cfg* cfg, int g, int b, int t, int c, int* bit) {
   int r = cfg->key_rank[g];
   int rb = row_bytes(cfg->qmode, r);
   int64_t base = orc_plane_offset(cfg, 0, g) +
                  ((int64_t)b * (pad_cap(cfg) / 16) + t / 16) * 16 * rb;
   int tau = t % 16, chunk = c / 8, w = c % 8;
-  *nib = 0;
+  *bit = 0;
   if (cfg->qmode == ORC_Q_F16) return base + chunk * 256 + tau * 16 + w * 2;
-  int n8 = orc_outlier_channels(cfg->qmode, r) / 8;
-  if (chunk < n8) return base + chunk * 128 + tau * 8 + w;
-  *nib = w % 2;
-  return base + n8 * 128 + (chunk - n8) * 64 + tau * 4 + w / 2;
+  int hb = hi_bits(cfg->qmode), lb = lo_bits(cfg->qmode);
+  int nhi = orc_outlier_channels(cfg->qmode, r) / 8;
+  int bits = chunk < nhi ? hb : lb;
+  int64_t cbase = chunk < nhi ? base + chunk * 16 * hb
+                              : base + nhi * 16 * hb + (chunk - nhi) * 16 * lb;
+  int64_t tok = cbase + tau * bits;            /* the token's 8 codes take `bits` bytes */
+  if (bits == 8) return tok + w;
+  if (bits == 4) { *bit = 4 * (w % 2); return tok + w / 2; }
+  *bit = 3 * w;                                /* 3-bit: the token's 24-bit word */
+  return tok;
 }
 
 /* Key meta: per 16-token block and group, 16 (s, z) fp16 pairs, one per token.
@@ -207,21 +231,30 @@ static void value_slot(int t, int* kq, int* slot) {
   *slot = 4 * sub + rem % 4;
 }
 
-static int64_t value_code_at(const orc_cfg* cfg, int b, int t, int c, int* nib) {
+/* Within a precision region the order is [channel][chunk][slots]; a
+ * (channel, chunk) holds its 8 slots in 16 bytes (fp16), 8 bytes (8-bit: slot
+ * in byte), 4 bytes (4-bit: slot 2k in nibble k, slot 2k+1 in nibble k+4 of
+ * the little-endian 32-bit word) or 3 bytes (3-bit: slot 2k at bits 3k..3k+2,
+ * slot 2k+1 at bits 12+3k..14+3k of the little-endian 24-bit word). */
+static int64_t value_code_at(const orc_cfg* cfg, int b, int t, int c, int* bit) {
   int r = cfg->value_rank;
   int rb = row_bytes(cfg->qmode, r);
   int64_t base = orc_plane_offset(cfg, 2, 0) +
                  ((int64_t)b * (pad_cap(cfg) / 32) + t / 32) * 32 * rb;
   int kq, slot;
   value_slot(t, &kq, &slot);
-  *nib = 0;
+  *bit = 0;
   if (cfg->qmode == ORC_Q_F16) return base + ((int64_t)c * 4 + kq) * 16 + slot * 2;
   int ro = orc_outlier_channels(cfg->qmode, r);
-  if (c < ro) return base + ((int64_t)c * 4 + kq) * 8 + slot;
-  /* in a 4-bit chunk word, slot 2k sits in nibble k and slot 2k+1 in nibble k+4 */
-  int p = (slot % 2 == 0) ? slot / 2 : slot / 2 + 4;
-  *nib = p % 2;
-  return base + 32 * ro + ((int64_t)(c - ro) * 4 + kq) * 4 + p / 2;
+  int hb = hi_bits(cfg->qmode), lb = lo_bits(cfg->qmode);
+  int bits = c < ro ? hb : lb;
+  int64_t word = c < ro ? base + ((int64_t)c * 4 + kq) * hb
+                        : base + 4 * (int64_t)ro * hb + ((int64_t)(c - ro) * 4 + kq) * lb;
+  if (bits == 8) return word + slot;
+  int pos = (slot % 2 == 0) ? slot / 2 : slot / 2 + 4;   /* nibble / 3-bit field index */
+  if (bits == 4) { *bit = 4 * (pos % 2); return word + pos / 2; }
+  *bit = (slot % 2 == 0) ? 3 * (slot / 2) : 12 + 3 * (slot / 2);
+  return word;
 }
 
 /* Value meta: per 32-token block, group and chunk, the 8 scales of the chunk's
@@ -239,18 +272,24 @@ static int64_t value_meta_at(const orc_cfg* cfg, int b, int t, int gi, int64_t* 
 static void put16(uint8_t* p, uint16_t v) { p[0] = (uint8_t)(v & 255); p[1] = (uint8_t)(v >> 8); }
 static uint16_t get16(const uint8_t* p) { return (uint16_t)(p[0] | (p[1] << 8)); }
 
-static void put_code(uint8_t* cache, int64_t off, int nib, int bits, uint16_t v) {
+static void put_code(uint8_t* cache, int64_t off, int bit, int bits, uint16_t v) {
   if (bits == 16) { put16(cache + off, v); return; }
   if (bits == 8) { cache[off] = (uint8_t)v; return; }
-  uint8_t old = cache[off];
-  if (nib) cache[off] = (uint8_t)((old & 0x0F) | ((v & 15) << 4));
-  else     cache[off] = (uint8_t)((old & 0xF0) | (v & 15));
+  int nbytes = bits == 3 ? 3 : 1;              /* the container */
+  uint32_t word = 0;
+  for (int i = 0; i < nbytes; ++i) word |= (uint32_t)cache[off + i] << (8 * i);
+  uint32_t mask = ((1u << bits) - 1) << bit;
+  word = (word & ~mask) | (((uint32_t)v << bit) & mask);
+  for (int i = 0; i < nbytes; ++i) cache[off + i] = (uint8_t)(word >> (8 * i));
 }
 
-static uint16_t get_code(const uint8_t* cache, int64_t off, int nib, int bits) {
+static uint16_t get_code(const uint8_t* cache, int64_t off, int bit, int bits) {
   if (bits == 16) return get16(cache + off);
   if (bits == 8) return cache[off];
-  return nib ? (cache[off] >> 4) : (cache[off] & 15);
+  int nbytes = bits == 3 ? 3 : 1;
+  uint32_t word = 0;
+  for (int i = 0; i < nbytes; ++i) word |= (uint32_t)cache[off + i] << (8 * i);
+  return (uint16_t)((word >> bit) & ((1u << bits) - 1));
 }
 
 static int sum_key_rank(const orc_cfg* cfg) {
@@ -268,10 +307,10 @@ static void store_block(const orc_cfg* cfg, uint8_t* cache, int g, int b, int t,
   int ng = 0;
   if (cfg->qmode != ORC_Q_F16) ng = orc_quantize_block(cfg->qmode, r, x, codes, s, z);
   for (int c = 0; c < r; ++c) {
-    int bits, nib;
+    int bits, bit;
     orc_channel_group(cfg->qmode, r, c, &bits);
-    int64_t off = g >= 0 ? key_code_at(cfg, g, b, t, c, &nib) : value_code_at(cfg, b, t, c, &nib);
-    put_code(cache, off, nib, bits, bits == 16 ? x[c] : codes[c]);
+    int64_t off = g >= 0 ? key_code_at(cfg, g, b, t, c, &bit) : value_code_at(cfg, b, t, c, &bit);
+    put_code(cache, off, bit, bits, bits == 16 ? x[c] : codes[c]);
   }
   for (int gi = 0; gi < ng; ++gi) {
     int64_t zoff;
@@ -361,10 +400,10 @@ static void load_block(const orc_cfg* cfg, const uint8_t* cache, int g, int b, i
                        double* out) {
   int r = g >= 0 ? cfg->key_rank[g] : cfg->value_rank;
   for (int c = 0; c < r; ++c) {
-    int bits, nib;
+    int bits, bit;
     int gi = orc_channel_group(cfg->qmode, r, c, &bits);
-    int64_t off = g >= 0 ? key_code_at(cfg, g, b, t, c, &nib) : value_code_at(cfg, b, t, c, &nib);
-    uint16_t code = get_code(cache, off, nib, bits);
+    int64_t off = g >= 0 ? key_code_at(cfg, g, b, t, c, &bit) : value_code_at(cfg, b, t, c, &bit);
+    uint16_t code = get_code(cache, off, bit, bits);
     if (bits == 16) { out[c] = orc_f16_to_double(code); continue; }
     int64_t zoff;
     int64_t soff = g >= 0 ? key_meta_at(cfg, g, b, t, gi, &zoff) : value_meta_at(cfg, b, t, gi, &zoff);

@@ -8,8 +8,9 @@
  *
  * What it computes (paper sections cited per function in oracle.c):
  *   - down-projection of hidden states into latents (Sec. 3.2),
- *   - per-token group quantization of the latents into an outlier (int8)
- *     and an inlier (int4) region (Sec. 4.4, Eq. for Z-hat),
+ *   - per-token group quantization of the latents into an outlier and an
+ *     inlier region (Sec. 4.4, Eq. for Z-hat): 8/4 bits, or the paper's own
+ *     4/3 bits with about 20 % outliers (Sec. 5, quantization results),
  *   - the cache byte layout (this library's format, documented in the
  *     public header of the product library; re-derived here independently),
  *   - decode attention read from that cache: dequantize, reconstruct keys
@@ -27,7 +28,7 @@
 extern "C" {
 #endif
 
-enum { ORC_Q_F16 = 0, ORC_Q_INT4 = 1, ORC_Q_MIX8_4 = 2 };
+enum { ORC_Q_F16 = 0, ORC_Q_INT4 = 1, ORC_Q_MIX8_4 = 2, ORC_Q_MIX4_3 = 3 };
 
 typedef struct {
   int32_t batch, n_q_heads, n_kv_heads, head_dim, capacity;
@@ -45,8 +46,8 @@ uint16_t orc_f16_ceil(double q);               /* smallest fp16 >= q, q >= 0 */
 double   orc_bf16_to_double(uint16_t b);
 
 /* ---- quantizer: one latent block of rank r for one token ----
- * x: r fp16 values.  codes: r entries (0..15 / 0..255; raw fp16 bits for F16
- * are not produced here).  s, z: one fp16 pair per group, int8 groups first.
+ * x: r fp16 values.  codes: r entries (0 .. 2^bits - 1; raw fp16 bits for F16
+ * are not produced here).  s, z: one fp16 pair per group, outlier groups first.
  * Returns the number of groups. */
 int orc_n_groups(int qmode, int r);
 int orc_outlier_channels(int qmode, int r);

@@ -16,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(HERE, "liborc_starkv.so")
 _lib = None
 
-Q_F16, Q_INT4, Q_MIX8_4 = 0, 1, 2
+Q_F16, Q_INT4, Q_MIX8_4, Q_MIX4_3 = 0, 1, 2, 3
 
 
 class OrcCfg(C.Structure):

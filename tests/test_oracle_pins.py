@@ -75,8 +75,14 @@ def _frac16(h):
 def _rational_quantize(qmode, xs_bits):
     """The quantizer written out in exact rationals, from its definition."""
     r = len(xs_bits)
-    ro = 8 * ((r + 31) // 32) if qmode == O.Q_MIX8_4 else 0
-    regions = ([(0, ro, 8)] if ro else []) + [(ro, r, 4)]
+    if qmode == O.Q_MIX8_4:
+        ro, hb, lb = 8 * ((r + 31) // 32), 8, 4          # a quarter, rounded up to 8
+    elif qmode == O.Q_MIX4_3:
+        # a fifth of the channels to the nearest multiple of 8 (halves up), at least 8
+        ro = min(r, max(8, 8 * int(Fraction(r, 40) + Fraction(1, 2)))) ; hb, lb = 4, 3
+    else:
+        ro, hb, lb = 0, 4, 4
+    regions = ([(0, ro, hb)] if ro else []) + [(ro, r, lb)]
     codes = [0] * r
     s_out, z_out = [], []
     for (a, b, bits) in regions:
@@ -107,7 +113,9 @@ def _rational_quantize(qmode, xs_bits):
 
 @pytest.mark.parametrize("qmode,r", [(O.Q_INT4, 16), (O.Q_INT4, 48), (O.Q_INT4, 96),
                                      (O.Q_MIX8_4, 16), (O.Q_MIX8_4, 32), (O.Q_MIX8_4, 48),
-                                     (O.Q_MIX8_4, 128), (O.Q_MIX8_4, 256)])
+                                     (O.Q_MIX8_4, 128), (O.Q_MIX8_4, 256),
+                                     (O.Q_MIX4_3, 16), (O.Q_MIX4_3, 48), (O.Q_MIX4_3, 80),
+                                     (O.Q_MIX4_3, 128), (O.Q_MIX4_3, 384)])
 def test_quantizer_matches_exact_rational_definition(qmode, r):
     rng = np.random.default_rng(r + 100 * qmode)
     for trial in range(6):
@@ -122,7 +130,8 @@ def test_quantizer_matches_exact_rational_definition(qmode, r):
         assert list(z) == rz
 
 
-@pytest.mark.parametrize("qmode,r", [(O.Q_INT4, 64), (O.Q_MIX8_4, 64), (O.Q_MIX8_4, 256)])
+@pytest.mark.parametrize("qmode,r", [(O.Q_INT4, 64), (O.Q_MIX8_4, 64), (O.Q_MIX8_4, 256),
+                                     (O.Q_MIX4_3, 64), (O.Q_MIX4_3, 256)])
 def test_quantizer_round_trip_within_half_step(qmode, r):
     rng = np.random.default_rng(7)
     for _ in range(50):
@@ -136,6 +145,8 @@ def test_quantizer_round_trip_within_half_step(qmode, r):
             assert abs(x - (zv + codes[c] * sv)) <= sv / 2
             if qmode == O.Q_MIX8_4:
                 assert bits == (8 if c < O.outlier_channels(qmode, r) else 4)
+            if qmode == O.Q_MIX4_3:
+                assert bits == (4 if c < O.outlier_channels(qmode, r) else 3)
 
 
 def test_outlier_region_is_a_quarter_rounded_up_to_8():
@@ -143,6 +154,19 @@ def test_outlier_region_is_a_quarter_rounded_up_to_8():
         assert O.outlier_channels(O.Q_MIX8_4, r) == ro
         assert O.n_groups(O.Q_MIX8_4, r) == -(-ro // 32) + -(-(r - ro) // 32)
     assert O.outlier_channels(O.Q_INT4, 64) == 0
+
+
+def test_paper_split_keeps_a_fifth_in_4_bits_and_averages_3_2_bits():
+    # Sec. 5 (quantization results): the first 20 % of the latent channels in 4 bits, the rest
+    # in 3 bits, 3.2 bits on average.  Where r/5 is a multiple of 8 the split is exact.
+    for r in (40 * 2, 40 * 4, 40 * 8):
+        ro = O.outlier_channels(O.Q_MIX4_3, r)
+        assert ro * 5 == r
+        bits = [O.channel_group(O.Q_MIX4_3, r, c)[1] for c in range(r)]
+        assert Fraction(sum(bits), r) == Fraction(16, 5)
+    # other ranks: the nearest multiple of 8 (at least 8, never past r)
+    for r, ro in [(16, 8), (32, 8), (48, 8), (64, 16), (96, 16), (128, 24), (256, 48), (384, 80)]:
+        assert O.outlier_channels(O.Q_MIX4_3, r) == ro
 
 
 # ---------------------------------------------------------------- layout / golden bytes
@@ -156,6 +180,9 @@ def _latents_for(ex):
     rk, rv = ex["cfg"]["key_rank"][0], ex["cfg"]["value_rank"]
     out = {}
     for tok in ex["tokens"]:
+        if isinstance(tok["key"], list):        # values listed in the example itself
+            out[tok["t"]] = O.f16_bits(np.array(tok["key"] + tok["value"], dtype=np.float64))
+            continue
         c = np.arange(rk, dtype=np.float64)
         cv = np.arange(rv, dtype=np.float64)
         if ex["name"] == "int4_r16":
@@ -168,7 +195,7 @@ def _latents_for(ex):
     return out
 
 
-@pytest.mark.parametrize("idx", [0, 1])
+@pytest.mark.parametrize("idx", [0, 1, 2])
 def test_packed_bytes_match_hand_derived_golden(idx):
     ex = json.load(open(os.path.join(HERE, "golden", "pack_examples.json")))["examples"][idx]
     cfg = _cfg_from(ex["cfg"])
@@ -277,7 +304,7 @@ def _deq_all(cfg, cache, B, L):
     return np.stack(ks), np.stack(vs)
 
 
-@pytest.mark.parametrize("qmode", [O.Q_F16, O.Q_INT4, O.Q_MIX8_4])
+@pytest.mark.parametrize("qmode", [O.Q_F16, O.Q_INT4, O.Q_MIX8_4, O.Q_MIX4_3])
 def test_full_rank_equals_dense_attention_gqa(qmode):
     """Keys K = K' U_K^T per head and values V = V' U_V^T (one shared latent) fed to plain
     dense attention give the oracle's output (Sec. 3.2 + Sec. 3.3), for every query head
@@ -320,7 +347,7 @@ def test_identity_up_projection_reproduces_stored_latents():
     np.testing.assert_allclose(out[0, 1], mean_v, rtol=1e-13)
 
 
-@pytest.mark.parametrize("qmode", [O.Q_INT4, O.Q_MIX8_4])
+@pytest.mark.parametrize("qmode", [O.Q_INT4, O.Q_MIX8_4, O.Q_MIX4_3])
 def test_single_token_and_zero_query_closed_forms(qmode):
     rng = np.random.default_rng(13)
     B, Hq, Hkv, d, L = 1, 4, 2, 16, 11
@@ -347,6 +374,7 @@ def test_brute_force_tiny_shapes():
     rng = np.random.default_rng(14)
     for (qmode, d, Hq, Hkv, ranks, rv, L) in [(O.Q_INT4, 4, 2, 1, [16], 16, 5),
                                               (O.Q_MIX8_4, 8, 4, 2, [16, 32], 16, 3),
+                                              (O.Q_MIX4_3, 8, 2, 1, [48], 48, 3),
                                               (O.Q_F16, 8, 2, 2, [16, 16], 32, 4)]:
         cfg, cache, lat = _build(qmode, 1, Hq, Hkv, d, L, ranks, rv, rng)
         Bk = O.f16_bits(rng.standard_normal((sum(ranks), d)))
