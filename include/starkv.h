@@ -59,8 +59,15 @@ typedef enum {
  *   INT4    every channel 4-bit;
  *   MIX8_4  the leading r_out = 8*ceil(r/32) channels (about 25 %, the outlier
  *           block; the latent channels are ordered by singular value) at 8 bits,
- *           the remaining channels (inlier block) at 4 bits. */
-typedef enum { STARKV_Q_F16 = 0, STARKV_Q_INT4 = 1, STARKV_Q_MIX8_4 = 2 } starkv_qmode;
+ *           the remaining channels (inlier block) at 4 bits;
+ *   MIX4_3  the paper's own split (Sec. 5, quantization results): the leading
+ *           r_out = 8*max(1, floor((r + 20)/40)) channels (a fifth of r to the
+ *           nearest multiple of 8, at least 8, at most r) at 4 bits, the rest at
+ *           3 bits -- 3.2 bits per channel on average when r/5 is a multiple of 8.
+ *           The block Hadamard rotations of Sec. 4.4 are fused into the
+ *           caller's down- and up-projection factors. */
+typedef enum { STARKV_Q_F16 = 0, STARKV_Q_INT4 = 1, STARKV_Q_MIX8_4 = 2,
+               STARKV_Q_MIX4_3 = 3 } starkv_qmode;
 
 /* Element types.  F32 is accepted for the attention output only. */
 typedef enum { STARKV_DT_F16 = 0, STARKV_DT_BF16 = 1, STARKV_DT_F32 = 2 } starkv_dtype;
@@ -97,20 +104,24 @@ typedef struct starkv_plan starkv_plan;   /* opaque, immutable after creation */
  *
  * A latent block of rank r (key head g: r = r_g; values: r = r_v) has regions:
  * F16: one region, 16-bit values.  INT4: one 4-bit region.  MIX8_4: 8-bit
- * channels [0, r_out), 4-bit channels [r_out, r).  Each quantized region is split
- * into groups of 32 channels from the region start (the last may be shorter);
- * groups are numbered 8-bit first.  Per token and group: z = min over the
+ * channels [0, r_out), 4-bit channels [r_out, r).  MIX4_3: 4-bit channels
+ * [0, r_out), 3-bit channels [r_out, r).  Each quantized region is split into
+ * groups of 32 channels from the region start (the last may be shorter); groups
+ * are numbered outlier region first.  Per token and group: z = min over the
  * group's fp16 values, s = the smallest fp16 >= (max - min)/(2^b - 1) (s = 0 when
  * max == min), code = round-half-even((x - z)/s) clamped to [0, 2^b - 1]
  * (evaluated in fp64, which is exact for these operands); decode x-hat = z + code*s.
- * Row bytes: F16 2r; INT4 r/2; MIX8_4 r_out + (r - r_out)/2.
+ * Row bytes: F16 2r; INT4 r/2; MIX8_4 r_out + (r - r_out)/2; MIX4_3
+ * r_out/2 + 3(r - r_out)/8.
  *
  * Keys, head g, sequence b, token t: 16-token block k = t/16, tau = t%16, at
  *   plane + (b*Cp/16 + k) * 16*row_bytes.  Inside a block the channels go in
  *   chunks of 8 (chunk c = channels 8c..8c+7); chunk c holds its 16 tokens
- *   back to back, chunk_bytes each (16 F16, 8 for 8-bit, 4 for 4-bit chunks),
- *   8-bit chunks first.  Within a chunk: F16 channel w at 2w; 8-bit channel w at
- *   byte w; 4-bit channel w at byte w/2, low nibble for even w.
+ *   back to back, chunk_bytes each (16 F16, 8 for 8-bit, 4 for 4-bit, 3 for
+ *   3-bit chunks), outlier chunks first.  Within a chunk: F16 channel w at 2w;
+ *   8-bit channel w at byte w; 4-bit channel w at byte w/2, low nibble for even
+ *   w; 3-bit channel w at bits 3w..3w+2 of the token's 3 bytes read as a
+ *   little-endian 24-bit word.
  *   Key meta: per 16-token block, per group, 16 (s, z) fp16 pairs (4 B per token).
  * Values, sequence b, token t: 32-token block k = t/32 at
  *   plane + (b*Cp/32 + k) * 32*row_bytes.  A block's tokens form four chunks q of
@@ -118,8 +129,10 @@ typedef struct starkv_plan starkv_plan;   /* opaque, immutable after creation */
  *   holds tokens 4q..4q+3 and 16+4q..16+4q+3).  For each chunk q and channel c the
  *   eight slots are stored together: F16 16 B (slot at 2*slot), 8-bit 8 B (slot at
  *   byte slot), 4-bit one 32-bit word (slot 2k in bits 4k..4k+3, slot 2k+1 in bits
- *   16+4k..16+4k+3, k = 0..3).  The 8-bit region precedes the 4-bit region;
- *   within a region the order is [channel][q][slots].
+ *   16+4k..16+4k+3, k = 0..3), 3-bit 3 bytes read as a little-endian 24-bit word
+ *   (slot 2k in bits 3k..3k+2, slot 2k+1 in bits 12+3k..14+3k).  The outlier
+ *   region precedes the inlier region; within a region the order is
+ *   [channel][q][slots].
  *   Value meta: per 32-token block, per group g, per chunk q: the 8 slots' s
  *   (16 B) then their z (16 B), at ((g*4 + q)*32) inside the block's meta.
  * ---------------------------------------------------------------------------- */

@@ -23,7 +23,7 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 UNITS = [("starkv_host.cpp", []), ("append.hip", []), ("decode.hip", ["-DSK_COMMON"])]
-UNITS += [("decode.hip", [f"-DSK_D={d}", f"-DSK_QM={q}"]) for d in (64, 128) for q in (0, 1, 2)]
+UNITS += [("decode.hip", [f"-DSK_D={d}", f"-DSK_QM={q}"]) for d in (64, 128) for q in (0, 1, 2, 3)]
 
 
 def _obj_name(src: str, defs) -> str:

@@ -4,7 +4,8 @@
 //   x (Sigma V)_V), bf16 operands on v_mfma_f32_16x16x32_bf16, fp32 partial sums
 //   per k-split, then a fixed-order reduction rounded to fp16.
 // pack: per-token group quantization of every latent block into the cache
-//   (Sec. 4.4: outlier block at 8 bits, inlier block at 4 bits).  The scale is
+//   (Sec. 4.4: an outlier block and an inlier block at b_out > b_in bits: 8/4,
+//   4/4, or the paper's 4/3).  The scale is
 //   the smallest fp16 not below (max - min)/(2^b - 1) and the codes round half
 //   to even; both are evaluated in fp64, which is exact for fp16 operands, so
 //   the codes do not depend on evaluation order.
@@ -97,13 +98,16 @@ __global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
   const int bl = p.item_block[item], gi = p.item_group[item];
   const int r = p.rank[bl], ro = p.ro[bl];
   const bool is_v = (bl == p.n_kv);
+  // bits of the outlier (hb) and inlier (lb) regions
+  const int hb = p.qmode == STARKV_Q_MIX8_4 ? 8 : 4;
+  const int lb = p.qmode == STARKV_Q_MIX4_3 ? 3 : 4;
   int c0, n, bits;
   if (p.qmode == STARKV_Q_F16) {
     c0 = 32 * gi; n = min(32, r - c0); bits = 16;
   } else {
-    const int ng8 = (ro + 31) / 32;
-    if (gi < ng8) { c0 = 32 * gi; n = min(32, ro - c0); bits = 8; }
-    else { c0 = ro + 32 * (gi - ng8); n = min(32, r - c0); bits = 4; }
+    const int ngo = (ro + 31) / 32;
+    if (gi < ngo) { c0 = 32 * gi; n = min(32, ro - c0); bits = hb; }
+    else { c0 = ro + 32 * (gi - ngo); n = min(32, r - c0); bits = lb; }
   }
   const bool on = lane < n;
   const int c = c0 + lane;
@@ -171,23 +175,31 @@ __global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
   if (!on) code = 0;
   if (!is_v) {
     uint8_t* kb = code_plane + kblk * 16 * rb;
-    const int n8 = ro / 8;
+    const int nhi = ro / 8;              // outlier chunks (16 tokens x hb bytes each)
+    const int ch = c / 8;
+    uint8_t* chunk = ch < nhi ? kb + ch * 16 * hb : kb + nhi * 16 * hb + (ch - nhi) * 16 * lb;
     if (bits == 8) {          // 4 codes per 32-bit word, lanes 4k..4k+3
       uint32_t wv = code << (8 * (lane & 3));
       wv |= __shfl_xor(wv, 1);
       wv |= __shfl_xor(wv, 2);
-      if (on && (lane & 3) == 0) {
-        const int ch = c / 8;
-        *reinterpret_cast<uint32_t*>(kb + ch * 128 + tau * 8 + (c % 8)) = wv;
-      }
-    } else {                  // 8 codes per word, lanes 8k..8k+7, channel w at nibble w
-      uint32_t wv = code << (4 * (lane & 7));
+      if (on && (lane & 3) == 0)
+        *reinterpret_cast<uint32_t*>(chunk + tau * 8 + (c % 8)) = wv;
+    } else {                  // a token's 8 codes of a chunk, lanes 8k..8k+7: channel
+      // w at bits bits*w (4-bit: one 32-bit word; 3-bit: 3 bytes, stored bytewise
+      // since neighbouring tokens share 32-bit words)
+      uint32_t wv = code << (bits * (lane & 7));
       wv |= __shfl_xor(wv, 1);
       wv |= __shfl_xor(wv, 2);
       wv |= __shfl_xor(wv, 4);
       if (on && (lane & 7) == 0) {
-        const int ch = c / 8;
-        *reinterpret_cast<uint32_t*>(kb + n8 * 128 + (ch - n8) * 64 + tau * 4) = wv;
+        if (bits == 4) {
+          *reinterpret_cast<uint32_t*>(chunk + tau * 4) = wv;
+        } else {
+          uint8_t* d = chunk + tau * 3;
+          d[0] = (uint8_t)wv;
+          d[1] = (uint8_t)(wv >> 8);
+          d[2] = (uint8_t)(wv >> 16);
+        }
       }
     }
     if (lane == 0) {
@@ -198,14 +210,29 @@ __global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
   } else {
     uint8_t* vb = code_plane + vblk * 32 * rb;
     if (on) {
+      // (channel, chunk) words: the outlier region (4*ro*hb bytes) first
+      const bool hi = c < ro;
+      const int64_t word = hi ? ((int64_t)c * 4 + kq) * hb
+                              : 4LL * ro * hb + ((int64_t)(c - ro) * 4 + kq) * lb;
       if (bits == 8) {
-        vb[((int64_t)c * 4 + kq) * 8 + slot] = (uint8_t)code;
+        vb[word + slot] = (uint8_t)code;
       } else {
-        // slot 2k -> bits 4k..4k+3, slot 2k+1 -> bits 16+4k..16+4k+3
-        const int sh = (slot % 2 == 0) ? 4 * (slot / 2) : 16 + 4 * (slot / 2);
-        unsigned int* wp = reinterpret_cast<unsigned int*>(vb + 32 * ro + ((int64_t)(c - ro) * 4 + kq) * 4);
-        atomicAnd(wp, ~(0xFu << sh));
-        atomicOr(wp, code << sh);
+        // 4-bit: slot 2k -> bits 4k.., slot 2k+1 -> bits 16+4k.. of the 32-bit word;
+        // 3-bit: slot 2k -> bits 3k.., slot 2k+1 -> bits 12+3k.. of the 24-bit word.
+        // Tokens of one launch own disjoint fields, updated with atomic AND/OR on
+        // the aligned 32-bit word(s) holding them (a 3-bit field may straddle two).
+        const int sh = bits == 4 ? ((slot % 2 == 0) ? 4 * (slot / 2) : 16 + 4 * (slot / 2))
+                                 : ((slot % 2 == 0) ? 3 * (slot / 2) : 12 + 3 * (slot / 2));
+        const uint64_t abit = (uint64_t)((vb + word) - p.cache) * 8 + sh;   // bit address
+        unsigned int* wp = reinterpret_cast<unsigned int*>(p.cache) + abit / 32;
+        const int s0 = (int)(abit % 32);
+        const uint32_t fmask = (1u << bits) - 1;
+        atomicAnd(wp, ~(fmask << s0));
+        atomicOr(wp, code << s0);
+        if (s0 + bits > 32) {                // the field's high bits in the next word
+          atomicAnd(wp + 1, ~(fmask >> (32 - s0)));
+          atomicOr(wp + 1, code >> (32 - s0));
+        }
       }
     }
     if (lane == 0) {

@@ -190,6 +190,28 @@ __device__ __forceinline__ u4 deq_int8p(u2 d, h2 s0, h2 z0, h2 s1, h2 z1, h2 s2,
   return r;
 }
 
+// 3-bit codes: the low 24 bits of x hold fields 0..7 (3 bits each).  Fields k
+// and k+4 are moved side by side into the two halves of a word and placed in
+// the low mantissa bits of fp16 1024 (see deq_pair): pairs (0,4), (1,5), (2,6),
+// (3,7).
+__device__ __forceinline__ u4 magic_int3(uint32_t x) {
+  const uint32_t w2 = (x & 0xFFFu) | ((x << 4) & 0x0FFF0000u);
+  u4 m;
+  m.x = (w2 & 0x00070007u) | 0x64006400u;
+  m.y = ((w2 >> 3) & 0x00070007u) | 0x64006400u;
+  m.z = ((w2 >> 6) & 0x00070007u) | 0x64006400u;
+  m.w = ((w2 >> 9) & 0x00070007u) | 0x64006400u;
+  return m;
+}
+
+// Three bytes at LDS byte offset off (any alignment) from two aligned 32-bit
+// reads: the code word of a 3-bit lane (and, at a 4-byte aligned offset, the
+// whole 32-bit word).
+__device__ __forceinline__ uint32_t lds_word_at(const uint8_t* base, int off) {
+  const uint32_t* w = reinterpret_cast<const uint32_t*>(base + (off & ~3));
+  return __builtin_amdgcn_alignbyte(w[1], w[0], (uint32_t)(off & 3));
+}
+
 // Packed fp16 cos/sin of one lane's four RoPE frequencies j0 + e (j0 = 16 kq +
 // 4 quad) at one token offset: c01 = (cos j0, cos j0+1), c23, s01, s23.
 struct CS4 {
@@ -242,10 +264,21 @@ __device__ __forceinline__ void key_head(const HeadRt& kh, const uint8_t* raw, c
       const int off = valid ? kb * 1024 + lane * 16 : 0;
 #pragma unroll
       for (int s = 0; s < 2; ++s) cf[s][kb] = *reinterpret_cast<const u4*>(rc + s * rb16 + off);
+    } else if (QM == STARKV_Q_MIX4_3) {
+      // outlier chunks (4-bit, 64 B per 16 tokens) first, then 3-bit chunks (48 B)
+      is8[kb] = c < kh.n8;
+      int off = is8[kb] ? kb * 256 + lane * 4 : kh.n8 * 64 + (c - kh.n8) * 48 + col * 3;
+      int gi = is8[kb] ? c / 4 : kh.ng8 + (c - kh.n8) / 4;
+      if (!valid) { off = 0; gi = 0; }
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        meta[s][kb] = *reinterpret_cast<const uint32_t*>(rm + (s * kh.ngroups + gi) * 64 + col * 4);
+        code[s][kb].x = lds_word_at(rc + s * rb16, off);
+      }
     } else {
       is8[kb] = QM == STARKV_Q_MIX8_4 && c < kh.n8;
       int off = is8[kb] ? kb * 512 + lane * 8 : kh.n8 * 64 + kb * 256 + lane * 4;
-      int gi = is8[kb] ? 0 : kh.ng8 + (c - kh.n8) / 4;
+      int gi = is8[kb] ? c / 4 : kh.ng8 + (c - kh.n8) / 4;
       if (!valid) { off = 0; gi = 0; }
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
@@ -275,13 +308,26 @@ __device__ __forceinline__ void key_head(const HeadRt& kh, const uint8_t* raw, c
         const h2 zv = as_h2(perm(mz, mz, 0x03020302u));
         u2 d = code[s][kb];
         const u2 nb = nibble_bytes(d.x);
-        if (QM == STARKV_Q_INT4) {
-          d = nb;
+        if (QM == STARKV_Q_MIX4_3) {
+          // 4-bit lanes: nibble bytes; 3-bit lanes: field pairs (element orders
+          // 0,2,4,6,1,3,5,7 and 0,4,1,5,2,6,3,7; the fragments match)
+          const u4 m3 = magic_int3(d.x);
+          u4 m;
+          m.x = is8[kb] ? perm(0x64646464u, nb.x, 0x05010400u) : m3.x;
+          m.y = is8[kb] ? perm(0x64646464u, nb.x, 0x05030402u) : m3.y;
+          m.z = is8[kb] ? perm(0x64646464u, nb.y, 0x05010400u) : m3.z;
+          m.w = is8[kb] ? perm(0x64646464u, nb.y, 0x05030402u) : m3.w;
+          v = (u4){deq_pair(m.x, sv, zv), deq_pair(m.y, sv, zv), deq_pair(m.z, sv, zv),
+                   deq_pair(m.w, sv, zv)};
         } else {
-          d.x = is8[kb] ? d.x : nb.x;
-          d.y = is8[kb] ? d.y : nb.y;
+          if (QM == STARKV_Q_INT4) {
+            d = nb;
+          } else {
+            d.x = is8[kb] ? d.x : nb.x;
+            d.y = is8[kb] ? d.y : nb.y;
+          }
+          v = deq_int8p(d, sv, zv, sv, zv, sv, zv, sv, zv);
         }
-        v = deq_int8p(d, sv, zv, sv, zv, sv, zv, sv, zv);
       }
       xop[s][kb] = __builtin_bit_cast(h8, v);
     }
@@ -535,12 +581,16 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       const int fl = f - fb;
       const int mt = fl / nkb, kb = fl % nkb;
       const int c = 4 * kb + kq;
-      const bool four = QM != STARKV_Q_F16 && c >= n8;
+      // element order of the chunk's key operand: 8-bit and fp16 in order,
+      // 4-bit 0,2,4,6,1,3,5,7, 3-bit 0,4,1,5,2,6,3,7
+      const int ord = QM == STARKV_Q_F16 ? 0
+                      : QM == STARKV_Q_MIX4_3 ? (c < n8 ? 1 : 2) : (c < n8 ? 0 : 1);
       const uint16_t* src = p.bk + (int64_t)bk_row * D + 16 * mt + jj;
       live[k] = 0;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const int wi = four ? (e < 4 ? 2 * e : 2 * (e - 4) + 1) : e;
+        const int wi = ord == 0 ? e : ord == 1 ? (e < 4 ? 2 * e : 2 * (e - 4) + 1)
+                                               : (e % 2 == 0 ? e / 2 : 4 + e / 2);
         const int row = 8 * c + wi;
         live[k] |= row < rank ? 1u << e : 0u;
         ld[k][e] = src[(int64_t)min(row, rank - 1) * D];
@@ -661,8 +711,10 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     // not stored), so the step loop needs no per-tile branch
     const int nt = min(w * NTW + t, NT - 1);
     const int rho = 16 * nt + col;
-    const bool is8 = rho < p.v_ro;
+    const bool is8 = rho < p.v_ro;   // outlier region (8-bit, or 4-bit for MIX4_3)
     if (QM == STARKV_Q_F16) v_off[t] = (rho * 4 + quad) * 16;
+    else if (QM == STARKV_Q_MIX4_3)
+      v_off[t] = is8 ? (rho * 4 + quad) * 4 : 16 * p.v_ro + ((rho - p.v_ro) * 4 + quad) * 3;
     else if (is8) v_off[t] = (rho * 4 + quad) * 8;
     else v_off[t] = 32 * p.v_ro + ((rho - p.v_ro) * 4 + quad) * 4;
     v_gi[t] = is8 ? rho / 32 : p.v_ng8 + (rho - p.v_ro) / 32;
@@ -676,8 +728,9 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     bool any8 = false, any4 = false;
     for (int t = 0; t < NTW; ++t) {
       const int nt = min(w * NTW + t, NT - 1);   // the tile the step loop reads
-      any8 |= QM == STARKV_Q_MIX8_4 && 16 * nt < p.v_ro;
-      any4 |= QM != STARKV_Q_MIX8_4 || 16 * nt + 16 > p.v_ro;
+      const bool mix = QM == STARKV_Q_MIX8_4 || QM == STARKV_Q_MIX4_3;
+      any8 |= mix && 16 * nt < p.v_ro;
+      any4 |= !mix || 16 * nt + 16 > p.v_ro;
     }
     vmode = any8 && any4 ? kValuesMixed : any8 ? kValues8 : kValues4;
   }
@@ -910,7 +963,21 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
             const uint8_t* mb = vmeta + ((ww * p.v_ng + v_gi[t]) * 4 + quad) * 32;
             const u4 sv = *reinterpret_cast<const u4*>(mb);
             const u4 zv = *reinterpret_cast<const u4*>(mb + 16);
-            if (VM == kValues8) {
+            if (QM == STARKV_Q_MIX4_3) {
+              // outlier tiles: one 4-bit word per lane; inlier tiles: 3 bytes
+              // (slot pairs 2k, 2k+1 at fields k, k+4 of the 24-bit word)
+              const uint32_t d = VM == kValues8 ? *reinterpret_cast<const uint32_t*>(vb + v_off[t])
+                                                : lds_word_at(vb, v_off[t]);
+              const u4 v4 = deq_int4m(d, nib_mask, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y),
+                                      as_h2(zv.y), as_h2(sv.z), as_h2(zv.z), as_h2(sv.w),
+                                      as_h2(zv.w));
+              const u4 m3 = magic_int3(d);
+              const u4 v3 = (u4){deq_pair(m3.x, as_h2(sv.x), as_h2(zv.x)),
+                                 deq_pair(m3.y, as_h2(sv.y), as_h2(zv.y)),
+                                 deq_pair(m3.z, as_h2(sv.z), as_h2(zv.z)),
+                                 deq_pair(m3.w, as_h2(sv.w), as_h2(zv.w))};
+              v = VM == kValues8 ? v4 : VM == kValues4 ? v3 : (v_is8[t] ? v4 : v3);
+            } else if (VM == kValues8) {
               const u2 d = *reinterpret_cast<const u2*>(vb + v_off[t]);
               v = deq_int8p(d, as_h2(sv.x), as_h2(zv.x), as_h2(sv.y), as_h2(zv.y), as_h2(sv.z),
                             as_h2(zv.z), as_h2(sv.w), as_h2(zv.w));
@@ -1025,23 +1092,33 @@ constexpr int kCandPerThread = kCombineMaxSplits * kCand / 256;
 __device__ __forceinline__ float h2f(uint16_t u) { return (float)__builtin_bit_cast(_Float16, u); }
 
 // Dequantized key latent channel ch of head g at token t of sequence b.
+// bits of the outlier and inlier regions of a quantized cache
+__device__ __forceinline__ int region_hi_bits(int qmode) { return qmode == STARKV_Q_MIX8_4 ? 8 : 4; }
+__device__ __forceinline__ int region_lo_bits(int qmode) { return qmode == STARKV_Q_MIX4_3 ? 3 : 4; }
+
+// `bits`-wide field at bit `sh` of the little-endian word starting at w (the
+// word's bytes are read one at a time: 3-bit words are not aligned)
+__device__ __forceinline__ int code_field(const uint8_t* w, int sh, int bits) {
+  const int b0 = sh / 8;
+  uint32_t v = w[b0];
+  if (sh % 8 + bits > 8) v |= (uint32_t)w[b0 + 1] << 8;
+  return (int)((v >> (sh % 8)) & ((1u << bits) - 1));
+}
+
 __device__ float key_latent(const CombineParams& p, int g, int b, int t, int ch) {
   const int64_t blk = (int64_t)b * (p.cap_pad / 16) + t / 16;
   const int tau = t % 16, c = ch / 8, wi = ch % 8;
   const uint8_t* code = p.cache + p.k_code_off[g] + blk * 16 * p.k_rb[g];
   if (p.qmode == STARKV_Q_F16)
     return h2f(*reinterpret_cast<const uint16_t*>(code + c * 256 + tau * 16 + wi * 2));
-  const int ro = p.k_ro[g];
-  int q, grp;
-  if (ch < ro) {
-    q = code[c * 128 + tau * 8 + wi];
-    grp = ch / 32;
-  } else {
-    const int n8 = ro / 8;
-    const uint8_t byte = code[n8 * 128 + (c - n8) * 64 + tau * 4 + wi / 2];
-    q = (wi & 1) ? (byte >> 4) : (byte & 15);
-    grp = (ro + 31) / 32 + (ch - ro) / 32;
-  }
+  const int ro = p.k_ro[g], nhi = ro / 8;
+  const int hb = region_hi_bits(p.qmode), lb = region_lo_bits(p.qmode);
+  const bool hi = ch < ro;
+  const int bits = hi ? hb : lb;
+  // chunk c: 16 tokens x `bits` bytes, outlier chunks first; channel wi at bits*wi
+  const uint8_t* tok = code + (hi ? c * 16 * hb : nhi * 16 * hb + (c - nhi) * 16 * lb) + tau * bits;
+  const int q = bits == 8 ? tok[wi] : code_field(tok, bits * wi, bits);
+  const int grp = hi ? ch / 32 : (ro + 31) / 32 + (ch - ro) / 32;
   const uint16_t* m = reinterpret_cast<const uint16_t*>(
       p.cache + p.k_meta_off[g] + (blk * p.k_ng[g] + grp) * 64 + tau * 4);
   return __builtin_fmaf((float)q, h2f(m[0]), h2f(m[1]));
@@ -1054,17 +1131,22 @@ __device__ float value_latent(const CombineParams& p, int b, int t, int r) {
   const uint8_t* code = p.cache + p.v_code_off + blk * 32 * p.v_rb;
   if (p.qmode == STARKV_Q_F16)
     return h2f(*reinterpret_cast<const uint16_t*>(code + (r * 4 + kq) * 16 + slot * 2));
-  int q, grp;
-  if (r < p.v_ro) {
-    q = code[(r * 4 + kq) * 8 + slot];
-    grp = r / 32;
+  const int hb = region_hi_bits(p.qmode), lb = region_lo_bits(p.qmode);
+  const bool hi = r < p.v_ro;
+  const int bits = hi ? hb : lb;
+  // (channel, chunk) words of `bits` bytes, the outlier region first
+  const uint8_t* wd = code + (hi ? (r * 4 + kq) * hb : 4 * p.v_ro * hb + ((r - p.v_ro) * 4 + kq) * lb);
+  int q;
+  if (bits == 8) {
+    q = wd[slot];
   } else {
-    const uint32_t wd =
-        *reinterpret_cast<const uint32_t*>(code + 32 * p.v_ro + ((r - p.v_ro) * 4 + kq) * 4);
-    const int sh = (slot & 1) ? 16 + 4 * (slot / 2) : 4 * (slot / 2);
-    q = (wd >> sh) & 15;
-    grp = (p.v_ro + 31) / 32 + (r - p.v_ro) / 32;
+    // slot 2k / 2k+1 at fields k / k+4 of the word (4 bits: 4 bits apiece and the
+    // second half at bit 16; 3 bits: 3 bits apiece and the second half at bit 12)
+    const int sh = bits == 4 ? ((slot & 1) ? 16 + 4 * (slot / 2) : 4 * (slot / 2))
+                             : ((slot & 1) ? 12 + 3 * (slot / 2) : 3 * (slot / 2));
+    q = code_field(wd, sh, bits);
   }
+  const int grp = hi ? r / 32 : (p.v_ro + 31) / 32 + (r - p.v_ro) / 32;
   const uint8_t* m = p.cache + p.v_meta_off + blk * p.v_ng * 128 + (grp * 4 + kq) * 32;
   return __builtin_fmaf((float)q, h2f(reinterpret_cast<const uint16_t*>(m)[slot]),
                         h2f(reinterpret_cast<const uint16_t*>(m + 16)[slot]));
@@ -1370,7 +1452,8 @@ int SK_NAME(SK_D, SK_QM)(const DecodeParams& p, int ct, int ntw, size_t lds, hip
 #ifdef SK_COMMON
 #define SK_DECL(a, b) \
   int launch_split_d##a##_q##b(const DecodeParams& p, int ct, int ntw, size_t lds, hipStream_t st);
-SK_DECL(64, 0) SK_DECL(64, 1) SK_DECL(64, 2) SK_DECL(128, 0) SK_DECL(128, 1) SK_DECL(128, 2)
+SK_DECL(64, 0) SK_DECL(64, 1) SK_DECL(64, 2) SK_DECL(64, 3)
+SK_DECL(128, 0) SK_DECL(128, 1) SK_DECL(128, 2) SK_DECL(128, 3)
 
 int split_lds_bytes(int frags, int nql, int head_dim, int ct, int raw_bytes, int v_ng,
                     int v_row_bytes) {
@@ -1385,12 +1468,14 @@ int launch_decode_split_ntw(const DecodeParams& p, int head_dim, int qmode, int 
       case STARKV_Q_F16: return launch_split_d128_q0(p, ct, ntw, lds, st);
       case STARKV_Q_INT4: return launch_split_d128_q1(p, ct, ntw, lds, st);
       case STARKV_Q_MIX8_4: return launch_split_d128_q2(p, ct, ntw, lds, st);
+      case STARKV_Q_MIX4_3: return launch_split_d128_q3(p, ct, ntw, lds, st);
     }
   } else if (head_dim == 64) {
     switch (qmode) {
       case STARKV_Q_F16: return launch_split_d64_q0(p, ct, ntw, lds, st);
       case STARKV_Q_INT4: return launch_split_d64_q1(p, ct, ntw, lds, st);
       case STARKV_Q_MIX8_4: return launch_split_d64_q2(p, ct, ntw, lds, st);
+      case STARKV_Q_MIX4_3: return launch_split_d64_q3(p, ct, ntw, lds, st);
     }
   }
   return (int)hipErrorInvalidValue;

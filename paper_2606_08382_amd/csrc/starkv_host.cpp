@@ -32,7 +32,15 @@ starkv_status fail(starkv_status st, const char* fmt, ...) {
 
 int64_t align256(int64_t x) { return (x + 255) / 256 * 256; }
 
-int outlier_channels(int qmode, int r) { return qmode == STARKV_Q_MIX8_4 ? 8 * ((r + 31) / 32) : 0; }
+// bits of the outlier and inlier regions of a quantized latent block
+int hi_bits(int qmode) { return qmode == STARKV_Q_MIX8_4 ? 8 : 4; }
+int lo_bits(int qmode) { return qmode == STARKV_Q_MIX4_3 ? 3 : 4; }
+
+int outlier_channels(int qmode, int r) {
+  if (qmode == STARKV_Q_MIX8_4) return 8 * ((r + 31) / 32);
+  if (qmode == STARKV_Q_MIX4_3) return std::min(r, 8 * std::max(1, (r + 20) / 40));
+  return 0;
+}
 
 int n_groups(int qmode, int r) {
   if (qmode == STARKV_Q_F16) return 0;
@@ -43,7 +51,7 @@ int n_groups(int qmode, int r) {
 int row_bytes(int qmode, int r) {
   if (qmode == STARKV_Q_F16) return 2 * r;
   const int ro = outlier_channels(qmode, r);
-  return ro + (r - ro) / 2;
+  return ro * hi_bits(qmode) / 8 + (r - ro) * lo_bits(qmode) / 8;
 }
 
 constexpr int kLdsLimit = 160 * 1024;
@@ -102,7 +110,7 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
   if (c->head_dim < 2 || c->head_dim % 2) return fail(STARKV_ERR_INVALID_ARG, "head_dim must be even");
   if (c->capacity < 1) return fail(STARKV_ERR_INVALID_ARG, "capacity %d < 1", c->capacity);
   if (!c->key_rank) return fail(STARKV_ERR_INVALID_ARG, "key_rank is NULL");
-  if (c->qmode < STARKV_Q_F16 || c->qmode > STARKV_Q_MIX8_4)
+  if (c->qmode < STARKV_Q_F16 || c->qmode > STARKV_Q_MIX4_3)
     return fail(STARKV_ERR_INVALID_ARG, "qmode %d", c->qmode);
   if (!(c->rope_theta > 1.0) || !std::isfinite(c->rope_theta))
     return fail(STARKV_ERR_INVALID_ARG, "rope_theta must be finite and > 1");

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(HERE, "libstarkv.so")
 STARKV_OK = 0
 STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "UNSUPPORTED", 3: "CAPACITY", 4: "WORKSPACE",
                 5: "ALIGNMENT", 6: "HIP"}
-Q_F16, Q_INT4, Q_MIX8_4 = 0, 1, 2
+Q_F16, Q_INT4, Q_MIX8_4, Q_MIX4_3 = 0, 1, 2, 3
 DT_F16, DT_BF16, DT_F32 = 0, 1, 2   # F32: attention output only
 MAX_KV_HEADS = 16
 

@@ -25,7 +25,7 @@ from typing import List, Optional
 
 import numpy as np
 
-Q_F16, Q_INT4, Q_MIX8_4 = 0, 1, 2
+Q_F16, Q_INT4, Q_MIX8_4, Q_MIX4_3 = 0, 1, 2, 3
 DT_F16, DT_BF16, DT_F32 = 0, 1, 2
 
 
@@ -70,6 +70,14 @@ WORKLOADS = {
     "c5": Workload("c5_70b_b2_ctx64k_mix8_4", 2, 64, 8, 128, 65536, None,
                    "choice:32,48,64,80,96,112,128", 384, Q_MIX8_4, 5e5, DT_BF16, DT_BF16,
                    d_model=8192, append_tokens=4096, seed=1005),
+    # C3's layer with the paper's own quantizer: about 20 % of the channels in
+    # 4 bits, the rest in 3 bits
+    "c3q": Workload("c3q_llama8b_b4_ctx128k_mix4_3", 4, 32, 8, 128, 131072, None,
+                    "perm:16,16,32,32,32,32,48,48", 256, Q_MIX4_3, 5e5, DT_BF16, DT_BF16,
+                    outlier_frac=0.01, d_model=4096, append_tokens=1, seed=1006),
+    "c5q": Workload("c5q_70b_b2_ctx64k_mix4_3", 2, 64, 8, 128, 65536, None,
+                    "choice:32,48,64,80,96,112,128", 384, Q_MIX4_3, 5e5, DT_BF16, DT_BF16,
+                    d_model=8192, append_tokens=4096, seed=1007),
 }
 
 

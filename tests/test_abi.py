@@ -49,7 +49,7 @@ def _cfg(**kw):
 @pytest.mark.parametrize("kw,status", [
     (dict(batch=0), 1), (dict(n_q_heads=7), 1), (dict(key_rank=[24, 32]), 1),
     (dict(key_rank=[32, 144]), 1), (dict(value_rank=40), 1), (dict(value_rank=272), 1),
-    (dict(qmode=7), 1), (dict(rope_theta=1.0), 1), (dict(capacity=0), 1),
+    (dict(qmode=7), 1), (dict(qmode=4), 1), (dict(rope_theta=1.0), 1), (dict(capacity=0), 1),
     (dict(head_dim=96), 2), (dict(group_size=64), 2), (dict(n_q_heads=96, n_kv_heads=2), 2),
     (dict(n_q_heads=6, n_kv_heads=2), 2), (dict(d_model=100), 2),
     (dict(q_dtype=S.DT_F32), 1), (dict(out_dtype=3), 1),
@@ -107,7 +107,7 @@ def test_entry_points_validate_before_launch():
     assert ei.value.status == 1                       # A_all missing
 
 
-@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5"])
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5", "c3q", "c5q"])
 def test_layout_matches_oracle_format(name):
     w = synth.WORKLOADS[name]
     inp = synth.generate(synth.shrink(w, ctx=64, batch=w.batch), with_latents=False)
@@ -147,3 +147,15 @@ def test_workspace_sizes():
     assert S.starkv_decode_workspace_bytes(plan, 0) == 0
     plan0 = S.starkv_plan_create(_cfg())
     assert S.starkv_append_workspace_bytes(plan0, 5) == 0
+
+
+def test_bytes_per_token_of_the_128k_workload_with_the_paper_quantizer():
+    # C3's layer at 4/3 bits (outlier channels r_out = 8 for ranks 16..48, 48 of the 256
+    # value channels): key codes 2*(4+3) + 4*(4+9) + 2*(4+15) = 104 B, key meta
+    # (2*2 + 4*2 + 2*3 groups) * 4 = 72 B, value codes 48/2 + 208*3/8 = 102 B, value meta
+    # (2+7)*4 = 36 B -> 314 B per token (424 B at 8/4 bits)
+    w = synth.WORKLOADS["c3q"]
+    inp = synth.generate(synth.shrink(w, ctx=64), with_latents=False)
+    plan = S.starkv_plan_create(S.make_config(4, 32, 8, 128, 131072, inp.key_rank, 256,
+                                              S.Q_MIX4_3, 5e5))
+    assert S.starkv_cache_bytes(plan) == 314 * 4 * 131072

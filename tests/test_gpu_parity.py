@@ -55,7 +55,8 @@ def _run_case(w, inp, capacity=None, max_ctx=None, ctx_len=None):
 
 @pytest.mark.parametrize("name,ctx,batch", [("c1", 1024, None), ("c1", 1000, None),
                                             ("c2", 700, 2), ("c3", 1100, 2), ("c3", 129, 1),
-                                            ("c5", 600, 2)])
+                                            ("c5", 600, 2), ("c3q", 1100, 2), ("c3q", 129, 1),
+                                            ("c5q", 600, 2)])
 @pytest.mark.parametrize("peaked", [0, 1])
 def test_decode_matches_oracle(name, ctx, batch, peaked):
     w = small(name, ctx, batch)
@@ -64,7 +65,7 @@ def test_decode_matches_oracle(name, ctx, batch, peaked):
 
 
 @pytest.mark.parametrize("name,ctx,batch", [("c1", 1024, None), ("c2", 700, 2), ("c3", 1100, 2),
-                                            ("c5", 600, 2)])
+                                            ("c5", 600, 2), ("c3q", 1100, 2)])
 @pytest.mark.parametrize("out_dtype", [None, synth.DT_F32])
 def test_decode_strongly_peaked(name, ctx, batch, out_dtype):
     """Scores of tens (log2 units) with several needles competing: the fp16 score path alone
@@ -117,7 +118,7 @@ def test_decode_is_deterministic():
         assert torch.equal(layer.out, o1)
 
 
-@pytest.mark.parametrize("name", ["c1", "c2", "c3"])
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c3q"])
 def test_incremental_appends_bit_exact(name):
     """Appends of 1, 3, 37, ... tokens at unaligned rows rewrite only their rows."""
     w = small(name, ctx=300, batch=2)
@@ -149,10 +150,12 @@ def test_incremental_appends_bit_exact(name):
     assert np.array_equal(layer.cache.cpu().numpy(), cache)
 
 
-@pytest.mark.parametrize("name,n_new,d_model", [("c4", 1, 4096), ("c3", 1, 4096), ("c5", 96, 1024)])
+@pytest.mark.parametrize("name,n_new,d_model", [("c4", 1, 4096), ("c3", 1, 4096), ("c5", 96, 1024),
+                                                 ("c3q", 1, 4096), ("c5q", 96, 1024)])
 def test_append_from_hidden_states(name, n_new, d_model):
     """Down-projection then quantization: latents within 1 fp16 ulp of the oracle's fp64
-    product; codes bit-exact when the oracle re-quantizes the GPU's fp16 latents."""
+    product plus the fp32 accumulation bound (which only matters where the sum cancels to
+    a tiny latent); codes bit-exact when the oracle re-quantizes the GPU's fp16 latents."""
     w = small(name, ctx=256, batch=min(synth.WORKLOADS[name].batch, 4))
     w = w.with_(d_model=d_model)
     inp = synth.generate(w, with_hidden=True, n_hidden_tokens=n_new)
@@ -169,7 +172,13 @@ def test_append_from_hidden_states(name, n_new, d_model):
     g = lat_gpu.reshape(-1, width).view(np.float16).astype(np.float64)
     r = lat_ref.view(np.float16).astype(np.float64)
     ulp = np.abs(np.spacing(r.astype(np.float16)).astype(np.float64))
-    assert np.all(np.abs(g - r) <= ulp), f"max diff {np.abs(g - r).max()}"
+    # fp32 accumulation of d_model products: |error| <= d_model * 2^-24 * sum |x_k A_kn|
+    # (recursive summation bound); it matters where the sum cancels to a tiny latent
+    xf = (inp.x.reshape(-1, d_model).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    af = (inp.A.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    acc_err = d_model * 2.0 ** -24 * (np.abs(xf) @ np.abs(af))
+    assert np.all(np.abs(g - r) <= ulp + acc_err), f"max diff {np.abs(g - r).max()}"
+    assert np.mean(np.abs(g - r) <= ulp) > 0.999
     cache = O.new_cache(cfg)
     O.append(cfg, cache, lat_gpu, pos)
     assert np.array_equal(layer.cache.cpu().numpy(), cache)
