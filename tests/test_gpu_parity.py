@@ -184,11 +184,12 @@ def test_append_from_hidden_states(name, n_new, d_model):
     assert np.array_equal(layer.cache.cpu().numpy(), cache)
 
 
-def test_full_size_128k_sampled_heads():
+@pytest.mark.parametrize("name", ["c3", "c3q"])
+def test_full_size_128k_sampled_heads(name):
     """The 128K workload at full size in the benchmark's launch configuration: the whole packed
     cache bit-exact, and sampled query heads (one per KV head, across the batch) within
     tolerance."""
-    w = synth.WORKLOADS["c3"]
+    w = synth.WORKLOADS[name]
     inp = synth.generate(w)
     say(f"full size {w.name}")
     layer = _layer(w, inp)
