@@ -1087,6 +1087,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 constexpr int kCombineMaxSplits = 64;   // one split per lane of the weight wave
 constexpr int kRescoreMax = 32;                        // tokens rescored per query head
 constexpr float kRescoreTau = 1.0f / 64.0f;
+constexpr int kBkVecPerThread = 8;   // B_k block of up to 128 x 128 fp16: 2048 vectors / 256 threads
 constexpr int kCandPerThread = kCombineMaxSplits * kCand / 256;
 
 __device__ __forceinline__ float h2f(uint16_t u) { return (float)__builtin_bit_cast(_Float16, u); }
@@ -1164,6 +1165,9 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   float* lat = reinterpret_cast<float*>(c_t + kRescoreMax); // [kRescoreMax][128] key latents
   float* misc = lat + kRescoreMax * 128; // M, L, L', unused, wave counts [4]
   int* cnt = reinterpret_cast<int*>(misc + 4);
+  // [r_g][D] the head's B_k block, 16-byte aligned
+  uint16_t* bks = reinterpret_cast<uint16_t*>(
+      sm + ((reinterpret_cast<uintptr_t>(misc + 8) - reinterpret_cast<uintptr_t>(sm) + 15) / 16) * 4);
   const int i = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int lane = tid & 63, w = tid >> 6;
   const int g = (int)(((int64_t)i * p.n_kv) / p.n_q);
@@ -1224,6 +1228,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
       if (rg + k * groups < p.rv) w0[k] = *reinterpret_cast<const u4*>(bl + (int64_t)k * groups * ldb);
     }
   }
+  const int r_g = p.k_rank[g];
   if (tid < 64) {                 // split weights: one wave, one split per lane
     const int s = min(tid, p.n_split - 1);
     const float mv = tid < ns ? part[s * sstride + p.rv] : -INFINITY;
@@ -1247,6 +1252,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
     const float x = ce[k].x;
     prio[k] = (x == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(x - M) / Lsum * (1.0f + fabsf(x));
   }
+  float vsel[kRescoreMax];   // candidates' value latents of the thread's first channel
   float tau = kRescoreTau;
   int n_sel = 0;
   for (int it = 0; it < 8; ++it) {
@@ -1281,17 +1287,35 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
       base += cnt[0] + cnt[1] + cnt[2] + cnt[3];
       __syncthreads();
     }
+    // one round of loads for the rescoring: the KV head's up-projection block
+    // B_k (r_g x D fp16, staged in LDS), the candidates' key latents and the
+    // candidates' value latents of this thread's first channel (used by the merge)
+    const int nbk = r_g * D / 8;           // 16-byte vectors
+    u4 bkv[kBkVecPerThread];
+    {
+      const u4* src = reinterpret_cast<const u4*>(p.bk + (int64_t)p.k_bkrow[g] * D);
+#pragma unroll
+      for (int k = 0; k < kBkVecPerThread; ++k)
+        bkv[k] = src[min(tid + k * 256, nbk - 1)];
+    }
+    if (tid < p.rv) {
+#pragma unroll
+      for (int j = 0; j < kRescoreMax; ++j)
+        if (j < n_sel) vsel[j] = value_latent(p, b, c_t[j], tid);
+    }
+#pragma unroll
+    for (int k = 0; k < kBkVecPerThread; ++k)
+      if (tid + k * 256 < nbk) reinterpret_cast<u4*>(bks)[tid + k * 256] = bkv[k];
     // ---- exact scores: dequantized key latents of every candidate, then one
     // (candidate, RoPE pair) item per thread; the items of a candidate are
     // consecutive lanes of one wave and are summed with shuffles
     const int HALF = D / 2;
-    const int r_g = p.k_rank[g];
     for (int it = tid; it < n_sel * r_g; it += 256) {
       const int j = it / r_g, ch = it % r_g;
       lat[j * 128 + ch] = key_latent(p, g, b, c_t[j], ch);
     }
     __syncthreads();
-    const uint16_t* bk = p.bk + (int64_t)p.k_bkrow[g] * D;
+    const uint16_t* bk = bks;
     const uint16_t* qs = static_cast<const uint16_t*>(p.q) + ((int64_t)b * p.n_q + i) * D;
     for (int it0 = 0; it0 < n_sel * HALF; it0 += 256) {
       const int it = it0 + tid;
@@ -1330,11 +1354,18 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   }
   __syncthreads();
   const float inv_l = 1.0f / misc[2];
-  auto merge_channel = [&](int r, const float (&v)[kCombineMaxSplits]) {
+  auto merge_channel = [&](int r, const float (&v)[kCombineMaxSplits], bool first) {
     float acc = 0.0f;
 #pragma unroll
     for (int s = 0; s < kCombineMaxSplits; ++s)
       if (s < ns) acc = __builtin_fmaf(wts[s], v[s], acc);
+    if (first) {                              // the thread's first channel: loaded above
+#pragma unroll
+      for (int j = 0; j < kRescoreMax; ++j)
+        if (j < n_sel) acc = __builtin_fmaf(c_d[j], vsel[j], acc);
+      a[r] = acc * inv_l;
+      return;
+    }
     for (int j0 = 0; j0 < n_sel; j0 += 8) {   // eight candidates' loads in flight
       float vl[8];
 #pragma unroll
@@ -1345,14 +1376,14 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
     }
     a[r] = acc * inv_l;
   };
-  if (tid < p.rv) merge_channel(tid, v0);
+  if (tid < p.rv) merge_channel(tid, v0, true);
   for (int r = tid + 256; r < p.rv; r += 256) {
     float v[kCombineMaxSplits];
 #pragma unroll
     for (int s = 0; s < kCombineMaxSplits; ++s)
       v[s] = *reinterpret_cast<const float*>(pbase + (uint32_t)r * 4u +
                                              (uint32_t)min(s, p.n_split - 1) * sbytes);
-    merge_channel(r, v);
+    merge_channel(r, v, false);
   }
   __syncthreads();
   // o = a . U_V^T restricted to KV head g's d columns (the reordering of Sec. 3.3):
@@ -1484,8 +1515,16 @@ int launch_decode_split_ntw(const DecodeParams& p, int head_dim, int qmode, int 
 int launch_decode_combine(const CombineParams& p, void* stream) {
   if (p.n_split > kCombineMaxSplits) return (int)hipErrorInvalidValue;
   const size_t lds =
-      (size_t)(p.rv + p.n_split + 32 * p.head_dim + 3 * kRescoreMax + kRescoreMax * 128 + 8) *
-      sizeof(float);
+      (size_t)(p.rv + p.n_split + 32 * p.head_dim + 3 * kRescoreMax + kRescoreMax * 128 + 8 + 4) *
+          sizeof(float) +
+      (size_t)p.head_dim * p.head_dim * sizeof(uint16_t);   // B_k block (rank <= head_dim)
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(decode_combine_kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return (int)e;
+    attr = true;
+  }
   dim3 grid(p.n_q, p.batch);
   hipLaunchKernelGGL(decode_combine_kernel, grid, dim3(256), lds,
                      static_cast<hipStream_t>(stream), p);
