@@ -1168,6 +1168,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   // [r_g][D] the head's B_k block, 16-byte aligned
   uint16_t* bks = reinterpret_cast<uint16_t*>(
       sm + ((reinterpret_cast<uintptr_t>(misc + 8) - reinterpret_cast<uintptr_t>(sm) + 15) / 16) * 4);
+  float* red4 = reinterpret_cast<float*>(bks + D * D);   // [4][rv] per-wave split sums
   const int i = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int lane = tid & 63, w = tid >> 6;
   const int g = (int)(((int64_t)i * p.n_kv) / p.n_q);
@@ -1212,13 +1213,21 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   // n_split * sstride floats, far below 4 GiB
   const uint8_t* pbase = reinterpret_cast<const uint8_t*>(part);
   const uint32_t sbytes = (uint32_t)sstride * 4u;
-  float v0[kCombineMaxSplits];
-  {
-    const uint32_t o = (uint32_t)min(tid, p.rv - 1) * 4u;
+  // Value-latent partials: wave w takes splits w, w + 4, .., lane l channels
+  // 4l..4l+3 of each 256-channel chunk, one 16-byte load per (split, chunk), so
+  // a chunk of all splits is 64 loads of 1 KiB per workgroup.  Chunk 0 is
+  // loaded now (it does not depend on the merge weights).
+  constexpr int kSplitsPerWave = kCombineMaxSplits / 4;
+  const int n_chunk = (p.rv + 255) / 256;
+  auto load_chunk = [&](int ch, f4 (&pv)[kSplitsPerWave]) {
+    const uint32_t o = (uint32_t)min(256 * ch + 4 * lane, p.rv - 4) * 4u;
 #pragma unroll
-    for (int s = 0; s < kCombineMaxSplits; ++s)
-      v0[s] = *reinterpret_cast<const float*>(pbase + o + (uint32_t)min(s, p.n_split - 1) * sbytes);
-  }
+    for (int k = 0; k < kSplitsPerWave; ++k)
+      pv[k] = *reinterpret_cast<const f4*>(pbase + o +
+                                           (uint32_t)min(w + 4 * k, p.n_split - 1) * sbytes);
+  };
+  f4 pv0[kSplitsPerWave];
+  load_chunk(0, pv0);
   u4 w0[8];
   {
     const uint16_t* bl = bv + (int64_t)rg * ldb;
@@ -1243,6 +1252,21 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   }
   __syncthreads();
   const float M = misc[0], Lsum = misc[1];
+  // weighted sums of this wave's splits, per channel, into red4[w][r]
+  auto sum_chunk = [&](int ch, const f4 (&pv)[kSplitsPerWave]) {
+    f4 acc = (f4){0, 0, 0, 0};
+#pragma unroll
+    for (int k = 0; k < kSplitsPerWave; ++k)
+      if (w + 4 * k < ns) acc += wts[w + 4 * k] * pv[k];
+    const int r = 256 * ch + 4 * lane;
+    if (r < p.rv) *reinterpret_cast<f4*>(red4 + w * p.rv + r) = acc;
+  };
+  sum_chunk(0, pv0);
+  for (int ch = 1; ch < n_chunk; ++ch) {
+    f4 pv[kSplitsPerWave];
+    load_chunk(ch, pv);
+    sum_chunk(ch, pv);
+  }
 
   // ---- candidate selection: share x (1 + |x|) >= tau, tau raised until at most
   // kRescoreMax remain; compaction in entry order (deterministic)
@@ -1354,11 +1378,8 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   }
   __syncthreads();
   const float inv_l = 1.0f / misc[2];
-  auto merge_channel = [&](int r, const float (&v)[kCombineMaxSplits], bool first) {
-    float acc = 0.0f;
-#pragma unroll
-    for (int s = 0; s < kCombineMaxSplits; ++s)
-      if (s < ns) acc = __builtin_fmaf(wts[s], v[s], acc);
+  auto merge_channel = [&](int r, bool first) {
+    float acc = red4[r] + red4[p.rv + r] + red4[2 * p.rv + r] + red4[3 * p.rv + r];
     if (first) {                              // the thread's first channel: loaded above
 #pragma unroll
       for (int j = 0; j < kRescoreMax; ++j)
@@ -1376,15 +1397,8 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
     }
     a[r] = acc * inv_l;
   };
-  if (tid < p.rv) merge_channel(tid, v0, true);
-  for (int r = tid + 256; r < p.rv; r += 256) {
-    float v[kCombineMaxSplits];
-#pragma unroll
-    for (int s = 0; s < kCombineMaxSplits; ++s)
-      v[s] = *reinterpret_cast<const float*>(pbase + (uint32_t)r * 4u +
-                                             (uint32_t)min(s, p.n_split - 1) * sbytes);
-    merge_channel(r, v, false);
-  }
+  if (tid < p.rv) merge_channel(tid, true);
+  for (int r = tid + 256; r < p.rv; r += 256) merge_channel(r, false);
   __syncthreads();
   // o = a . U_V^T restricted to KV head g's d columns (the reordering of Sec. 3.3):
   // thread (rg, j8) covers rows rg, rg + groups, .. and columns 8*j8..8*j8+7
@@ -1517,7 +1531,8 @@ int launch_decode_combine(const CombineParams& p, void* stream) {
   const size_t lds =
       (size_t)(p.rv + p.n_split + 32 * p.head_dim + 3 * kRescoreMax + kRescoreMax * 128 + 8 + 4) *
           sizeof(float) +
-      (size_t)p.head_dim * p.head_dim * sizeof(uint16_t);   // B_k block (rank <= head_dim)
+      (size_t)p.head_dim * p.head_dim * sizeof(uint16_t) +  // B_k block (rank <= head_dim)
+      (size_t)4 * p.rv * sizeof(float);                      // per-wave split sums
   static bool attr = false;
   if (!attr) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(decode_combine_kernel),
