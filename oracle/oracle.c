@@ -481,7 +481,8 @@ typedef struct {
   int q_is_bf16;
   const int32_t* ctx_len;
   const unsigned char* want;                   /* [B][H_q] */
-  double* out;
+  double* out;                                 /* [B][H_q][d], or NULL */
+  double* lat;                                 /* [B][H_q][r_v] a/l, or NULL */
   int next_task;                               /* protected by lock */
   pthread_mutex_t lock;
 } attn_job;
@@ -497,8 +498,12 @@ static void attn_task(attn_job* J, int b, int g) {
   int L = J->ctx_len[b];
   if (L > cfg->capacity) L = cfg->capacity;
   if (L <= 0) {
-    for (int h = 0; h < nh; ++h)
-      for (int j = 0; j < d; ++j) J->out[((int64_t)b * Hq + heads[h]) * d + j] = 0.0;
+    for (int h = 0; h < nh; ++h) {
+      if (J->out)
+        for (int j = 0; j < d; ++j) J->out[((int64_t)b * Hq + heads[h]) * d + j] = 0.0;
+      if (J->lat)
+        for (int c = 0; c < rv; ++c) J->lat[((int64_t)b * Hq + heads[h]) * rv + c] = 0.0;
+    }
     return;
   }
   double* qd = malloc(sizeof(double) * nh * d);
@@ -535,7 +540,11 @@ static void attn_task(attn_job* J, int b, int g) {
     }
   }
   int ldv = Hkv * d;
-  for (int h = 0; h < nh; ++h) {
+  if (J->lat)
+    for (int h = 0; h < nh; ++h)
+      for (int c = 0; c < rv; ++c)
+        J->lat[((int64_t)b * Hq + heads[h]) * rv + c] = a[(size_t)h * rv + c] / l[h];
+  for (int h = 0; h < nh && J->out; ++h) {
     for (int j = 0; j < d; ++j) {
       double o = 0.0;
       for (int c = 0; c < rv; ++c)
@@ -559,10 +568,10 @@ static void* attn_worker(void* arg) {
   return NULL;
 }
 
-int orc_decode_attn(const orc_cfg* cfg, const uint8_t* cache, const uint16_t* q,
+static int run_attn(const orc_cfg* cfg, const uint8_t* cache, const uint16_t* q,
                     int q_is_bf16, const uint16_t* Bk, const uint16_t* Bv,
                     const int32_t* ctx_len, const int32_t* sel, int n_sel,
-                    double* out, int n_threads) {
+                    double* out, double* lat, int n_threads) {
   int Hq = cfg->n_q_heads;
   unsigned char* want = calloc((size_t)cfg->batch * Hq, 1);
   if (sel) {
@@ -572,7 +581,7 @@ int orc_decode_attn(const orc_cfg* cfg, const uint8_t* cache, const uint16_t* q,
   }
   attn_job J;
   J.cfg = cfg; J.cache = cache; J.q = q; J.Bk = Bk; J.Bv = Bv; J.q_is_bf16 = q_is_bf16;
-  J.ctx_len = ctx_len; J.want = want; J.out = out; J.next_task = 0;
+  J.ctx_len = ctx_len; J.want = want; J.out = out; J.lat = lat; J.next_task = 0;
   pthread_mutex_init(&J.lock, NULL);
   if (n_threads <= 0) n_threads = (int)sysconf(_SC_NPROCESSORS_ONLN);
   int n_tasks = cfg->batch * cfg->n_kv_heads;
@@ -585,6 +594,22 @@ int orc_decode_attn(const orc_cfg* cfg, const uint8_t* cache, const uint16_t* q,
   pthread_mutex_destroy(&J.lock);
   free(want);
   return n_threads;
+}
+
+int orc_decode_attn(const orc_cfg* cfg, const uint8_t* cache, const uint16_t* q,
+                    int q_is_bf16, const uint16_t* Bk, const uint16_t* Bv,
+                    const int32_t* ctx_len, const int32_t* sel, int n_sel,
+                    double* out, int n_threads) {
+  return run_attn(cfg, cache, q, q_is_bf16, Bk, Bv, ctx_len, sel, n_sel, out, NULL, n_threads);
+}
+
+/* The normalized value latent a_i / l_i of every selected query head: the
+ * quantity that the reordering of Sec. 3.3 multiplies by U_V (or, with the
+ * weights absorbed, by W_out,i U_V,i) once per query head. */
+int orc_decode_latent(const orc_cfg* cfg, const uint8_t* cache, const uint16_t* q,
+                      int q_is_bf16, const uint16_t* Bk, const int32_t* ctx_len,
+                      const int32_t* sel, int n_sel, double* lat, int n_threads) {
+  return run_attn(cfg, cache, q, q_is_bf16, Bk, NULL, ctx_len, sel, n_sel, NULL, lat, n_threads);
 }
 
 /* Dense attention (Sec. 3.1) from explicit keys and values; RoPE on keys. */

@@ -92,6 +92,12 @@ int orc_decode_attn(const orc_cfg* cfg, const uint8_t* cache, const uint16_t* q,
                     const int32_t* ctx_len, const int32_t* sel, int n_sel,
                     double* out, int n_threads);
 
+/* the same pass up to the normalized value latent: lat [B][H_q][r_v] fp64 gets
+ * a_i / l_i (zero for ctx_len <= 0) for the selected (b, head) pairs. */
+int orc_decode_latent(const orc_cfg* cfg, const uint8_t* cache, const uint16_t* q,
+                      int q_is_bf16, const uint16_t* Bk, const int32_t* ctx_len,
+                      const int32_t* sel, int n_sel, double* lat, int n_threads);
+
 /* dense attention for one query head from explicit pre-RoPE keys and values:
  * q[d], K[L][d], V[L][d] (fp64) -> out[d]; RoPE applied to K at positions 0..L-1 */
 void orc_dense_attn(int d, int L, const double* q, const double* K,

@@ -59,6 +59,9 @@ def lib():
         L.orc_rope.restype = None
         L.orc_decode_attn.argtypes = [C.POINTER(OrcCfg), P, P, C.c_int, P, P, P, P,
                                       C.c_int, P, C.c_int]
+        L.orc_decode_latent.argtypes = [C.POINTER(OrcCfg), P, P, C.c_int, P, P, P,
+                                        C.c_int, P, C.c_int]
+        L.orc_decode_latent.restype = C.c_int
         L.orc_dense_attn.argtypes = [C.c_int, C.c_int, P, P, P, C.c_double, P]
         L.orc_dense_attn.restype = None
         _lib = L
@@ -198,6 +201,44 @@ def decode_attn(cfg: OrcCfg, cache, q_bits, q_is_bf16, Bk_bits, Bv_bits, ctx_len
                                _p(Bk_bits), _p(Bv_bits), _p(ctx), sp, n_sel, _p(out),
                                int(n_threads))
     return out, nt
+
+
+def decode_latent(cfg: OrcCfg, cache, q_bits, q_is_bf16, Bk_bits, ctx_len, sel=None,
+                  n_threads: int = 0):
+    """The normalized value latent a_i / l_i per query head, fp64 [B][H_q][r_v] (NaN where
+    not selected; zero for an empty context).  sel: list of (b, head) pairs."""
+    q_bits = np.ascontiguousarray(q_bits, dtype=np.uint16)
+    Bk_bits = np.ascontiguousarray(Bk_bits, dtype=np.uint16)
+    ctx = np.ascontiguousarray(ctx_len, dtype=np.int32)
+    lat = np.full((cfg.batch, cfg.n_q_heads, cfg.value_rank), np.nan, np.float64)
+    if sel is not None:
+        s = np.ascontiguousarray(np.asarray(sel, dtype=np.int32).reshape(-1))
+        n_sel, sp = s.size // 2, _p(s)
+    else:
+        s, n_sel, sp = None, 0, None
+    nt = lib().orc_decode_latent(C.byref(cfg), _p(cache), _p(q_bits), int(q_is_bf16),
+                                 _p(Bk_bits), _p(ctx), sp, n_sel, _p(lat), int(n_threads))
+    return lat, nt
+
+
+def decode_attn_absorbed(cfg: OrcCfg, cache, q_bits, q_is_bf16, Bk_bits, W_abs_bits, ctx_len,
+                         batches=None, n_threads: int = 0):
+    """Attention output with the value up-projection absorbed into the output projection
+    (Sec. 3.3, weight absorption): y_b = sum_i (a_i / l_i) . W'_out,i^T, where W_abs_bits
+    [d_out][H_q * r_v] fp16 holds W'_out,i = W_out,i U_V,g(i) of query head i in columns
+    i*r_v .. i*r_v + r_v - 1.  The sum over heads and latent channels is one fp64 matrix
+    product.  batches: the sequences to compute (others are NaN).  Returns (y fp64
+    [B][d_out], threads used)."""
+    H, rv = cfg.n_q_heads, cfg.value_rank
+    bs = list(range(cfg.batch)) if batches is None else list(batches)
+    sel = [(b, i) for b in bs for i in range(H)]
+    lat, nt = decode_latent(cfg, cache, q_bits, q_is_bf16, Bk_bits, ctx_len, sel, n_threads)
+    W = np.ascontiguousarray(W_abs_bits, dtype=np.uint16).view(np.float16).astype(np.float64)
+    assert W.shape[1] == H * rv
+    y = np.full((cfg.batch, W.shape[0]), np.nan, np.float64)
+    if bs:
+        y[bs] = lat[bs].reshape(len(bs), H * rv) @ W.T
+    return y, nt
 
 
 def dense_attn(q: np.ndarray, K: np.ndarray, V: np.ndarray, theta: float) -> np.ndarray:

@@ -26,6 +26,9 @@ Readings (the paper leaves them open):
 * Hadamard matrices of sizes that are not powers of two are taken
   block-diagonal over the binary expansion of the size (Sylvester blocks,
   each normalized): orthonormal, and spreading energy within each block.
+* The output projection can take the value up-projection in (Sec. 3.3, weight
+  absorption): W'_out,i = W_out,i U_V,g(i) per query head i, stored next to each
+  other as one [d_out][H_q * r_v] fp16 matrix (``absorb_output``).
 * The outlier block has the library's size for the chosen cache precision
   (MIX8_4: 8*ceil(r/32); MIX4_3: a fifth of r to the nearest multiple of 8,
   at least 8); with no mixed precision there is a single block.
@@ -166,3 +169,26 @@ def factorize_layer(W_k: np.ndarray, W_v: np.ndarray, n_kv_heads: int, head_dim:
         Av, Bv = fuse_hadamard(Av, Bv, outlier_channels(qmode, rv))
     return Factors(ranks, rv, np.concatenate(A_blocks + [Av], axis=1), np.concatenate(B_blocks),
                    Bv, sig_k, sig_v)
+
+
+def absorb_output(W_out: np.ndarray, B_v: np.ndarray, n_q_heads: int, n_kv_heads: int,
+                  head_dim: int) -> np.ndarray:
+    """Weight absorption of the value up-projection into the output projection (Sec. 3.3).
+
+    W_out: [d_out][H_q * head_dim], the output projection (y = W_out . concat_i o_i);
+    B_v:   [r_v][H_kv * head_dim], U_V^T as ``starkv_decode_attn`` takes it.
+    Returns W_abs [d_out][H_q * r_v] in fp64 with columns i*r_v .. i*r_v + r_v - 1 holding
+    W'_out,i = W_out,i U_V,g(i), g(i) = floor(i * H_kv / H_q), so that
+    y = sum_i W'_out,i (a_i / l_i) for the normalized value latents a_i / l_i.  Stored as
+    fp16 (``np.float16``) for ``starkv_decode_attn_absorbed``."""
+    W_out = np.asarray(W_out, dtype=np.float64)
+    B_v = np.asarray(B_v, dtype=np.float64)
+    d_out = W_out.shape[0]
+    r_v = B_v.shape[0]
+    assert W_out.shape[1] == n_q_heads * head_dim and B_v.shape[1] == n_kv_heads * head_dim
+    W_abs = np.empty((d_out, n_q_heads * r_v))
+    for i in range(n_q_heads):
+        g = i * n_kv_heads // n_q_heads
+        W_abs[:, i * r_v:(i + 1) * r_v] = (W_out[:, i * head_dim:(i + 1) * head_dim]
+                                           @ B_v[:, g * head_dim:(g + 1) * head_dim].T)
+    return W_abs

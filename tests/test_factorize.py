@@ -150,3 +150,23 @@ def test_storage_formats():
     back = (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
     assert np.all(np.abs(back - f.A_all) <= np.abs(f.A_all) * 2.0 ** -8)
     assert bk.shape == (32, 16) and bv.shape == (32, 32)
+
+
+def test_absorbed_output_weights_match_the_per_head_products():
+    """W'_out,i = W_out,i U_V,g(i) (Sec. 3.3), with GQA's head map, against an explicit
+    contraction over the head dimension written with einsum."""
+    rng = np.random.default_rng(7)
+    Hq, Hkv, d, rv, d_out = 6, 2, 8, 16, 20
+    W_out = rng.standard_normal((d_out, Hq * d))
+    B_v = rng.standard_normal((rv, Hkv * d))
+    W_abs = F.absorb_output(W_out, B_v, Hq, Hkv, d)
+    Wo = W_out.reshape(d_out, Hq, d)
+    Bv = B_v.reshape(rv, Hkv, d)
+    g_of = np.array([i * Hkv // Hq for i in range(Hq)])
+    ref = np.einsum("nij,cij->nic", Wo, Bv[:, g_of, :]).reshape(d_out, Hq * rv)
+    np.testing.assert_allclose(W_abs, ref, rtol=1e-13, atol=1e-13)
+    # y = W_out concat(o) for o_i = lat_i U_V,g(i): absorption changes nothing in fp64
+    lat = rng.standard_normal((3, Hq, rv))
+    o = np.stack([lat[:, i] @ Bv[:, g_of[i], :] for i in range(Hq)], axis=1)
+    np.testing.assert_allclose(lat.reshape(3, -1) @ W_abs.T, o.reshape(3, -1) @ W_out.T,
+                               rtol=1e-12, atol=1e-12)

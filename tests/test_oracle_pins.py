@@ -422,6 +422,70 @@ def test_selected_heads_match_full_run():
     assert np.array_equal(part[1, 5], full[1, 5]) and np.array_equal(part[0, 2], full[0, 2])
 
 
+# ---------------------------------------------------------------- weight absorption
+
+def _dyadic(rng, shape, step):
+    """Small multiples of a power of two: every product and short sum below is exact."""
+    return rng.integers(-2, 3, size=shape).astype(np.float64) * step
+
+
+@pytest.mark.parametrize("qmode,Hq,Hkv", [(O.Q_MIX8_4, 8, 2), (O.Q_MIX4_3, 4, 4),
+                                          (O.Q_INT4, 6, 1)])
+def test_absorbed_output_equals_output_projection_of_the_heads(qmode, Hq, Hkv):
+    """Sec. 3.3, weight absorption: (p V' U_V^T) W_out^T = (p V') (U_V^T W_out^T).  W_out and
+    U_V are dyadic so that W'_out,i = W_out,i U_V,g is exact in fp16; the absorbed output must
+    then equal W_out applied to the oracle's per-head outputs (themselves pinned against dense
+    attention above) up to fp64 rounding.  W'_out is formed here by explicit loops."""
+    rng = np.random.default_rng(17 + qmode)
+    B, d, L, rv, d_out = 3, 16, 29, 32, 40
+    ranks = [16] * Hkv
+    cfg, cache, _ = _build(qmode, B, Hq, Hkv, d, L, ranks, rv, rng)
+    Bk = O.f16_bits(rng.standard_normal((sum(ranks), d)) / 4)
+    Bv_f = _dyadic(rng, (rv, Hkv * d), 2.0 ** -3)
+    W_out = _dyadic(rng, (d_out, Hq * d), 2.0 ** -4)
+    W_abs = np.zeros((d_out, Hq * rv))
+    for i in range(Hq):
+        g = i * Hkv // Hq
+        for n in range(d_out):
+            for c in range(rv):
+                W_abs[n, i * rv + c] = sum(W_out[n, i * d + j] * Bv_f[c, g * d + j] for j in range(d))
+    W_bits = O.f16_bits(W_abs)
+    assert np.array_equal(W_bits.view(np.float16).astype(np.float64), W_abs)   # exact in fp16
+    q = O.f16_bits(rng.standard_normal((B, Hq, d)))
+    ctx = [L, 7, 0]
+    o, _ = O.decode_attn(cfg, cache, q, False, Bk, O.f16_bits(Bv_f), ctx)
+    y, _ = O.decode_attn_absorbed(cfg, cache, q, False, Bk, W_bits, ctx)
+    ref = o.reshape(B, Hq * d) @ W_out.T
+    np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-13)
+    assert np.all(y[2] == 0.0)                                  # empty context
+    # the latents themselves: o_i = lat_i . U_V[g-slice]
+    lat, _ = O.decode_latent(cfg, cache, q, False, Bk, ctx)
+    for i in range(Hq):
+        g = i * Hkv // Hq
+        np.testing.assert_allclose(lat[:, i] @ Bv_f[:, g * d:(g + 1) * d], o[:, i],
+                                   rtol=1e-12, atol=1e-13)
+
+
+def test_absorbed_single_token_closed_form_and_sequence_selection():
+    """L = 1: every probability is one, so y = sum_i W'_out,i v'_0 with the dequantized value
+    latent of the only token; computing a subset of the sequences leaves the others alone."""
+    rng = np.random.default_rng(19)
+    B, Hq, Hkv, d, rv, d_out = 2, 4, 2, 16, 48, 24
+    cfg, cache, _ = _build(O.Q_MIX8_4, B, Hq, Hkv, d, 5, [16, 32], rv, rng)
+    Bk = O.f16_bits(rng.standard_normal((48, d)))
+    W_bits = O.f16_bits(rng.standard_normal((d_out, Hq * rv)) / 8)
+    Wf = W_bits.view(np.float16).astype(np.float64)
+    q = O.f16_bits(rng.standard_normal((B, Hq, d)) * 3)
+    _, Vhat = _deq_all(cfg, cache, B, 5)
+    y, _ = O.decode_attn_absorbed(cfg, cache, q, False, Bk, W_bits, [1, 5])
+    for n in range(d_out):
+        expect = sum(Wf[n, i * rv + c] * Vhat[0, 0, c] for i in range(Hq) for c in range(rv))
+        assert abs(y[0, n] - expect) <= 1e-12 * (1 + abs(expect))
+    y1, _ = O.decode_attn_absorbed(cfg, cache, q, False, Bk, W_bits, [1, 5], batches=[1])
+    assert np.all(np.isnan(y1[0]))
+    np.testing.assert_allclose(y1[1], y[1], rtol=1e-14, atol=1e-15)   # matmul blocking only
+
+
 # ---------------------------------------------------------------- down-projection
 
 def test_downprojection_matches_numpy_matmul_and_rounding():
