@@ -119,6 +119,8 @@ def main():
                     help="context tokens of the oracle sample (0: the full context)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches, not graph replays")
+    ap.add_argument("--no-absorbed", action="store_true",
+                    help="skip the step variant with the weight-absorbed output")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -205,6 +207,8 @@ def main():
             graphs[i % len(graphs)].replay()
         torch.cuda.synchronize()
         ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    absorbed = None if args.no_absorbed else time_absorbed(args, w, inp, layers, q, Bk, ctx, x,
+                                                           pos_new, A, stream)
     tokens = int(inp.ctx_len.sum())
     layout = S.starkv_cache_layout(layers[0].plan)
     per_token = (sum(layout.key_row_bytes[g] + 4 * layout.key_groups[g]
@@ -258,6 +262,8 @@ def main():
         "copy_stream": copy,
         "read_stream": rstream,
     }
+    if absorbed is not None:
+        result["absorbed_output"] = absorbed
     if tsum is not None:
         result["roofline"]["traffic_detail"] = {
             k: tsum[k] for k in ("fetch_bytes_per_launch", "write_bytes_per_launch",
@@ -266,6 +272,69 @@ def main():
         log("cpu baseline (oracle)")
         result["cpu_baseline"] = cpu_baseline(w, inp, min(args.cpu_sample_ctx or L, L))
     print(json.dumps(result), flush=True)
+
+
+def time_absorbed(args, w, inp, layers, q, Bk, ctx, x, pos_new, A, stream):
+    """The same decode step with the value up-projection absorbed into the output
+    projection (Sec. 3.3): append, split, then the merge writing the normalized latents and
+    their product with W_abs [d_out][H_q * r_v] into the block output [B][d_out]."""
+    import torch
+    from paper_2606_08382_amd import starkv as S
+    from paper_2606_08382_amd import synth
+    from paper_2606_08382_amd.device import to_dev
+    B, L = w.batch, w.ctx
+    d_out = w.d_model or w.n_q_heads * w.head_dim
+    W = to_dev(synth.absorbed_weights(w, d_out))
+    y = torch.empty((B, d_out), dtype=torch.float32 if w.out_dtype == synth.DT_F32 else torch.int16,
+                    device="cuda")
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+
+    def step(i, events=None):
+        layer = layers[i % len(layers)]
+        if x is not None:
+            layer.append(x, pos_new, A_all=A)
+        if events:
+            events[0].record(stream)
+        S.starkv_decode_split(layer.plan, layer.cache, q, Bk, ctx, L, layer.dec_ws)
+        if events:
+            events[1].record(stream)
+        S.starkv_decode_combine_absorbed(layer.plan, layer.cache, q, Bk, W, d_out, ctx, L, y,
+                                         layer.dec_ws)
+        if events:
+            events[2].record(stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        step(i, ev[i])
+    torch.cuda.synchronize()
+    t_comb = np.array([e[1].elapsed_time(e[2]) for e in ev]) * 1e3
+    ms_step = None
+    if not args.no_graph:
+        graphs = []
+        for li in range(len(layers)):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                step(li)
+            graphs.append(g)
+        for i in range(args.warmup):
+            graphs[i % len(graphs)].replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            graphs[i % len(graphs)].replay()
+        torch.cuda.synchronize()
+        ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    w_bytes = d_out * w.n_q_heads * w.value_rank * 2
+    log(f"absorbed output: combine + product {t_comb.mean():.1f} us, wall/step "
+        f"{(ms_step or 0) * 1e3:.1f} us (W_abs {w_bytes / 1e6:.1f} MB)")
+    return {"d_out": d_out, "W_abs_bytes": w_bytes,
+            "combine_and_product_us": float(t_comb.mean()),
+            "ms_per_step": ms_step,
+            "tokens_per_s": (B / (ms_step / 1e3)) if ms_step else None,
+            "note": "append + split + merge to normalized latents + product with W'_out; "
+                    "the output is the attention block's [B][d_out] (after the output projection)"}
 
 
 _fill_plans = {}

@@ -164,7 +164,8 @@ starkv_status starkv_cache_layout(const starkv_plan* plan, starkv_layout* out);
 
 /* Workspace sizes (bytes).  Append: the fp16 latents of the new tokens plus, when
  * d_model > 0, the down-projection's fp32 partial sums.  Decode: the split
- * partials, for contexts up to max_ctx. */
+ * partials for contexts up to max_ctx, and the normalized value latents that
+ * the absorbed output reads (the same size serves both decode entry points). */
 size_t        starkv_append_workspace_bytes(const starkv_plan* plan, int32_t n_new);
 size_t        starkv_decode_workspace_bytes(const starkv_plan* plan, int32_t max_ctx);
 
@@ -233,6 +234,36 @@ starkv_status starkv_decode_combine(const starkv_plan* plan, const void* cache, 
                                     const void* B_k, const void* B_v,
                                     const int32_t* ctx_len_dev, int32_t max_ctx, void* out,
                                     void* ws, size_t ws_bytes, starkv_stream_t stream);
+
+/* starkv_decode_attn_absorbed -- starkv_decode_attn with the value up-projection
+ * absorbed into the output projection (Sec. 3.3, weight absorption): instead of
+ * the per-head outputs o_i = (a_i / l_i) U_V,g^T it writes the attention block's
+ * output y_b = sum_i o_i W_out,i^T = sum_i W'_out,i (a_i / l_i), with the
+ * absorbed weights W'_out,i = W_out,i U_V,g(i) formed once, offline.
+ *   cache, q, B_k, ctx_len_dev, max_ctx, ws: as for starkv_decode_attn (B_v is
+ *                not used).
+ *   W_abs        device fp16 [d_out][H_q * r_v], 16-byte aligned: W'_out,i of query
+ *                head i in columns i*r_v .. i*r_v + r_v - 1 (W_out,i: the columns
+ *                i*d .. i*d+d-1 of the output projection [d_out][H_q*d]).
+ *   d_out        output width (the model dimension), >= 1.
+ *   out          device [B][d_out] in out_dtype, 16-byte aligned; a sequence with
+ *                ctx_len 0 gets zeros.
+ * Accuracy: the normalized latents (fp32) enter the product as two fp16 parts,
+ * each product exact, accumulated in fp32.
+ * Errors: as starkv_decode_attn; INVALID_ARG for a NULL W_abs or out or d_out < 1. */
+starkv_status starkv_decode_attn_absorbed(const starkv_plan* plan, const void* cache,
+                                          const void* q, const void* B_k, const void* W_abs,
+                                          int32_t d_out, const int32_t* ctx_len_dev,
+                                          int32_t max_ctx, void* out, void* ws, size_t ws_bytes,
+                                          starkv_stream_t stream);
+/* Its second part, after starkv_decode_split (for timing, as above): the merge of
+ * the splits with the exact rescoring, the normalized latents into ws, then the
+ * product with W_abs into out. */
+starkv_status starkv_decode_combine_absorbed(const starkv_plan* plan, const void* cache,
+                                             const void* q, const void* B_k, const void* W_abs,
+                                             int32_t d_out, const int32_t* ctx_len_dev,
+                                             int32_t max_ctx, void* out, void* ws,
+                                             size_t ws_bytes, starkv_stream_t stream);
 
 /* Number of context splits used for max_ctx (tokens per split =
  * starkv_decode_split_tokens); informative. */

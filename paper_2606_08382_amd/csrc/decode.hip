@@ -1175,7 +1175,14 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   int L = p.ctx_len[b];
   L = L < 0 ? 0 : (L > p.max_ctx ? p.max_ctx : L);
   const int64_t out_row = ((int64_t)b * p.n_q + i) * D;
+  const bool to_lat = p.lat != nullptr;
+  const int64_t lat_row = ((int64_t)b * p.n_q + i) * p.rv;
+  const int64_t lat_lo = (int64_t)p.batch * p.n_q * p.rv;
   if (L == 0) {
+    if (to_lat) {
+      for (int r = tid; r < p.rv; r += 256) p.lat[lat_row + r] = p.lat[lat_lo + lat_row + r] = 0;
+      return;
+    }
     for (int j = tid; j < D; j += 256) {
       if (p.out_dtype == STARKV_DT_F32) static_cast<float*>(p.out)[out_row + j] = 0.0f;
       else static_cast<uint16_t*>(p.out)[out_row + j] = 0;
@@ -1234,7 +1241,8 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       w0[k] = (u4){0, 0, 0, 0};
-      if (rg + k * groups < p.rv) w0[k] = *reinterpret_cast<const u4*>(bl + (int64_t)k * groups * ldb);
+      if (!to_lat && rg + k * groups < p.rv)
+        w0[k] = *reinterpret_cast<const u4*>(bl + (int64_t)k * groups * ldb);
     }
   }
   const int r_g = p.k_rank[g];
@@ -1400,6 +1408,15 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   if (tid < p.rv) merge_channel(tid, true);
   for (int r = tid + 256; r < p.rv; r += 256) merge_channel(r, false);
   __syncthreads();
+  if (to_lat) {                 // absorbed output: the latents go to the product pass
+    for (int r = tid; r < p.rv; r += 256) {
+      const float x = a[r];
+      const _Float16 h = (_Float16)x;
+      p.lat[lat_row + r] = __builtin_bit_cast(uint16_t, h);
+      p.lat[lat_lo + lat_row + r] = __builtin_bit_cast(uint16_t, (_Float16)(x - (float)h));
+    }
+    return;
+  }
   // o = a . U_V^T restricted to KV head g's d columns (the reordering of Sec. 3.3):
   // thread (rg, j8) covers rows rg, rg + groups, .. and columns 8*j8..8*j8+7
   float o[8] = {0, 0, 0, 0, 0, 0, 0, 0};

@@ -385,11 +385,18 @@ static int64_t cand_offset(const starkv_plan* P, int32_t max_ctx) {
   return align256((int64_t)P->cfg.batch * ns * P->cfg.n_q_heads * part_stride(P) * 4);
 }
 
+// Then, for the absorbed output, the normalized value latents as two fp16 parts
+// [2][B][H_q * r_v].
+static int64_t lat_offset(const starkv_plan* P, int32_t max_ctx) {
+  const int64_t ns = starkv_decode_splits(P, max_ctx);
+  return cand_offset(P, max_ctx) +
+         align256((int64_t)P->cfg.batch * ns * P->cfg.n_q_heads * kCand * 8);
+}
+
 size_t starkv_decode_workspace_bytes(const starkv_plan* P, int32_t max_ctx) {
   if (!P || max_ctx < 1) return 0;
-  const int64_t ns = starkv_decode_splits(P, max_ctx);
-  return (size_t)(cand_offset(P, max_ctx) +
-                  align256((int64_t)P->cfg.batch * ns * P->cfg.n_q_heads * kCand * 8));
+  return (size_t)(lat_offset(P, max_ctx) +
+                  align256((int64_t)2 * P->cfg.batch * P->cfg.n_q_heads * P->cfg.value_rank * 2));
 }
 
 static starkv_status check_common(const starkv_plan* P, int32_t max_ctx, size_t ws_bytes,
@@ -484,6 +491,10 @@ starkv_status starkv_decode_split(const starkv_plan* P, const void* cache, const
   return hip_status(e, "decode_split launch");
 }
 
+static void combine_params(const starkv_plan* P, const void* cache, const void* q,
+                           const void* B_k, const void* B_v, const int32_t* ctx_len_dev,
+                           int32_t max_ctx, void* out, void* ws, CombineParams& p);
+
 starkv_status starkv_decode_combine(const starkv_plan* P, const void* cache, const void* q,
                                     const void* B_k, const void* B_v,
                                     const int32_t* ctx_len_dev, int32_t max_ctx, void* out,
@@ -491,9 +502,16 @@ starkv_status starkv_decode_combine(const starkv_plan* P, const void* cache, con
   starkv_status st = check_decode(P, cache, q, B_k, B_v, ctx_len_dev, max_ctx, out, ws, ws_bytes,
                                   true);
   if (st != STARKV_OK) return st;
+  CombineParams p;
+  combine_params(P, cache, q, B_k, B_v, ctx_len_dev, max_ctx, out, ws, p);
+  return hip_status(launch_decode_combine(p, static_cast<void*>(stream)), "decode_combine launch");
+}
+
+static void combine_params(const starkv_plan* P, const void* cache, const void* q,
+                           const void* B_k, const void* B_v, const int32_t* ctx_len_dev,
+                           int32_t max_ctx, void* out, void* ws, CombineParams& p) {
   const starkv_config& c = P->cfg;
   const starkv_layout& L = P->layout;
-  CombineParams p;
   std::memset(&p, 0, sizeof(p));
   p.part = static_cast<const float*>(ws);
   p.cand = reinterpret_cast<const float2*>(static_cast<const uint8_t*>(ws) + cand_offset(P, max_ctx));
@@ -532,7 +550,6 @@ starkv_status starkv_decode_combine(const starkv_plan* P, const void* cache, con
   p.v_ro = L.value_outlier_channels;
   p.v_ng = L.value_groups;
   p.v_rb = L.value_row_bytes;
-  return hip_status(launch_decode_combine(p, static_cast<void*>(stream)), "decode_combine launch");
 }
 
 starkv_status starkv_decode_attn(const starkv_plan* P, const void* cache, const void* q,
@@ -546,6 +563,62 @@ starkv_status starkv_decode_attn(const starkv_plan* P, const void* cache, const 
   if (st != STARKV_OK) return st;
   return starkv_decode_combine(P, cache, q, B_k, B_v, ctx_len_dev, max_ctx, out, ws, ws_bytes,
                                stream);
+}
+
+// ---------------------------------------------------------------- absorbed output
+
+static starkv_status check_absorbed(const starkv_plan* P, const void* W_abs, int32_t d_out,
+                                    const void* out) {
+  if (!W_abs || !out) return fail(STARKV_ERR_INVALID_ARG, "NULL device pointer");
+  if (d_out < 1) return fail(STARKV_ERR_INVALID_ARG, "d_out %d < 1", d_out);
+  if ((int64_t)d_out * P->cfg.n_q_heads * P->cfg.value_rank > ((int64_t)1 << 40))
+    return fail(STARKV_ERR_UNSUPPORTED, "W_abs too large");
+  if (reinterpret_cast<uintptr_t>(W_abs) % 16) return fail(STARKV_ERR_ALIGNMENT, "W_abs not 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(out) % 16) return fail(STARKV_ERR_ALIGNMENT, "out not 16-byte aligned");
+  return STARKV_OK;
+}
+
+starkv_status starkv_decode_combine_absorbed(const starkv_plan* P, const void* cache,
+                                             const void* q, const void* B_k, const void* W_abs,
+                                             int32_t d_out, const int32_t* ctx_len_dev,
+                                             int32_t max_ctx, void* out, void* ws,
+                                             size_t ws_bytes, starkv_stream_t stream) {
+  starkv_status st = check_decode(P, cache, q, B_k, nullptr, ctx_len_dev, max_ctx, nullptr, ws,
+                                  ws_bytes, false);
+  if (st != STARKV_OK) return st;
+  st = check_absorbed(P, W_abs, d_out, out);
+  if (st != STARKV_OK) return st;
+  uint16_t* lat = reinterpret_cast<uint16_t*>(static_cast<uint8_t*>(ws) + lat_offset(P, max_ctx));
+  CombineParams cp;
+  combine_params(P, cache, q, B_k, nullptr, ctx_len_dev, max_ctx, nullptr, ws, cp);
+  cp.lat = lat;
+  st = hip_status(launch_decode_combine(cp, static_cast<void*>(stream)), "decode_combine launch");
+  if (st != STARKV_OK) return st;
+  AbsorbParams ap;
+  std::memset(&ap, 0, sizeof(ap));
+  ap.lat = lat;
+  ap.w = static_cast<const uint16_t*>(W_abs);
+  ap.out = out;
+  ap.batch = P->cfg.batch;
+  ap.n_out = d_out;
+  ap.k = P->cfg.n_q_heads * P->cfg.value_rank;
+  ap.out_dtype = P->cfg.out_dtype;
+  return hip_status(launch_absorbed_out(ap, static_cast<void*>(stream)), "absorbed_out launch");
+}
+
+starkv_status starkv_decode_attn_absorbed(const starkv_plan* P, const void* cache, const void* q,
+                                          const void* B_k, const void* W_abs, int32_t d_out,
+                                          const int32_t* ctx_len_dev, int32_t max_ctx, void* out,
+                                          void* ws, size_t ws_bytes, starkv_stream_t stream) {
+  starkv_status st = check_decode(P, cache, q, B_k, nullptr, ctx_len_dev, max_ctx, nullptr, ws,
+                                  ws_bytes, false);
+  if (st != STARKV_OK) return st;
+  st = check_absorbed(P, W_abs, d_out, out);
+  if (st != STARKV_OK) return st;
+  st = starkv_decode_split(P, cache, q, B_k, ctx_len_dev, max_ctx, ws, ws_bytes, stream);
+  if (st != STARKV_OK) return st;
+  return starkv_decode_combine_absorbed(P, cache, q, B_k, W_abs, d_out, ctx_len_dev, max_ctx, out,
+                                        ws, ws_bytes, stream);
 }
 
 // ---------------------------------------------------------------- append

@@ -81,6 +81,10 @@ struct CombineParams {
   const void* q;
   const int32_t* ctx_len;
   void* out;
+  // non-NULL: write the normalized value latents a_i / l_i instead of the
+  // up-projected output, as fp16 parts [2][B][H_q * r_v] (hi = fp16(x), then
+  // lo = fp16(x - hi)); bv and out are unused
+  uint16_t* lat;
   int32_t batch, n_q, n_kv, head_dim, rv;
   int32_t max_ctx, split_len, n_split, part_stride;
   int32_t out_dtype, q_bf16, qmode, cap_pad;
@@ -92,6 +96,15 @@ struct CombineParams {
   int32_t k_rb[STARKV_MAX_KV_HEADS], k_bkrow[STARKV_MAX_KV_HEADS];
   int64_t v_code_off, v_meta_off;
   int32_t v_ro, v_ng, v_rb;
+};
+
+// y [B][n_out] = lat [B][k] . w^T, w [n_out][k] fp16, lat as two fp16 parts
+// (see CombineParams::lat)
+struct AbsorbParams {
+  const uint16_t* lat;
+  const uint16_t* w;
+  void* out;
+  int32_t batch, n_out, k, out_dtype;
 };
 
 struct AppendParams {
@@ -132,6 +145,7 @@ int split_lds_bytes(int frags, int nql, int head_dim, int ct, int raw_bytes, int
 int launch_decode_split_ntw(const DecodeParams& p, int head_dim, int qmode, int ct, int ntw,
                             size_t lds_bytes, void* stream);
 int launch_decode_combine(const CombineParams& p, void* stream);
+int launch_absorbed_out(const AbsorbParams& p, void* stream);
 int launch_append_pack(const AppendParams& p, void* stream);
 // rows (B * n_new) up to which the down-projection streams A_all with the
 // small-M kernel: k blocks of 64 rows, one fp32 partial per block

@@ -66,6 +66,21 @@ class Layer:
                              stream=stream)
         return out
 
+    def decode_absorbed(self, q, B_k, W_abs, ctx_len, max_ctx: Optional[int] = None, out=None,
+                        stream=None):
+        """Attention-block output [B][d_out] with the value up-projection absorbed into the
+        output projection; W_abs [d_out][H_q * r_v] fp16 bits (int16 tensor)."""
+        import torch
+        mc = self.max_ctx if max_ctx is None else max_ctx
+        d_out = int(W_abs.shape[0])
+        if out is None:
+            out = torch.empty((self.batch, d_out),
+                              dtype=torch.float32 if self.out_dtype == S.DT_F32 else torch.int16,
+                              device=self.device)
+        S.starkv_decode_attn_absorbed(self.plan, self.cache, q, B_k, W_abs, d_out, ctx_len, mc,
+                                      out, self.dec_ws, stream=stream)
+        return out
+
     def out_float(self, out=None):
         """Output bit patterns -> float64 numpy."""
         import torch

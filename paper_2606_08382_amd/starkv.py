@@ -54,7 +54,8 @@ EXPORTS = ["starkv_plan_create", "starkv_plan_destroy", "starkv_cache_bytes",
            "starkv_cache_layout", "starkv_append_workspace_bytes",
            "starkv_decode_workspace_bytes", "starkv_append", "starkv_decode_attn",
            "starkv_decode_split", "starkv_decode_combine", "starkv_decode_splits",
-           "starkv_decode_split_tokens", "starkv_status_string", "starkv_last_error"]
+           "starkv_decode_split_tokens", "starkv_status_string", "starkv_last_error",
+           "starkv_decode_attn_absorbed", "starkv_decode_combine_absorbed"]
 
 _lib = None
 
@@ -87,6 +88,12 @@ def lib():
         L.starkv_decode_split.restype = C.c_int
         L.starkv_decode_combine.argtypes = [P, P, P, P, P, P, C.c_int32, P, P, S, P]
         L.starkv_decode_combine.restype = C.c_int
+        L.starkv_decode_attn_absorbed.argtypes = [P, P, P, P, P, C.c_int32, P, C.c_int32, P, P,
+                                                  S, P]
+        L.starkv_decode_attn_absorbed.restype = C.c_int
+        L.starkv_decode_combine_absorbed.argtypes = [P, P, P, P, P, C.c_int32, P, C.c_int32, P,
+                                                     P, S, P]
+        L.starkv_decode_combine_absorbed.restype = C.c_int
         L.starkv_decode_splits.argtypes = [P, C.c_int32]
         L.starkv_decode_splits.restype = C.c_int32
         L.starkv_decode_split_tokens.argtypes = [P, C.c_int32]
@@ -214,6 +221,26 @@ def starkv_decode_combine(plan: Plan, cache, q, B_k, B_v, ctx_len, max_ctx: int,
                                        _ptr(ctx_len), max_ctx, _ptr(out), _ptr(ws),
                                        _nbytes(ws) if ws_bytes is None else ws_bytes,
                                        _stream(stream)))
+
+
+def starkv_decode_attn_absorbed(plan: Plan, cache, q, B_k, W_abs, d_out: int, ctx_len,
+                                max_ctx: int, out, ws, ws_bytes: Optional[int] = None,
+                                stream=None) -> None:
+    _check(lib().starkv_decode_attn_absorbed(plan.handle, _ptr(cache), _ptr(q), _ptr(B_k),
+                                             _ptr(W_abs), d_out, _ptr(ctx_len), max_ctx,
+                                             _ptr(out), _ptr(ws),
+                                             _nbytes(ws) if ws_bytes is None else ws_bytes,
+                                             _stream(stream)))
+
+
+def starkv_decode_combine_absorbed(plan: Plan, cache, q, B_k, W_abs, d_out: int, ctx_len,
+                                   max_ctx: int, out, ws, ws_bytes: Optional[int] = None,
+                                   stream=None) -> None:
+    _check(lib().starkv_decode_combine_absorbed(plan.handle, _ptr(cache), _ptr(q), _ptr(B_k),
+                                                _ptr(W_abs), d_out, _ptr(ctx_len), max_ctx,
+                                                _ptr(out), _ptr(ws),
+                                                _nbytes(ws) if ws_bytes is None else ws_bytes,
+                                                _stream(stream)))
 
 
 def starkv_status_string(status: int) -> str:

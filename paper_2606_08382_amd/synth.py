@@ -14,6 +14,9 @@ and weights are not available):
   * B_k,g ~ N(0,1)/sqrt(r_g), B_v ~ N(0,1)/sqrt(r_v), stored fp16;
   * q ~ N(0,1) (already rotated), fp16 or bf16;
   * hidden states x ~ N(0,1) bf16; down-projection column i ~ N(0,1)*sigma_i/sqrt(d_model);
+  * absorbed output weights W'_out,i (``absorbed_weights``, own stream): entries
+    ~ N(0, 1/(H_q r_v)), the variance of W_out,i U_V,i for an output projection
+    W_out ~ N(0, 1/(H_q d)) and U_V as above; fp16;
   * peaked variant of strength k (peaked=True is k = 1): q x 4k and four needle
     tokens per sequence whose key latents are scaled x 8k (attention concentrates
     on a few tokens with large scores; outputs of order 0.5-1.5).
@@ -185,6 +188,16 @@ def generate(w: Workload, seed: Optional[int] = None, peaked: int = 0,
                   Bk=to_bits(Bk, DT_F16), Bv=to_bits(Bv, DT_F16),
                   q=to_bits(q, w.q_dtype), ctx_len=ctx, latents=latents, scale=scale,
                   x=x, A=A, needles=needles)
+
+
+def absorbed_weights(w: Workload, d_out: int, seed: Optional[int] = None) -> np.ndarray:
+    """fp16 bits [d_out][H_q * r_v]: the absorbed output weights, one column block per query
+    head (drawn from their own stream, seed w.seed + 7919 unless given)."""
+    rng = np.random.Generator(np.random.PCG64(w.seed + 7919 if seed is None else seed))
+    k = w.n_q_heads * w.value_rank
+    W = rng.standard_normal((d_out, k), dtype=np.float32)
+    W *= np.float32(1.0 / np.sqrt(k))
+    return to_bits(W, DT_F16)
 
 
 def shrink(w: Workload, ctx: int, batch: Optional[int] = None, ragged=None) -> Workload:

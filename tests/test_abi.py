@@ -98,6 +98,22 @@ def test_entry_points_validate_before_launch():
     with pytest.raises(S.StarkvError) as ei:
         S.starkv_append(plan, fake + 4, fake, None, fake, 1, None, 0)
     assert ei.value.status == 5
+    # absorbed output: B_v is not needed, W_abs, d_out and out are
+    S.starkv_decode_attn_absorbed  # exported (above); argument errors come first
+    for args, status in [((fake, fake, fake, None, 64, fake, 1000, fake), 1),   # W_abs NULL
+                         ((fake, fake, fake, fake, 0, fake, 1000, fake), 1),    # d_out < 1
+                         ((fake, fake, fake, fake, 64, fake, 1000, None), 1),   # out NULL
+                         ((fake, fake, fake, fake + 8, 64, fake, 1000, fake), 5),
+                         ((fake, fake, fake, fake, 64, fake, 1000, fake + 2), 5),
+                         ((fake, fake, fake, fake, 64, fake, 1001, fake), 3)]:
+        for fn in (S.starkv_decode_attn_absorbed, S.starkv_decode_combine_absorbed):
+            with pytest.raises(S.StarkvError) as ei:
+                fn(plan, *args, fake, need)
+            assert ei.value.status == status, (fn.__name__, args)
+    with pytest.raises(S.StarkvError) as ei:
+        S.starkv_decode_attn_absorbed(plan, fake, fake, fake, fake, 64, fake, 1000, fake, fake,
+                                      need - 1)
+    assert ei.value.status == 4
     hid = S.starkv_plan_create(_cfg(d_model=256))
     with pytest.raises(S.StarkvError) as ei:
         S.starkv_append(hid, fake, fake, fake, fake, 3, fake, 10)

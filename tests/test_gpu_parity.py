@@ -210,6 +210,83 @@ def test_full_size_128k_sampled_heads(name):
     for (b, i) in sel:
         e, s = assert_close(got[b, i], ref[b, i], f"b={b} head={i}", w.out_dtype)
     say(f"  sampled heads ok, last max err {e:.3e} |o| {s:.3e}")
+    # the weight-absorbed output of the same step (hidden size 4096), sampled sequences
+    W = synth.absorbed_weights(w, 4096)
+    y = layer.out_float(layer.decode_absorbed(_dev(inp.q), _dev(inp.Bk), _dev(W),
+                                              _dev(inp.ctx_len)))
+    yref, _ = O.decode_attn_absorbed(cfg, cache, inp.q, True, inp.Bk, W, inp.ctx_len,
+                                     batches=[0, 3])
+    for b in (0, 3):
+        e, s = assert_close(y[b], yref[b], f"absorbed b={b}", w.out_dtype)
+    say(f"  absorbed output ok, last max err {e:.3e} |y| {s:.3e}")
+
+
+def _absorbed_case(w, inp, d_out, ctx_len=None, max_ctx=None, capacity=None):
+    """Append at row 0, decode with the absorbed output, compare with the oracle's y."""
+    say(f"absorbed {w.name} B={w.batch} ctx={w.ctx} d_out={d_out} qmode={w.qmode}")
+    layer = _layer(w, inp, capacity, max_ctx=max_ctx)
+    pos = torch.zeros(w.batch, dtype=torch.int32, device="cuda")
+    layer.append(_dev(inp.latents), pos)
+    W = synth.absorbed_weights(w, d_out)
+    ctx = inp.ctx_len if ctx_len is None else np.asarray(ctx_len, np.int32)
+    y = layer.decode_absorbed(_dev(inp.q), _dev(inp.Bk), _dev(W), _dev(ctx))
+    torch.cuda.synchronize()
+    cfg = oracle_cfg(w, inp, capacity)
+    cache = O.new_cache(cfg)
+    O.append(cfg, cache, inp.latents, [0] * w.batch)
+    mc = layer.max_ctx if max_ctx is None else max_ctx
+    ref, _ = O.decode_attn_absorbed(cfg, cache, inp.q, w.q_dtype == synth.DT_BF16, inp.Bk, W,
+                                    np.minimum(ctx, mc))
+    got = layer.out_float(y)
+    e, sc = assert_close(got, ref, w.name, w.out_dtype)
+    say(f"  max err {e:.3e}  max |y| {sc:.3e}")
+    return layer, got, ref
+
+
+@pytest.mark.parametrize("name,ctx,batch,d_out,ragged", [
+    ("c1", 1024, None, 64, None), ("c3", 1100, 2, 4096, None), ("c3q", 700, 2, 1000, None),
+    ("c5", 600, 2, 2048, None), ("c4", 600, 20, 200, (1, 600)), ("c2", 300, 40, 72, None),
+    ("c1", 200, 70, 40, (5, 200))])
+@pytest.mark.parametrize("peaked", [0, 2])
+def test_absorbed_output_matches_oracle(name, ctx, batch, d_out, ragged, peaked):
+    """Weight-absorbed output (Sec. 3.3): y_b = sum_i W'_out,i a_i / l_i over all query
+    heads; widths that are not multiples of 16, one to five 16-sequence tiles (more than 64
+    sequences take a second row of workgroups), ragged lengths."""
+    w = small(name, ctx, batch, ragged=ragged)
+    inp = synth.generate(w, peaked=peaked)
+    _absorbed_case(w, inp, d_out)
+
+
+def test_absorbed_output_empty_and_clamped_contexts_fp32():
+    w = small("c3", ctx=600, batch=3).with_(out_dtype=synth.DT_F32)
+    inp = synth.generate(w)
+    layer, got, _ = _absorbed_case(w, inp, 256, ctx_len=[0, 600, 5], max_ctx=600)
+    assert np.all(got[0] == 0.0)
+    _absorbed_case(w, inp, 48, ctx_len=[999, 0, 17], max_ctx=400, capacity=1000)
+
+
+def test_absorbed_output_equals_projected_heads():
+    """The same cache decoded both ways: the absorbed output against W_out applied on the CPU
+    to the per-head outputs, with W'_out,i = W_out,i U_V,g(i) formed by absorb_output (fp16);
+    they differ only by the fp16 rounding of W'_out and the GPU arithmetic."""
+    from paper_2606_08382_amd import factorize as F
+    w = small("c3", ctx=900, batch=2).with_(out_dtype=synth.DT_F32)
+    inp = synth.generate(w, peaked=1)
+    layer = _layer(w, inp)
+    layer.append(_dev(inp.latents), torch.zeros(w.batch, dtype=torch.int32, device="cuda"))
+    rng = np.random.default_rng(21)
+    d_out = 512
+    W_out = rng.standard_normal((d_out, w.n_q_heads * w.head_dim)) / np.sqrt(w.n_q_heads * w.head_dim)
+    Bv = inp.Bv.view(np.float16).astype(np.float64)
+    W_abs = F.absorb_output(W_out, Bv, w.n_q_heads, w.n_kv_heads, w.head_dim)
+    Wb = W_abs.astype(np.float16).view(np.uint16)
+    q, Bk, ctx = _dev(inp.q), _dev(inp.Bk), _dev(inp.ctx_len)
+    o = layer.out_float(layer.decode(q, Bk, _dev(inp.Bv), ctx).clone())
+    y = layer.out_float(layer.decode_absorbed(q, Bk, _dev(Wb), ctx))
+    ref = o.reshape(w.batch, -1) @ W_out.T
+    err = np.abs(y - ref)
+    say(f"absorbed vs projected: max err {err.max():.3e} max |y| {np.abs(ref).max():.3e}")
+    assert err.max() <= 2e-3 * np.abs(ref).max()
 
 
 def test_graph_replay_matches_eager():
