@@ -154,10 +154,27 @@ int orc_quantize_block(int qmode, int r, const uint16_t* x,
 /* order, each starting on a 256-byte boundary: for every KV head g its key  */
 /* code plane and key meta plane, then the value code plane and value meta   */
 /* plane.  Keys are tiled in 16-token blocks, values in 32-token blocks.     */
+/* A plane has one row per token slot: per sequence a padded run of rows,  */
+/* or, paged, a pool of pages that a block table hands out to sequences.    */
 /* ------------------------------------------------------------------------ */
 
 static int64_t pad_cap(const orc_cfg* c) { return ((int64_t)c->capacity + 255) / 256 * 256; }
 static int64_t align256(int64_t x) { return (x + 255) / 256 * 256; }
+
+/* Rows of every plane: one padded run per sequence, or the page pool. */
+static int64_t plane_rows(const orc_cfg* c) {
+  return c->page_tokens > 0 ? (int64_t)c->n_pages * c->page_tokens
+                            : (int64_t)c->batch * pad_cap(c);
+}
+
+/* Row of token t of sequence b, or -1 when its page is not a pool page. */
+static int64_t row_of(const orc_cfg* c, int b, int t) {
+  if (c->page_tokens <= 0) return (int64_t)b * pad_cap(c) + t;
+  int per_seq = (c->capacity + c->page_tokens - 1) / c->page_tokens;
+  int32_t pg = c->table[(int64_t)b * per_seq + t / c->page_tokens];
+  if (pg < 0 || pg >= c->n_pages) return -1;
+  return (int64_t)pg * c->page_tokens + t % c->page_tokens;
+}
 
 static int row_bytes(int qmode, int r) {
   if (qmode == ORC_Q_F16) return 2 * r;
@@ -166,7 +183,7 @@ static int row_bytes(int qmode, int r) {
 }
 
 int64_t orc_plane_offset(const orc_cfg* cfg, int which, int head) {
-  int64_t rows = (int64_t)cfg->batch * pad_cap(cfg);
+  int64_t rows = plane_rows(cfg);
   int64_t off = 0;
   for (int g = 0; g < cfg->n_kv_heads; ++g) {
     int r = cfg->key_rank[g];
@@ -195,8 +212,7 @@ int64_t orc_cache_bytes(const orc_cfg* cfg) { return orc_plane_offset(cfg, 4, 0)
 static int64_t key_code_at(const orc_cfg* cfg, int g, int b, int t, int c, int* bit) {
   int r = cfg->key_rank[g];
   int rb = row_bytes(cfg->qmode, r);
-  int64_t base = orc_plane_offset(cfg, 0, g) +
-                 ((int64_t)b * (pad_cap(cfg) / 16) + t / 16) * 16 * rb;
+  int64_t base = orc_plane_offset(cfg, 0, g) + (row_of(cfg, b, t) / 16) * 16 * rb;
   int tau = t % 16, chunk = c / 8, w = c % 8;
   *bit = 0;
   if (cfg->qmode == ORC_Q_F16) return base + chunk * 256 + tau * 16 + w * 2;
@@ -217,7 +233,7 @@ static int64_t key_code_at(const orc_cfg* cfg, int g, int b, int t, int c, int* 
 static int64_t key_meta_at(const orc_cfg* cfg, int g, int b, int t, int gi, int64_t* zoff) {
   int ng = orc_n_groups(cfg->qmode, cfg->key_rank[g]);
   int64_t off = orc_plane_offset(cfg, 1, g) +
-                (((int64_t)b * (pad_cap(cfg) / 16) + t / 16) * ng + gi) * 64 + (t % 16) * 4;
+                ((row_of(cfg, b, t) / 16) * ng + gi) * 64 + (t % 16) * 4;
   *zoff = off + 2;
   return off;
 }
@@ -239,8 +255,7 @@ static void value_slot(int t, int* kq, int* slot) {
 static int64_t value_code_at(const orc_cfg* cfg, int b, int t, int c, int* bit) {
   int r = cfg->value_rank;
   int rb = row_bytes(cfg->qmode, r);
-  int64_t base = orc_plane_offset(cfg, 2, 0) +
-                 ((int64_t)b * (pad_cap(cfg) / 32) + t / 32) * 32 * rb;
+  int64_t base = orc_plane_offset(cfg, 2, 0) + (row_of(cfg, b, t) / 32) * 32 * rb;
   int kq, slot;
   value_slot(t, &kq, &slot);
   *bit = 0;
@@ -264,7 +279,7 @@ static int64_t value_meta_at(const orc_cfg* cfg, int b, int t, int gi, int64_t* 
   int kq, slot;
   value_slot(t, &kq, &slot);
   int64_t off = orc_plane_offset(cfg, 3, 0) +
-                ((int64_t)b * (pad_cap(cfg) / 32) + t / 32) * ng * 128 + (gi * 4 + kq) * 32 + slot * 2;
+                (row_of(cfg, b, t) / 32) * ng * 128 + (gi * 4 + kq) * 32 + slot * 2;
   *zoff = off + 16;
   return off;
 }
@@ -339,7 +354,8 @@ static void* append_one_sequence(void* arg) {
   {
     for (int j = 0; j < n_new; ++j) {
       int t = pos[b] + j;
-      if (t < 0 || t >= cfg->capacity) continue;   /* rows outside the cache are dropped */
+      /* rows outside the cache (or on a page outside the pool) are dropped */
+      if (t < 0 || t >= cfg->capacity || row_of(cfg, b, t) < 0) continue;
       const uint16_t* x = latents + ((int64_t)b * n_new + j) * width;
       int off = 0;
       for (int g = 0; g < cfg->n_kv_heads; ++g) {

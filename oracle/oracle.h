@@ -37,6 +37,13 @@ typedef struct {
   int32_t qmode;
   double  rope_theta;
   int32_t d_model;
+  /* paged layout (page_tokens > 0): the cache is a pool of n_pages pages of
+   * page_tokens rows; token t of sequence b lives in row
+   * table[b][t / page_tokens] * page_tokens + t % page_tokens, with table
+   * [batch][ceil(capacity / page_tokens)] (host memory).  page_tokens == 0:
+   * sequence b owns rows b * padded capacity + t. */
+  int32_t page_tokens, n_pages;
+  const int32_t* table;
 } orc_cfg;
 
 /* ---- fp16 / bf16 (own implementations of the IEEE formats) ---- */

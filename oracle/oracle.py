@@ -23,7 +23,8 @@ class OrcCfg(C.Structure):
     _fields_ = [("batch", C.c_int32), ("n_q_heads", C.c_int32), ("n_kv_heads", C.c_int32),
                 ("head_dim", C.c_int32), ("capacity", C.c_int32),
                 ("key_rank", C.c_int32 * 64), ("value_rank", C.c_int32),
-                ("qmode", C.c_int32), ("rope_theta", C.c_double), ("d_model", C.c_int32)]
+                ("qmode", C.c_int32), ("rope_theta", C.c_double), ("d_model", C.c_int32),
+                ("page_tokens", C.c_int32), ("n_pages", C.c_int32), ("table", C.c_void_p)]
 
 
 def lib():
@@ -74,8 +75,16 @@ def _p(a: np.ndarray):
 
 
 def make_cfg(batch, n_q_heads, n_kv_heads, head_dim, capacity, key_rank, value_rank,
-             qmode, rope_theta, d_model=0) -> OrcCfg:
+             qmode, rope_theta, d_model=0, page_tokens=0, n_pages=0, table=None) -> OrcCfg:
+    """page_tokens > 0: a paged cache of n_pages pages; table [batch][ceil(capacity /
+    page_tokens)] int32 gives the pool page of each sequence's page (kept alive here)."""
     c = OrcCfg()
+    c.page_tokens, c.n_pages = int(page_tokens), int(n_pages)
+    if page_tokens:
+        per_seq = -(-capacity // page_tokens)
+        t = np.ascontiguousarray(np.asarray(table, dtype=np.int32).reshape(batch, per_seq))
+        c._table = t
+        c.table = t.ctypes.data_as(C.c_void_p).value
     c.batch, c.n_q_heads, c.n_kv_heads = batch, n_q_heads, n_kv_heads
     c.head_dim, c.capacity = head_dim, capacity
     for g, r in enumerate(key_rank):

@@ -486,6 +486,84 @@ def test_absorbed_single_token_closed_form_and_sequence_selection():
     np.testing.assert_allclose(y1[1], y[1], rtol=1e-14, atol=1e-15)   # matmul blocking only
 
 
+# ---------------------------------------------------------------- paged cache
+
+def _paged_pair(qmode, B, cap, P, table, n_pages, Hq=4, Hkv=2, d=16, ranks=(16, 32), rv=48):
+    flat = O.make_cfg(B, Hq, Hkv, d, cap, list(ranks), rv, qmode, THETA)
+    paged = O.make_cfg(B, Hq, Hkv, d, cap, list(ranks), rv, qmode, THETA, page_tokens=P,
+                       n_pages=n_pages, table=table)
+    return flat, paged
+
+
+@pytest.mark.parametrize("qmode", [O.Q_F16, O.Q_INT4, O.Q_MIX8_4, O.Q_MIX4_3])
+def test_paged_cache_with_consecutive_pages_is_the_contiguous_cache(qmode):
+    """With each sequence's pages handed out in order (b*4 .. b*4+3 of 128 rows, capacity 512)
+    the pool is byte for byte the contiguous layout (pinned by the golden rows above)."""
+    rng = np.random.default_rng(31 + qmode)
+    B, cap, P = 3, 512, 128
+    table = np.arange(B * 4, dtype=np.int32).reshape(B, 4)
+    flat, paged = _paged_pair(qmode, B, cap, P, table, B * 4)
+    assert O.cache_bytes(flat) == O.cache_bytes(paged)
+    lat = O.f16_bits(rng.standard_normal((B, 300, 16 + 32 + 48)))
+    c1, c2 = O.new_cache(flat), O.new_cache(paged)
+    O.append(flat, c1, lat, [0, 100, 212])
+    O.append(paged, c2, lat, [0, 100, 212])
+    assert np.array_equal(c1, c2)
+
+
+@pytest.mark.parametrize("qmode", [O.Q_INT4, O.Q_MIX4_3])
+def test_paged_shuffled_pages_read_back_and_attend_like_contiguous(qmode):
+    """Pages scattered over a larger pool, appends crossing page boundaries: every token reads
+    back as in the contiguous cache, decode gives the same outputs, and pages no sequence owns
+    stay untouched."""
+    rng = np.random.default_rng(41 + qmode)
+    B, cap, P, n_pages = 2, 700, 128, 17                 # 6 pages per sequence, 5 spare
+    perm = rng.permutation(n_pages).astype(np.int32)
+    table = perm[:12].reshape(B, 6)
+    flat, paged = _paged_pair(qmode, B, cap, P, table, n_pages)
+    c1, c2 = O.new_cache(flat), O.new_cache(paged)
+    width = 16 + 32 + 48
+    start = 0
+    for n in (1, 127, 2, 200, 70, 300):
+        lat = O.f16_bits(rng.standard_normal((B, n, width)))
+        O.append(flat, c1, lat, [start, start])
+        O.append(paged, c2, lat, [start, start])
+        start += n
+    for b in range(B):
+        for t in list(range(0, start, 37)) + [127, 128, start - 1]:
+            k1, v1 = O.read_token(flat, c1, b, t)
+            k2, v2 = O.read_token(paged, c2, b, t)
+            assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
+    Bk = O.f16_bits(rng.standard_normal((48, 16)) / 4)
+    Bv = O.f16_bits(rng.standard_normal((48, 32)) / 4)
+    q = O.f16_bits(rng.standard_normal((B, 4, 16)))
+    o1, _ = O.decode_attn(flat, c1, q, False, Bk, Bv, [start, 129])
+    o2, _ = O.decode_attn(paged, c2, q, False, Bk, Bv, [start, 129])
+    assert np.array_equal(o1, o2)
+    # spare pages: all planes' rows of those pages are still zero
+    starts = [O.plane_offset(paged, 0, 0), O.plane_offset(paged, 1, 0), O.plane_offset(paged, 0, 1),
+              O.plane_offset(paged, 1, 1), O.plane_offset(paged, 2), O.plane_offset(paged, 3),
+              O.cache_bytes(paged)]
+    for lo, hi in zip(starts[:-1], starts[1:]):          # the six planes (256-byte padded)
+        plane = c2[lo:hi]
+        per_row = plane.size // (n_pages * P)            # bytes per row of this plane
+        for pg in perm[12:]:
+            assert not plane[pg * P * per_row:(pg + 1) * P * per_row].any()
+
+
+def test_paged_rows_on_pages_outside_the_pool_are_dropped():
+    rng = np.random.default_rng(51)
+    table = np.array([[2, -1], [0, 7]], np.int32)        # -1 and 7 are not pool pages (3)
+    _, paged = _paged_pair(O.Q_MIX8_4, 2, 256, 128, table, 3)
+    c = O.new_cache(paged)
+    lat = O.f16_bits(rng.standard_normal((2, 256, 96)))
+    O.append(paged, c, lat, [0, 0])
+    ref = O.new_cache(paged)
+    O.append(paged, ref, np.ascontiguousarray(lat[:, :128]), [0, 0])
+    assert np.array_equal(c, ref)                        # only the first pages were written
+    assert c.any()
+
+
 # ---------------------------------------------------------------- down-projection
 
 def test_downprojection_matches_numpy_matmul_and_rounding():
