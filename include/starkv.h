@@ -90,13 +90,30 @@ typedef struct {
   int32_t q_dtype;        /* starkv_dtype of q */
   int32_t out_dtype;      /* starkv_dtype of the attention output (F16, BF16 or F32) */
   int32_t x_dtype;        /* starkv_dtype of hidden states (when d_model > 0) */
+  /* Paged cache, for continuous batching (zero-initialize for the contiguous
+   * layout).  page_tokens = 0: sequence b owns a padded run of rows.  Otherwise a
+   * power of two in [128, 8192]: the cache is a pool of n_pages pages of
+   * page_tokens rows, and block_table maps each sequence's pages to pool pages. */
+  int32_t page_tokens;
+  int32_t n_pages;        /* pages in the pool, >= 1 (paged caches) */
+  /* device int32 [B][ceil(capacity / page_tokens)], 4-byte aligned: pool page of
+   * page j (tokens j*page_tokens ..) of each sequence.  The pointer is fixed at
+   * plan creation; the contents are read by every append and decode call at its
+   * place in the stream, so the caller hands out pages by rewriting entries
+   * between calls (also between replays of a captured graph).  Append drops rows
+   * whose entry is outside [0, n_pages); decode must only reach valid entries
+   * (it clamps others into the pool and reads whatever is there). */
+  const int32_t* block_table;
 } starkv_config;
 
 typedef struct starkv_plan starkv_plan;   /* opaque, immutable after creation */
 
 /* ------------------------------------------------------------------------------
  * Cache format.  All integers little-endian, fp16 as IEEE binary16.
- * Rows (token positions) per sequence are padded to Cp = ceil(capacity/256)*256.
+ * Every plane has one row per token slot.  Contiguous caches: rows per sequence
+ * are padded to Cp = ceil(capacity/256)*256 and token t of sequence b is row
+ * R = b*Cp + t.  Paged caches: the planes have n_pages*P rows (P = page_tokens)
+ * and token t of sequence b is row R = block_table[b][t/P]*P + t%P.
  * The cache is a sequence of planes, each starting on a 256-byte boundary, in
  * this order: for g = 0..H_kv-1 {key code plane g, key meta plane g}, then the
  * value code plane, then the value meta plane.  Meta planes of F16 caches are
@@ -114,8 +131,8 @@ typedef struct starkv_plan starkv_plan;   /* opaque, immutable after creation */
  * Row bytes: F16 2r; INT4 r/2; MIX8_4 r_out + (r - r_out)/2; MIX4_3
  * r_out/2 + 3(r - r_out)/8.
  *
- * Keys, head g, sequence b, token t: 16-token block k = t/16, tau = t%16, at
- *   plane + (b*Cp/16 + k) * 16*row_bytes.  Inside a block the channels go in
+ * Keys, head g, sequence b, token t (row R): 16-token block R/16, tau = t%16, at
+ *   plane + (R/16) * 16*row_bytes.  Inside a block the channels go in
  *   chunks of 8 (chunk c = channels 8c..8c+7); chunk c holds its 16 tokens
  *   back to back, chunk_bytes each (16 F16, 8 for 8-bit, 4 for 4-bit, 3 for
  *   3-bit chunks), outlier chunks first.  Within a chunk: F16 channel w at 2w;
@@ -123,10 +140,10 @@ typedef struct starkv_plan starkv_plan;   /* opaque, immutable after creation */
  *   w; 3-bit channel w at bits 3w..3w+2 of the token's 3 bytes read as a
  *   little-endian 24-bit word.
  *   Key meta: per 16-token block, per group, 16 (s, z) fp16 pairs (4 B per token).
- * Values, sequence b, token t: 32-token block k = t/32 at
- *   plane + (b*Cp/32 + k) * 32*row_bytes.  A block's tokens form four chunks q of
- *   eight slots: with u = t%32, q = (u%16)/4 and slot = 4*(u/16) + u%4 (so chunk q
- *   holds tokens 4q..4q+3 and 16+4q..16+4q+3).  For each chunk q and channel c the
+ * Values, sequence b, token t (row R): 32-token block R/32 at
+ *   plane + (R/32) * 32*row_bytes.  A block's tokens form four chunks q of
+ *   eight slots: with u = t%32, q = u%4 and slot = 4*(u/16) + (u%16)/4 (so chunk q
+ *   holds the tokens q, q+4, .., q+28 of the block, in that order).  For each chunk q and channel c the
  *   eight slots are stored together: F16 16 B (slot at 2*slot), 8-bit 8 B (slot at
  *   byte slot), 4-bit one 32-bit word (slot 2k in bits 4k..4k+3, slot 2k+1 in bits
  *   16+4k..16+4k+3, k = 0..3), 3-bit 3 bytes read as a little-endian 24-bit word
@@ -150,6 +167,9 @@ typedef struct {
   int32_t value_row_bytes;
   int32_t value_groups;
   int32_t value_outlier_channels;
+  int64_t rows;                                  /* rows of every plane: B*Cp, or n_pages*P */
+  int32_t page_tokens;                           /* P (0: contiguous) */
+  int32_t pages_per_sequence;                    /* block_table row length (paged) */
 } starkv_layout;
 
 /* Validates cfg and builds a plan (host memory owned by the library).

@@ -239,12 +239,13 @@ static int64_t key_meta_at(const orc_cfg* cfg, int g, int b, int t, int gi, int6
 }
 
 /* Value code of channel c at token t.  A 32-token block is split into four
- * 8-token chunks k: tokens 4k..4k+3 and 16+4k..16+4k+3; slot 0..3 and 4..7.
- * Within a precision region the order is [channel][chunk][slots]. */
+ * 8-token chunks k: the tokens u = 16h + 4j + k (h = 0, 1; j = 0..3) of the
+ * block, at slot 4h + j.  Within a precision region the order is
+ * [channel][chunk][slots]. */
 static void value_slot(int t, int* kq, int* slot) {
   int tau = t % 32, sub = tau / 16, rem = tau % 16;
-  *kq = rem / 4;
-  *slot = 4 * sub + rem % 4;
+  *kq = rem % 4;
+  *slot = 4 * sub + rem / 4;
 }
 
 /* Within a precision region the order is [channel][chunk][slots]; a

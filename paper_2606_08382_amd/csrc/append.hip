@@ -141,14 +141,19 @@ __global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
     }
   }
   if (t < 0 || t >= p.capacity) return;     // rows outside the cache are dropped
+  if (p.rmap.table) {                        // and rows on pages outside the pool
+    const int pg = p.rmap.table[(int64_t)b * p.rmap.per_seq + (t >> p.rmap.shift)];
+    if (pg < 0 || pg >= p.rmap.n_pages) return;
+  }
   uint8_t* code_plane = p.cache + p.code_off[bl];
   uint8_t* meta_plane = p.cache + p.meta_off[bl];
   const int rb = p.row_bytes[bl];
   const int ngr = p.ng[bl];
-  const int64_t kblk = (int64_t)b * (p.cap_pad / 16) + t / 16;
+  const int64_t row = cache_row(p.rmap, b, t);
+  const int64_t kblk = row / 16;
   const int tau = t % 16;
-  const int64_t vblk = (int64_t)b * (p.cap_pad / 32) + t / 32;
-  const int u = t % 32, kq = (u % 16) / 4, slot = 4 * (u / 16) + u % 4;
+  const int64_t vblk = row / 32;
+  const int u = t % 32, kq = u % 4, slot = 4 * (u / 16) + (u % 16) / 4;
   if (bits == 16) {
     if (on) {
       if (!is_v)

@@ -242,7 +242,7 @@ struct HeadRt {
 template <int D, int QM, int CTH, int KB>
 __device__ __forceinline__ void key_head(const HeadRt& kh, const uint8_t* raw, const h8* frag,
                                          const _Float16* qc, int qzero, int gl, int ct0, int G,
-                                         int lane, int col, int quad,
+                                         int lane, int col, int tcol, int quad,
                                          const CS4 (&cs)[2][D / 32], f4 (&acc_s)[2][CTH]) {
   constexpr int NKBS = D / 32;
   constexpr int QS = D + 8;                  // padded query row (halves)
@@ -261,28 +261,28 @@ __device__ __forceinline__ void key_head(const HeadRt& kh, const uint8_t* raw, c
     const int c = 4 * kb + quad;
     const bool valid = (kb < KB - 1) || (8 * c < kh.rank);
     if (QM == STARKV_Q_F16) {
-      const int off = valid ? kb * 1024 + lane * 16 : 0;
+      const int off = valid ? kb * 1024 + quad * 256 + tcol * 16 : 0;
 #pragma unroll
       for (int s = 0; s < 2; ++s) cf[s][kb] = *reinterpret_cast<const u4*>(rc + s * rb16 + off);
     } else if (QM == STARKV_Q_MIX4_3) {
       // outlier chunks (4-bit, 64 B per 16 tokens) first, then 3-bit chunks (48 B)
       is8[kb] = c < kh.n8;
-      int off = is8[kb] ? kb * 256 + lane * 4 : kh.n8 * 64 + (c - kh.n8) * 48 + col * 3;
+      int off = is8[kb] ? kb * 256 + quad * 64 + tcol * 4 : kh.n8 * 64 + (c - kh.n8) * 48 + tcol * 3;
       int gi = is8[kb] ? c / 4 : kh.ng8 + (c - kh.n8) / 4;
       if (!valid) { off = 0; gi = 0; }
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
-        meta[s][kb] = *reinterpret_cast<const uint32_t*>(rm + (s * kh.ngroups + gi) * 64 + col * 4);
+        meta[s][kb] = *reinterpret_cast<const uint32_t*>(rm + (s * kh.ngroups + gi) * 64 + tcol * 4);
         code[s][kb].x = lds_word_at(rc + s * rb16, off);
       }
     } else {
       is8[kb] = QM == STARKV_Q_MIX8_4 && c < kh.n8;
-      int off = is8[kb] ? kb * 512 + lane * 8 : kh.n8 * 64 + kb * 256 + lane * 4;
+      int off = is8[kb] ? kb * 512 + quad * 128 + tcol * 8 : kh.n8 * 64 + kb * 256 + quad * 64 + tcol * 4;
       int gi = is8[kb] ? c / 4 : kh.ng8 + (c - kh.n8) / 4;
       if (!valid) { off = 0; gi = 0; }
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
-        meta[s][kb] = *reinterpret_cast<const uint32_t*>(rm + (s * kh.ngroups + gi) * 64 + col * 4);
+        meta[s][kb] = *reinterpret_cast<const uint32_t*>(rm + (s * kh.ngroups + gi) * 64 + tcol * 4);
         if (QM == STARKV_Q_INT4) {
           code[s][kb].x = *reinterpret_cast<const uint32_t*>(rc + s * rb16 + off);
         } else {
@@ -434,6 +434,13 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   const int tg = w & (kTokenGroups - 1);   // token group: tokens 32*tg.. of each step
   const int hh = w / kTokenGroups;         // half of the group's KV heads
   const int col = lane & 15, quad = lane >> 4;
+  // Token order of the score tiles: row 4*quad + e of a 16-token subtile is
+  // token 4*e + quad, so a lane's rows are tokens quad, quad+4, quad+8,
+  // quad+12 -- consecutive tokens (an attention sink, a local cluster) fall in
+  // different lanes and so in different rescoring candidates.  The key
+  // reconstruction reads token tcol into MFMA column col, and the value chunks
+  // hold their slots in the same order.
+  const int tcol = 4 * (col & 3) + (col >> 2);
   const int split = blockIdx.x, b = blockIdx.y, hg = blockIdx.z;
   const int g0 = p.hg_first[hg], g1 = p.hg_first[hg + 1], gm = p.hg_mid[hg];
   const int G = p.group_q;
@@ -449,6 +456,15 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   // query loads follow, and the RoPE tables are computed while they are in
   // flight.  The prologue then costs about two memory round trips.
   int L = p.ctx_len[b];
+  // Paged caches: lane j holds the pool page of the split's j-th page (a split
+  // of at most 8192 tokens spans at most 64 pages of at least 128 tokens).
+  const int pg_first = p.rmap.table ? (split * p.split_len) >> p.rmap.shift : 0;
+  int l_page = 0;
+  if (p.rmap.table) {
+    const int pj = min(pg_first + lane, p.rmap.per_seq - 1);
+    const int pg = p.rmap.table[(int64_t)b * p.rmap.per_seq + pj];
+    l_page = pg < 0 ? 0 : (pg >= p.rmap.n_pages ? p.rmap.n_pages - 1 : pg);
+  }
   // The half's heads in processing order (grouped by k-block count): lane i
   // of the head table holds the i-th head's packed fields (staging offsets;
   // row bytes, rank, 8-bit chunks, 8-bit groups, groups, slot; fragment base;
@@ -517,9 +533,15 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   // the next step is issued as soon as the head has been processed, so the
   // copies have most of a step to land.  Lane 0 of every issued copy is active,
   // so the wave issues exactly n_kw copies per step.
-  const int64_t blk16 = (int64_t)b * (p.cap_pad / 16) + (t_begin + 32 * tg) / 16;
-  auto copy_head = [&](const HeadRt& kh, int step) {
-    const int64_t blk = blk16 + (int64_t)step * (kStepTokens / 16);
+  // cache row of the first token of a step (steps never cross a page)
+  auto step_row = [&](int step) -> int64_t {
+    const int t = t_begin + step * kStepTokens;
+    if (!p.rmap.table) return (int64_t)b * p.rmap.cap_pad + t;
+    const int pg = __builtin_amdgcn_readlane(l_page, min((t >> p.rmap.shift) - pg_first, 63));
+    return ((int64_t)pg << p.rmap.shift) + (t & ((1 << p.rmap.shift) - 1));
+  };
+  // blk: the wave's first 16-token key block of the step
+  auto copy_head = [&](const HeadRt& kh, int64_t blk) {
     copy_to_lds_wave(raw + kh.raw_code, p.cache + kh.code_off + blk * 16 * kh.row_bytes,
                      32 * kh.row_bytes, lane);
     if (QM != STARKV_Q_F16)
@@ -554,7 +576,10 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     for (int i = 0; i < n_h; ++i) n_kw += __builtin_amdgcn_readlane(l_kw, i);
   }
   // step 0's key copies (the key staging is not used by the prologue)
-  for (int i = 0; i < n_h; ++i) copy_head(head_rt(i), 0);
+  {
+    const int64_t blk0 = (step_row(0) + 32 * tg) >> 4;
+    for (int i = 0; i < n_h; ++i) copy_head(head_rt(i), blk0);
+  }
 
   // Up-projection fragments.  Fragment (slot, m-tile mt, k-block kb), lane
   // (jj, kq): 8 halves = B_k[row][16*mt + jj] for the 8 channels of chunk
@@ -682,7 +707,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int j = 16 * kq + 4 * quad + e;
-        const float2 r = cmul(rope_ws[(2 * tg + s) * 64 + j], rope_col[col * 65 + j]);
+        const float2 r = cmul(rope_ws[(2 * tg + s) * 64 + j], rope_col[tcol * 65 + j]);
         cc[e] = r.x;
         ss[e] = r.y;
       }
@@ -734,18 +759,16 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     }
     vmode = any8 && any4 ? kValuesMixed : any8 ? kValues8 : kValues4;
   }
-  const int64_t vblk0 = (int64_t)b * (p.cap_pad / 32) + t_begin / 32;
   const int vmeta_bytes = 4 * p.v_ng * 128;
   // value copies this wave issues per step (copy_to_lds: one per 8 KB stride)
   auto n_copies = [&](int n_bytes) { return w * 1024 < n_bytes ? (n_bytes - w * 1024 + 8191) / 8192 : 0; };
   const int n_vw = __builtin_amdgcn_readfirstlane(
       n_copies(vcode_bytes) + (QM != STARKV_Q_F16 ? n_copies(vmeta_bytes) : 0));
   auto load_v = [&](int step) {
-    copy_to_lds(vcode, p.cache + p.v_code_off + (vblk0 + (int64_t)step * 4) * 32 * p.v_row_bytes,
-                vcode_bytes, w, lane);
+    const int64_t vblk = step_row(step) >> 5;
+    copy_to_lds(vcode, p.cache + p.v_code_off + vblk * 32 * p.v_row_bytes, vcode_bytes, w, lane);
     if (QM != STARKV_Q_F16)
-      copy_to_lds(vmeta, p.cache + p.v_meta_off + (vblk0 + (int64_t)step * 4) * p.v_ng * 128,
-                  vmeta_bytes, w, lane);
+      copy_to_lds(vmeta, p.cache + p.v_meta_off + vblk * p.v_ng * 128, vmeta_bytes, w, lane);
   };
   const uint32_t nib_mask = opaque_u32(0x000F000Fu);
 
@@ -786,6 +809,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     const int t_step = t_begin + step * kStepTokens;
     const int tw = t_step + 32 * tg;
     const bool full = (t_step + kStepTokens <= t_end);
+    const int64_t kblk_next = (step_row(step + 1) + 32 * tg) >> 4;   // used while step + 1 < n_steps
     // this step's keys were copied before the value copies of the step, which
     // may still be in flight
     wait_vm(n_vw);
@@ -808,13 +832,13 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       for (int i = cls_end[k - 1]; i < cls_end[k]; ++i) {
         const int partner = prog_s[w ^ 4];
         const HeadRt kh = head_rt(i);
-        if (k == 1) key_head<D, QM, CTH, 1>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, quad, cs, acc_s);
-        if (k == 2) key_head<D, QM, CTH, 2>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, quad, cs, acc_s);
-        if (NKBS > 2 && k == 3) key_head<D, QM, CTH, (NKBS > 2 ? 3 : 1)>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, quad, cs, acc_s);
-        if (NKBS > 3 && k == 4) key_head<D, QM, CTH, (NKBS > 3 ? 4 : 1)>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, quad, cs, acc_s);
+        if (k == 1) key_head<D, QM, CTH, 1>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, cs, acc_s);
+        if (k == 2) key_head<D, QM, CTH, 2>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, cs, acc_s);
+        if (NKBS > 2 && k == 3) key_head<D, QM, CTH, (NKBS > 2 ? 3 : 1)>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, cs, acc_s);
+        if (NKBS > 3 && k == 4) key_head<D, QM, CTH, (NKBS > 3 ? 4 : 1)>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, cs, acc_s);
         // the head's staging has been read (its values are consumed): copy
         // the next step's codes and meta of this head into it
-        if (step + 1 < n_steps) copy_head(kh, step + 1);
+        if (step + 1 < n_steps) copy_head(kh, kblk_next);
         prog += 2 + k;
         if (lane == 0) prog_s[w] = prog;
         const int mine_n = prog * cost_other, part_n = partner * cost_me;
@@ -838,7 +862,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       for (int s = 0; s < 2; ++s)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const bool out = tw + 16 * s + 4 * quad + e >= t_end;
+          const bool out = tw + 16 * s + 4 * e + quad >= t_end;
 #pragma unroll
           for (int c = 0; c < CTH; ++c) x[c][s][e] = out ? -INFINITY : x[c][s][e];
         }
@@ -863,7 +887,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
           const float v = x[c][s][e];
           mx = fmaxf(mx, v);
           const bool gt = v > bx[c][s];
-          bt[c][s] = gt ? step * kStepTokens + 16 * s + e : bt[c][s];
+          bt[c][s] = gt ? step * kStepTokens + 16 * s + 4 * e : bt[c][s];
           bx[c][s] = fmaxf(bx[c][s], v);
         }
       mx = wave_max16(mx);
@@ -943,14 +967,14 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 #pragma unroll
         for (int c = 0; c < CT; ++c) pa[c] = pbuf[(ww * CT + c) * 64 + lane];
         // slots 2k, 2k+1 of this lane's chunk: tokens
-        //   k < 2: 4*quad + 2k + {0,1};  k >= 2: 16 + 4*quad + 2(k-2) + {0,1}
+        //   k < 2: quad + 8k + {0,4};  k >= 2: 16 + quad + 8(k-2) + {0,4}
         u4 vmask;
         if (!FULL) {
           const int tb = t_step + 32 * ww;
 #pragma unroll
           for (int k = 0; k < 4; ++k) {
-            const int t0 = tb + (k < 2 ? 4 * quad + 2 * k : 16 + 4 * quad + 2 * (k - 2));
-            vmask[k] = (t0 < t_end ? 0x0000FFFFu : 0u) | (t0 + 1 < t_end ? 0xFFFF0000u : 0u);
+            const int t0 = tb + quad + (k < 2 ? 8 * k : 16 + 8 * (k - 2));
+            vmask[k] = (t0 < t_end ? 0x0000FFFFu : 0u) | (t0 + 4 < t_end ? 0xFFFF0000u : 0u);
           }
         }
         const uint8_t* vb = vcode + ww * 32 * p.v_row_bytes;
@@ -1033,7 +1057,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       float2* cd = p.cand + (pbase + qmap[il]) * kCand + (tg * 4 + quad) * 2;
 #pragma unroll
       for (int s = 0; s < 2; ++s)
-        cd[s] = make_float2(bx[c][s], __int_as_float(t_begin + bt[c][s] + 32 * tg + 4 * quad));
+        cd[s] = make_float2(bx[c][s], __int_as_float(t_begin + bt[c][s] + 32 * tg + quad));
     }
   }
   if (tg == 0 && quad == 0) {
@@ -1107,7 +1131,7 @@ __device__ __forceinline__ int code_field(const uint8_t* w, int sh, int bits) {
 }
 
 __device__ float key_latent(const CombineParams& p, int g, int b, int t, int ch) {
-  const int64_t blk = (int64_t)b * (p.cap_pad / 16) + t / 16;
+  const int64_t blk = cache_row(p.rmap, b, t) / 16;
   const int tau = t % 16, c = ch / 8, wi = ch % 8;
   const uint8_t* code = p.cache + p.k_code_off[g] + blk * 16 * p.k_rb[g];
   if (p.qmode == STARKV_Q_F16)
@@ -1127,8 +1151,8 @@ __device__ float key_latent(const CombineParams& p, int g, int b, int t, int ch)
 
 // Dequantized value latent channel r at token t of sequence b.
 __device__ float value_latent(const CombineParams& p, int b, int t, int r) {
-  const int64_t blk = (int64_t)b * (p.cap_pad / 32) + t / 32;
-  const int u = t % 32, kq = (u % 16) / 4, slot = 4 * (u / 16) + u % 4;
+  const int64_t blk = cache_row(p.rmap, b, t) / 32;
+  const int u = t % 32, kq = u % 4, slot = 4 * (u / 16) + (u % 16) / 4;
   const uint8_t* code = p.cache + p.v_code_off + blk * 32 * p.v_rb;
   if (p.qmode == STARKV_Q_F16)
     return h2f(*reinterpret_cast<const uint16_t*>(code + (r * 4 + kq) * 16 + slot * 2));

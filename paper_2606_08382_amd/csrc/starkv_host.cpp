@@ -78,6 +78,7 @@ struct starkv_plan {
   uint32_t o_raw[STARKV_MAX_KV_HEADS], o_geo[STARKV_MAX_KV_HEADS], o_fb[STARKV_MAX_KV_HEADS];
   uint32_t o_code[STARKV_MAX_KV_HEADS], o_meta[STARKV_MAX_KV_HEADS];
   int32_t lds_bytes;
+  RowMap rmap;            // cache rows (contiguous or paged)
 };
 
 extern "C" {
@@ -143,6 +144,17 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
                 c->n_kv_heads * D);
   if (rv > 1024) return fail(STARKV_ERR_UNSUPPORTED, "value_rank %d > 1024", rv);
   if (n_groups(c->qmode, rv) > 24) return fail(STARKV_ERR_UNSUPPORTED, "value_rank %d: too many groups", rv);
+  if (c->page_tokens != 0) {
+    const int P = c->page_tokens;
+    if (P < 128 || P > 8192 || (P & (P - 1)))
+      return fail(STARKV_ERR_INVALID_ARG, "page_tokens %d: need a power of two in [128, 8192]", P);
+    if (c->n_pages < 1) return fail(STARKV_ERR_INVALID_ARG, "n_pages %d < 1", c->n_pages);
+    if ((int64_t)c->n_pages * P > ((int64_t)1 << 31) - 1)
+      return fail(STARKV_ERR_UNSUPPORTED, "page pool of %d x %d rows too large", c->n_pages, P);
+    if (!c->block_table) return fail(STARKV_ERR_INVALID_ARG, "block_table is NULL");
+    if (reinterpret_cast<uintptr_t>(c->block_table) % 4)
+      return fail(STARKV_ERR_ALIGNMENT, "block_table not 4-byte aligned");
+  }
   if (c->d_model > 0) {
     if (c->x_dtype != STARKV_DT_BF16) return fail(STARKV_ERR_UNSUPPORTED, "hidden states must be bf16");
     if (c->d_model % 8) return fail(STARKV_ERR_UNSUPPORTED, "d_model %d not a multiple of 8", c->d_model);
@@ -159,8 +171,17 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
   starkv_layout& L = P->layout;
   std::memset(&L, 0, sizeof(L));
   const int64_t Cp = ((int64_t)c->capacity + 255) / 256 * 256;
-  const int64_t rows = (int64_t)c->batch * Cp;
+  const bool paged = c->page_tokens != 0;
+  const int64_t rows = paged ? (int64_t)c->n_pages * c->page_tokens : (int64_t)c->batch * Cp;
   L.padded_capacity = (int32_t)Cp;
+  L.rows = rows;
+  L.page_tokens = paged ? c->page_tokens : 0;
+  L.pages_per_sequence = paged ? (c->capacity + c->page_tokens - 1) / c->page_tokens : 0;
+  P->rmap.table = paged ? c->block_table : nullptr;
+  P->rmap.cap_pad = (int32_t)Cp;
+  P->rmap.shift = paged ? __builtin_ctz((unsigned)c->page_tokens) : 0;
+  P->rmap.per_seq = L.pages_per_sequence;
+  P->rmap.n_pages = paged ? c->n_pages : 0;
   L.sum_key_rank = sum_r;
   int64_t off = 0;
   for (int g = 0; g < c->n_kv_heads; ++g) {
@@ -459,7 +480,7 @@ starkv_status starkv_decode_split(const starkv_plan* P, const void* cache, const
   p.n_q = c.n_q_heads;
   p.n_kv = c.n_kv_heads;
   p.group_q = c.n_q_heads / c.n_kv_heads;
-  p.cap_pad = P->layout.padded_capacity;
+  p.rmap = P->rmap;
   p.max_ctx = max_ctx;
   p.split_len = starkv_decode_split_tokens(P, max_ctx);
   p.n_split = starkv_decode_splits(P, max_ctx);
@@ -533,7 +554,7 @@ static void combine_params(const starkv_plan* P, const void* cache, const void* 
   p.out_dtype = c.out_dtype;
   p.q_bf16 = c.q_dtype == STARKV_DT_BF16;
   p.qmode = c.qmode;
-  p.cap_pad = L.padded_capacity;
+  p.rmap = P->rmap;
   p.score_scale = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
   p.log2_theta = std::log2(c.rope_theta);
   for (int g = 0; g < c.n_kv_heads; ++g) {
@@ -707,7 +728,7 @@ starkv_status starkv_append(const starkv_plan* P, void* cache, const void* x_or_
   a.n_new = n_new;
   a.width = P->width;
   a.capacity = c.capacity;
-  a.cap_pad = P->layout.padded_capacity;
+  a.rmap = P->rmap;
   a.qmode = c.qmode;
   a.n_kv = c.n_kv_heads;
   int lo = 0;

@@ -13,6 +13,26 @@ constexpr int kThreads = 64 * kWaves;
 constexpr int kWaveTokens = 32;           // tokens per wave per step (two 16-token subtiles)
 constexpr int kStepTokens = kTokenGroups * kWaveTokens;
 
+// Rows of the cache planes.  Contiguous caches (table == NULL): sequence b owns
+// rows b*cap_pad .. b*cap_pad + cap_pad - 1.  Paged caches: the planes have
+// n_pages << shift rows, and token t of sequence b lives in row
+// (table[b*per_seq + (t >> shift)] << shift) + (t & ((1 << shift) - 1)).
+struct RowMap {
+  const int32_t* table;
+  int32_t cap_pad, shift, per_seq, n_pages;
+};
+
+#if defined(__HIP__)
+// Row of token t of sequence b; page ids are clamped into the pool (the append
+// kernel checks them itself and drops rows on other pages).
+__device__ __forceinline__ int64_t cache_row(const RowMap& m, int b, int t) {
+  if (!m.table) return (int64_t)b * m.cap_pad + t;
+  int pg = m.table[(int64_t)b * m.per_seq + (t >> m.shift)];
+  pg = pg < 0 ? 0 : (pg >= m.n_pages ? m.n_pages - 1 : pg);
+  return ((int64_t)pg << m.shift) + (t & ((1 << m.shift) - 1));
+}
+#endif
+
 // One key head as seen by the split kernel (all offsets in bytes).
 struct KHeadInfo {
   int64_t code_off;      // key code plane
@@ -38,7 +58,7 @@ struct DecodeParams {
   float* part;                 // split partials
   float2* cand;                // per (b, split, query head): kCand (score, token) candidates
   int32_t batch, n_q, n_kv, group_q;   // group_q = H_q / H_kv
-  int32_t cap_pad;             // Cp
+  RowMap rmap;
   int32_t max_ctx, split_len, n_split;
   int32_t q_bf16;
   float score_scale;           // log2(e)/sqrt(d)
@@ -87,7 +107,8 @@ struct CombineParams {
   uint16_t* lat;
   int32_t batch, n_q, n_kv, head_dim, rv;
   int32_t max_ctx, split_len, n_split, part_stride;
-  int32_t out_dtype, q_bf16, qmode, cap_pad;
+  int32_t out_dtype, q_bf16, qmode;
+  RowMap rmap;
   float score_scale;
   double log2_theta;
   // key head of this query head's group and the value latent (cache layout)
@@ -114,7 +135,8 @@ struct AppendParams {
   uint16_t* lat_out;           // fp16 latents written when summing partials
   int32_t k_split;
   const int32_t* pos;
-  int32_t batch, n_new, width, capacity, cap_pad, qmode;
+  int32_t batch, n_new, width, capacity, qmode;
+  RowMap rmap;
   int32_t n_kv;
   // per block: 0..n_kv-1 key heads, n_kv = values
   int32_t rank[STARKV_MAX_KV_HEADS + 1];

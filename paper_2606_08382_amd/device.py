@@ -21,16 +21,71 @@ def to_dev(bits: np.ndarray, device="cuda"):
     return torch.from_numpy(a.copy()).to(device)
 
 
+class PagePool:
+    """Host-side page allocator of a paged cache (continuous batching).
+
+    Keeps the free pool pages and, per sequence slot, the pages it holds; the block
+    table lives on the device (the plan reads it) with a host copy that ``sync``
+    uploads.  Pages are handed out lowest-free-first unless ``rng`` shuffles the
+    free list (tests use that to scatter sequences over the pool)."""
+
+    def __init__(self, n_pages: int, page_tokens: int, batch: int, capacity: int,
+                 device="cuda", rng: Optional[np.random.Generator] = None):
+        import torch
+        self.n_pages, self.page_tokens, self.batch = n_pages, page_tokens, batch
+        self.capacity = capacity
+        self.per_seq = -(-capacity // page_tokens)
+        free = np.arange(n_pages, dtype=np.int32)
+        if rng is not None:
+            free = rng.permutation(free).astype(np.int32)
+        self.free = list(free[::-1])                 # pop() hands out free[0] first
+        self.host = np.full((batch, self.per_seq), -1, np.int32)
+        self.table = torch.full((batch, self.per_seq), -1, dtype=torch.int32, device=device)
+
+    def ensure(self, b: int, n_tokens: int) -> None:
+        """Give sequence b pages for its first n_tokens tokens."""
+        need = -(-n_tokens // self.page_tokens)
+        if n_tokens > self.capacity:
+            raise ValueError(f"sequence {b}: {n_tokens} tokens exceed the capacity")
+        for j in range(need):
+            if self.host[b, j] < 0:
+                if not self.free:
+                    raise MemoryError("page pool exhausted")
+                self.host[b, j] = self.free.pop()
+
+    def release(self, b: int) -> None:
+        """Return all pages of sequence b to the pool."""
+        for j in range(self.per_seq):
+            if self.host[b, j] >= 0:
+                self.free.append(int(self.host[b, j]))
+                self.host[b, j] = -1
+
+    def pages_in_use(self) -> int:
+        return int((self.host >= 0).sum())
+
+    def sync(self) -> None:
+        """Upload the host table (stream-ordered before later library calls)."""
+        import torch
+        self.table.copy_(torch.from_numpy(self.host))
+
+
 class Layer:
-    """Plan + cache + workspaces of one attention layer."""
+    """Plan + cache + workspaces of one attention layer (contiguous, or paged when
+    page_tokens > 0: then ``pool`` is the layer's PagePool)."""
 
     def __init__(self, batch, n_q_heads, n_kv_heads, head_dim, capacity, key_rank, value_rank,
                  qmode, rope_theta, q_dtype, out_dtype, d_model=0, device="cuda",
-                 max_ctx: Optional[int] = None):
+                 max_ctx: Optional[int] = None, page_tokens: int = 0, n_pages: int = 0,
+                 page_rng: Optional[np.random.Generator] = None):
         import torch
+        self.pool = None
+        if page_tokens:
+            self.pool = PagePool(n_pages, page_tokens, batch, capacity, device, page_rng)
         self.cfg = S.make_config(batch, n_q_heads, n_kv_heads, head_dim, capacity, key_rank,
                                  value_rank, qmode, rope_theta, d_model=d_model,
-                                 q_dtype=q_dtype, out_dtype=out_dtype)
+                                 q_dtype=q_dtype, out_dtype=out_dtype, page_tokens=page_tokens,
+                                 n_pages=n_pages,
+                                 block_table=self.pool.table if self.pool else None)
         self.plan = S.starkv_plan_create(self.cfg)
         self.device = device
         self.batch, self.n_q, self.head_dim = batch, n_q_heads, head_dim

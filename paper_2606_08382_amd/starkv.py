@@ -34,7 +34,8 @@ class starkv_config(C.Structure):
                 ("key_rank", C.POINTER(C.c_int32)), ("value_rank", C.c_int32),
                 ("qmode", C.c_int32), ("group_size", C.c_int32), ("rope_theta", C.c_double),
                 ("d_model", C.c_int32), ("q_dtype", C.c_int32), ("out_dtype", C.c_int32),
-                ("x_dtype", C.c_int32)]
+                ("x_dtype", C.c_int32), ("page_tokens", C.c_int32), ("n_pages", C.c_int32),
+                ("block_table", C.c_void_p)]
 
 
 class starkv_layout(C.Structure):
@@ -47,7 +48,8 @@ class starkv_layout(C.Structure):
                 ("key_outlier_channels", C.c_int32 * MAX_KV_HEADS),
                 ("value_code_offset", C.c_int64), ("value_meta_offset", C.c_int64),
                 ("value_row_bytes", C.c_int32), ("value_groups", C.c_int32),
-                ("value_outlier_channels", C.c_int32)]
+                ("value_outlier_channels", C.c_int32), ("rows", C.c_int64),
+                ("page_tokens", C.c_int32), ("pages_per_sequence", C.c_int32)]
 
 
 EXPORTS = ["starkv_plan_create", "starkv_plan_destroy", "starkv_cache_bytes",
@@ -144,11 +146,14 @@ class Plan:
 
 def make_config(batch, n_q_heads, n_kv_heads, head_dim, capacity, key_rank, value_rank,
                 qmode, rope_theta, d_model=0, q_dtype=DT_BF16, out_dtype=DT_BF16,
-                x_dtype=DT_BF16, group_size=32):
+                x_dtype=DT_BF16, group_size=32, page_tokens=0, n_pages=0, block_table=None):
+    """block_table: device int32 [batch][ceil(capacity / page_tokens)] (tensor or address)
+    for a paged cache."""
     ranks = (C.c_int32 * max(len(key_rank), 1))(*[int(r) for r in key_rank])
     cfg = starkv_config(batch, n_q_heads, n_kv_heads, head_dim, capacity,
                         C.cast(ranks, C.POINTER(C.c_int32)), value_rank, qmode, group_size,
-                        float(rope_theta), d_model, q_dtype, out_dtype, x_dtype)
+                        float(rope_theta), d_model, q_dtype, out_dtype, x_dtype,
+                        page_tokens, n_pages, _ptr(block_table))
     cfg._ranks = ranks   # keep the array alive with the struct
     return cfg
 
