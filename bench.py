@@ -119,6 +119,9 @@ def main():
                     help="context tokens of the oracle sample (0: the full context)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches, not graph replays")
+    ap.add_argument("--page-tokens", type=int, default=0,
+                    help="paged cache: pool pages of this many tokens, handed out in shuffled "
+                         "order (0: each sequence owns a contiguous run of rows)")
     ap.add_argument("--no-absorbed", action="store_true",
                     help="skip the step variant with the weight-absorbed output")
     args = ap.parse_args()
@@ -140,9 +143,18 @@ def main():
     B, L = w.batch, w.ctx
     layers = []
     lat_chunk = 16384
+    P = args.page_tokens
     for li in range(args.layers):
+        paged = {}
+        if P:
+            n_pages = int(sum(-(-int(x) // P) for x in inp.ctx_len))
+            paged = dict(page_tokens=P, n_pages=n_pages, page_rng=np.random.default_rng(1000 + li))
         layer = Layer(B, w.n_q_heads, w.n_kv_heads, w.head_dim, L, inp.key_rank, w.value_rank,
-                      w.qmode, w.rope_theta, w.q_dtype, w.out_dtype, d_model=w.d_model)
+                      w.qmode, w.rope_theta, w.q_dtype, w.out_dtype, d_model=w.d_model, **paged)
+        if P:
+            for b in range(B):
+                layer.pool.ensure(b, int(inp.ctx_len[b]))
+            layer.pool.sync()
         pos = torch.zeros(B, dtype=torch.int32, device="cuda")
         for t0 in range(0, L, lat_chunk):
             chunk = to_dev(np.ascontiguousarray(inp.latents[:, t0:t0 + lat_chunk]))
@@ -242,7 +254,10 @@ def main():
         "config": {"workload": w.name, "batch": B, "ctx": L, "q_heads": w.n_q_heads,
                    "kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
                    "key_ranks": inp.key_rank, "value_rank": w.value_rank,
-                   "cache": "int8/int4 mixed, 32-channel groups", "layers_rotated": args.layers,
+                   "cache": {0: "fp16", 1: "int4", 2: "int8/int4 mixed", 3: "int4/int3 mixed"}[w.qmode]
+                            + ", 32-channel groups"
+                            + (f", paged ({P}-token pages, shuffled pool)" if P else ""),
+                   "layers_rotated": args.layers,
                    "append": f"{w.append_tokens} token/seq from bf16 hidden {w.d_model}",
                    "launch": "eager" if args.no_graph else "hip graph per layer",
                    "ms_per_step_eager": ms_eager},
@@ -346,9 +361,13 @@ def _fill_plan(layer, w, inp):
     from paper_2606_08382_amd import starkv as S
     key = id(layer)
     if key not in _fill_plans:
+        pool = layer.pool
         cfg = S.make_config(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.ctx, inp.key_rank,
                             w.value_rank, w.qmode, w.rope_theta, d_model=0,
-                            q_dtype=w.q_dtype, out_dtype=w.out_dtype)
+                            q_dtype=w.q_dtype, out_dtype=w.out_dtype,
+                            page_tokens=pool.page_tokens if pool else 0,
+                            n_pages=pool.n_pages if pool else 0,
+                            block_table=pool.table if pool else None)
         _fill_plans[key] = S.starkv_plan_create(cfg)
     return _fill_plans[key]
 

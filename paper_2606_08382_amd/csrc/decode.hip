@@ -71,6 +71,45 @@ __device__ __forceinline__ float wave_sum16(float v) {
   return v;
 }
 
+// ceil(x / k) for 0 <= x < 2^17 + 64 and 1 <= k <= 64, with rk = rcp_up(k),
+// the smallest float >= 1/k: the product rounds to the exact quotient's floor
+// (x/k is at least 1/64 below the next integer unless it is one, and the
+// relative error stays below 2^-22).
+__device__ __forceinline__ float rcp_up(int k) {
+  float r = __builtin_amdgcn_rcpf((float)k);           // within 1 ulp of 1/k
+  const float e = __builtin_fmaf(r, (float)k, -1.0f);  // exact residual
+  if (e >= 0.0f) {                                     // step down while still >= 1/k
+    const float d = __uint_as_float(__float_as_uint(r) - 1u);
+    if (__builtin_fmaf(d, (float)k, -1.0f) >= 0.0f) r = d;
+  } else {
+    r = __uint_as_float(__float_as_uint(r) + 1u);
+  }
+  return r;
+}
+__device__ __forceinline__ int div_up_small(int x, int k, float rk) {
+  return (int)((float)(x + k - 1) * rk);
+}
+
+// Work plan of one decode step for up to 64 sequences of ragged lengths: the
+// split length S = kStepTokens * k is the smallest with at most `cap` work
+// items sum_b ceil(L_b / S) (k >= k_lo keeps every sequence at <= 64 splits,
+// k <= 64 keeps S <= 8192), and the items are the sequences' splits in order.
+// Every wave that calls this gets the same plan.  len: the clamped length held
+// by lane b (lanes >= B hold 0).  Returns k; *cnt gets the split count of
+// sequence `lane`.
+__device__ __forceinline__ int wave_split_plan(int len, int B, int k_lo, int cap, int lane,
+                                               int* cnt) {
+  const int m = (len + kStepTokens - 1) / kStepTokens;      // steps of sequence `lane`
+  const int k = min(k_lo + lane, 64);                       // candidate of this lane
+  const float rk = rcp_up(k);
+  int items = 0;
+  for (int j = 0; j < B; ++j) items += div_up_small(__builtin_amdgcn_readlane(m, j), k, rk);
+  const uint64_t ok = __ballot(items <= cap);
+  const int ks = ok ? min(k_lo + (int)__builtin_ctzll(ok), 64) : 64;
+  *cnt = div_up_small(m, ks, rcp_up(ks));
+  return ks;
+}
+
 __device__ __forceinline__ float2 cmul(float2 a, float2 b) {
   return make_float2(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x);
 }
@@ -441,7 +480,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   // reconstruction reads token tcol into MFMA column col, and the value chunks
   // hold their slots in the same order.
   const int tcol = 4 * (col & 3) + (col >> 2);
-  const int split = blockIdx.x, b = blockIdx.y, hg = blockIdx.z;
+  const int hg = blockIdx.z;
   const int g0 = p.hg_first[hg], g1 = p.hg_first[hg + 1], gm = p.hg_mid[hg];
   const int G = p.group_q;
   const int nql = (g1 - g0) * G;
@@ -455,16 +494,9 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   // this thread's query vectors); the key copies of step 0, the fragment and
   // query loads follow, and the RoPE tables are computed while they are in
   // flight.  The prologue then costs about two memory round trips.
-  int L = p.ctx_len[b];
-  // Paged caches: lane j holds the pool page of the split's j-th page (a split
-  // of at most 8192 tokens spans at most 64 pages of at least 128 tokens).
-  const int pg_first = p.rmap.table ? (split * p.split_len) >> p.rmap.shift : 0;
-  int l_page = 0;
-  if (p.rmap.table) {
-    const int pj = min(pg_first + lane, p.rmap.per_seq - 1);
-    const int pg = p.rmap.table[(int64_t)b * p.rmap.per_seq + pj];
-    l_page = pg < 0 ? 0 : (pg >= p.rmap.n_pages ? p.rmap.n_pages - 1 : pg);
-  }
+  // context length: of this workgroup's sequence, or (work plan over ragged
+  // lengths) of sequence `lane`
+  int L = p.dyn ? (lane < p.batch ? p.ctx_len[lane] : 0) : p.ctx_len[blockIdx.y];
   // The half's heads in processing order (grouped by k-block count): lane i
   // of the head table holds the i-th head's packed fields (staging offsets;
   // row bytes, rank, 8-bit chunks, 8-bit groups, groups, slot; fragment base;
@@ -502,9 +534,41 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   }
   const int qm = tid < nql ? p.kh[g0 + tid / G].head * G + tid % G : 0;
   L = L < 0 ? 0 : (L > p.max_ctx ? p.max_ctx : L);
-  const int t_begin = split * p.split_len;
+  // the work item: sequence b, its split, the split length S, and the slot of
+  // the item's partials
+  int b, split, S, pitem;
+  if (p.dyn) {
+    int cnt;
+    S = wave_split_plan(L, p.batch, p.k_lo, p.cap, lane, &cnt) * kStepTokens;
+    pitem = blockIdx.x;
+    // the item's sequence: a scalar walk over the sequences' split counts
+    b = -1;
+    split = pitem;
+    for (int j = 0; j < p.batch; ++j) {
+      const int cj = __builtin_amdgcn_readlane(cnt, j);
+      if (split < cj) { b = j; break; }
+      split -= cj;
+    }
+    if (b < 0) return;                      // past the last item
+    L = __builtin_amdgcn_readlane(L, b);
+  } else {
+    b = blockIdx.y;
+    split = blockIdx.x;
+    S = p.split_len;
+    pitem = b * p.n_split + split;
+  }
+  const int t_begin = split * S;
   if (t_begin >= L) return;
-  const int t_end = min(t_begin + p.split_len, L);
+  const int t_end = min(t_begin + S, L);
+  // Paged caches: lane j holds the pool page of the split's j-th page (a split
+  // of at most 8192 tokens spans at most 64 pages of at least 128 tokens).
+  const int pg_first = p.rmap.table ? t_begin >> p.rmap.shift : 0;
+  int l_page = 0;
+  if (p.rmap.table) {
+    const int pj = min(pg_first + lane, p.rmap.per_seq - 1);
+    const int pg = p.rmap.table[(int64_t)b * p.rmap.per_seq + pj];
+    l_page = pg < 0 ? 0 : (pg >= p.rmap.n_pages ? p.rmap.n_pages - 1 : pg);
+  }
   const int n_steps = (t_end - t_begin + kStepTokens - 1) / kStepTokens;
 
   const int raw_bytes = p.hg_raw_bytes[hg];
@@ -1048,7 +1112,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     if (quad == 0) red[((ct0 + c) * 16 + col) * kTokenGroups + tg] = l;
   }
   __syncthreads();
-  const int64_t pbase = ((int64_t)b * p.n_split + split) * p.n_q;
+  const int64_t pbase = (int64_t)pitem * p.n_q;
 #pragma unroll
   for (int c = 0; c < CTH; ++c) {
     if (c >= ctn) break;
@@ -1196,8 +1260,21 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   const int i = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int lane = tid & 63, w = tid >> 6;
   const int g = (int)(((int64_t)i * p.n_kv) / p.n_q);
-  int L = p.ctx_len[b];
+  // this sequence's splits: under the work plan, items first .. first + ns - 1
+  int L = p.dyn ? (lane < p.batch ? p.ctx_len[lane] : 0) : p.ctx_len[b];
   L = L < 0 ? 0 : (L > p.max_ctx ? p.max_ctx : L);
+  int ns, first;
+  if (p.dyn) {
+    int cnt;
+    wave_split_plan(L, p.batch, p.k_lo, p.cap, lane, &cnt);
+    first = 0;
+    for (int j = 0; j < b; ++j) first += __builtin_amdgcn_readlane(cnt, j);
+    ns = __builtin_amdgcn_readlane(cnt, b);
+    L = __builtin_amdgcn_readlane(L, b);
+  } else {
+    ns = (L + p.split_len - 1) / p.split_len;
+    first = b * p.n_split;
+  }
   const int64_t out_row = ((int64_t)b * p.n_q + i) * D;
   const bool to_lat = p.lat != nullptr;
   const int64_t lat_row = ((int64_t)b * p.n_q + i) * p.rv;
@@ -1213,12 +1290,11 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
     }
     return;
   }
-  const int ns = (L + p.split_len - 1) / p.split_len;
-  const float* part = p.part + ((int64_t)b * p.n_split * p.n_q + i) * p.part_stride;
+  const float* part = p.part + ((int64_t)first * p.n_q + i) * p.part_stride;
   const int64_t sstride = (int64_t)p.n_q * p.part_stride;
   // candidates of all splits, loaded ahead of the split weights
   const int n_ent = ns * kCand;
-  const float2* cand = p.cand + ((int64_t)b * p.n_split * p.n_q + i) * kCand;
+  const float2* cand = p.cand + ((int64_t)first * p.n_q + i) * kCand;
   // (every load below reads a clamped, valid address; entries beyond the
   // sequence's splits are masked where they are used)
   // (addresses are a per-lane base plus wave-uniform offsets; entries beyond
@@ -1255,7 +1331,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
 #pragma unroll
     for (int k = 0; k < kSplitsPerWave; ++k)
       pv[k] = *reinterpret_cast<const f4*>(pbase + o +
-                                           (uint32_t)min(w + 4 * k, p.n_split - 1) * sbytes);
+                                           (uint32_t)min(w + 4 * k, ns - 1) * sbytes);
   };
   f4 pv0[kSplitsPerWave];
   load_chunk(0, pv0);
@@ -1271,7 +1347,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   }
   const int r_g = p.k_rank[g];
   if (tid < 64) {                 // split weights: one wave, one split per lane
-    const int s = min(tid, p.n_split - 1);
+    const int s = min(tid, ns - 1);
     const float mv = tid < ns ? part[s * sstride + p.rv] : -INFINITY;
     const float lv = part[s * sstride + p.rv + 1];
     float m = mv;
@@ -1505,7 +1581,7 @@ static int launch_split_t(const DecodeParams& p, size_t lds, hipStream_t st) {
     if (e != hipSuccess) return (int)e;
     attr = true;
   }
-  dim3 grid(p.n_split, p.batch, p.n_hg);
+  dim3 grid(p.dyn ? p.cap : p.n_split, p.dyn ? 1 : p.batch, p.n_hg);
   hipLaunchKernelGGL(k, grid, dim3(kThreads), lds, st, p);
   return (int)hipGetLastError();
 }

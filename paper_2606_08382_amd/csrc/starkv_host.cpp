@@ -378,8 +378,40 @@ starkv_status starkv_cache_layout(const starkv_plan* plan, starkv_layout* out) {
 
 // ---------------------------------------------------------------- decode sizing
 
+// Work plan of the split pass.  Batches of up to kMaxPlanBatch sequences use the
+// device-side plan over their actual lengths: the kernels pick the split length
+// S = 128 k (k >= k_lo) as the smallest giving at most `cap` work items, one
+// compute unit's workgroup per item and head group (or more items where even
+// 8192-token splits need them).  Larger batches split every sequence alike
+// for max_ctx.
+constexpr int kComputeUnits = 256;
+constexpr int kMaxPlanBatch = 64;
+struct WorkPlan {
+  bool dyn;
+  int32_t k_lo, cap;
+};
+static WorkPlan work_plan(const starkv_plan* P, int32_t max_ctx) {
+  WorkPlan w;
+  const int64_t B = P->cfg.batch;
+  const int64_t steps = ((int64_t)max_ctx + kStepTokens - 1) / kStepTokens;
+  w.dyn = B <= kMaxPlanBatch;
+  w.k_lo = (int32_t)std::max<int64_t>(1, (steps + kMaxSplits - 1) / kMaxSplits);
+  const int64_t per_cu = std::max<int64_t>(1, kComputeUnits / P->n_hg);
+  const int64_t at_max = B * (((int64_t)max_ctx + kMaxSplitTokens - 1) / kMaxSplitTokens);
+  w.cap = (int32_t)std::max(per_cu, at_max);
+  return w;
+}
+
 int32_t starkv_decode_split_tokens(const starkv_plan* P, int32_t max_ctx) {
   if (!P || max_ctx < 1) return 0;
+  const WorkPlan wp = work_plan(P, max_ctx);
+  if (wp.dyn) {
+    // the device plan for max_ctx tokens in every sequence
+    const int64_t steps = ((int64_t)max_ctx + kStepTokens - 1) / kStepTokens;
+    for (int k = wp.k_lo; k < kMaxSplits; ++k)
+      if (P->cfg.batch * ((steps + k - 1) / k) <= wp.cap) return k * kStepTokens;
+    return kMaxSplits * kStepTokens;
+  }
   // enough splits to give every compute unit a workgroup, at most kMaxSplits
   // per sequence (the combine pass merges up to that many)
   const int64_t wgs_per_split = (int64_t)P->cfg.batch * P->n_hg;
@@ -399,19 +431,24 @@ int32_t starkv_decode_splits(const starkv_plan* P, int32_t max_ctx) {
 
 static int part_stride(const starkv_plan* P) { return P->cfg.value_rank + 4; }
 
-// Workspace: the split partials [B][splits][H_q][part_stride] fp32, then the
-// rescoring candidates [B][splits][H_q][kCand] (score, token) pairs.
+// Work items whose partials the workspace holds: the device plan's cap, or
+// every (sequence, split).
+static int64_t part_slots(const starkv_plan* P, int32_t max_ctx) {
+  const WorkPlan wp = work_plan(P, max_ctx);
+  return wp.dyn ? wp.cap : (int64_t)P->cfg.batch * starkv_decode_splits(P, max_ctx);
+}
+
+// Workspace: the split partials [items][H_q][part_stride] fp32, then the
+// rescoring candidates [items][H_q][kCand] (score, token) pairs.
 static int64_t cand_offset(const starkv_plan* P, int32_t max_ctx) {
-  const int64_t ns = starkv_decode_splits(P, max_ctx);
-  return align256((int64_t)P->cfg.batch * ns * P->cfg.n_q_heads * part_stride(P) * 4);
+  return align256(part_slots(P, max_ctx) * P->cfg.n_q_heads * part_stride(P) * 4);
 }
 
 // Then, for the absorbed output, the normalized value latents as two fp16 parts
 // [2][B][H_q * r_v].
 static int64_t lat_offset(const starkv_plan* P, int32_t max_ctx) {
-  const int64_t ns = starkv_decode_splits(P, max_ctx);
   return cand_offset(P, max_ctx) +
-         align256((int64_t)P->cfg.batch * ns * P->cfg.n_q_heads * kCand * 8);
+         align256(part_slots(P, max_ctx) * P->cfg.n_q_heads * kCand * 8);
 }
 
 size_t starkv_decode_workspace_bytes(const starkv_plan* P, int32_t max_ctx) {
@@ -426,7 +463,8 @@ static starkv_status check_common(const starkv_plan* P, int32_t max_ctx, size_t 
   if (max_ctx < 1) return fail(STARKV_ERR_INVALID_ARG, "max_ctx %d < 1", max_ctx);
   if (max_ctx > P->cfg.capacity)
     return fail(STARKV_ERR_CAPACITY, "max_ctx %d > capacity %d", max_ctx, P->cfg.capacity);
-  if (starkv_decode_split_tokens(P, max_ctx) > kMaxSplitTokens)
+  if (starkv_decode_split_tokens(P, max_ctx) > kMaxSplitTokens ||
+      (int64_t)max_ctx > (int64_t)kMaxSplits * kMaxSplitTokens)
     return fail(STARKV_ERR_UNSUPPORTED, "max_ctx %d > %d", max_ctx, kMaxSplits * kMaxSplitTokens);
   const size_t need = starkv_decode_workspace_bytes(P, max_ctx);
   if (!ws || ws_bytes < need)
@@ -484,6 +522,12 @@ starkv_status starkv_decode_split(const starkv_plan* P, const void* cache, const
   p.max_ctx = max_ctx;
   p.split_len = starkv_decode_split_tokens(P, max_ctx);
   p.n_split = starkv_decode_splits(P, max_ctx);
+  {
+    const WorkPlan wp = work_plan(P, max_ctx);
+    p.dyn = wp.dyn;
+    p.k_lo = wp.k_lo;
+    p.cap = wp.cap;
+  }
   p.q_bf16 = c.q_dtype == STARKV_DT_BF16;
   p.score_scale = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
   p.log2_theta = std::log2(c.rope_theta);
@@ -550,6 +594,13 @@ static void combine_params(const starkv_plan* P, const void* cache, const void* 
   p.max_ctx = max_ctx;
   p.split_len = starkv_decode_split_tokens(P, max_ctx);
   p.n_split = starkv_decode_splits(P, max_ctx);
+  {
+    const WorkPlan wp = work_plan(P, max_ctx);
+    p.dyn = wp.dyn;
+    p.k_lo = wp.k_lo;
+    p.cap = wp.cap;
+    if (wp.dyn) p.n_split = kMaxSplits;   // a sequence has at most this many splits
+  }
   p.part_stride = part_stride(P);
   p.out_dtype = c.out_dtype;
   p.q_bf16 = c.q_dtype == STARKV_DT_BF16;

@@ -60,6 +60,10 @@ struct DecodeParams {
   int32_t batch, n_q, n_kv, group_q;   // group_q = H_q / H_kv
   RowMap rmap;
   int32_t max_ctx, split_len, n_split;
+  // work plan over ragged lengths (dyn != 0, batch <= 64): grid.x = cap items,
+  // the split length chosen on the device from the lengths (see the kernels);
+  // otherwise grid (n_split, batch) with split_len tokens per split
+  int32_t dyn, k_lo, cap;
   int32_t q_bf16;
   float score_scale;           // log2(e)/sqrt(d)
   double log2_theta;
@@ -107,6 +111,7 @@ struct CombineParams {
   uint16_t* lat;
   int32_t batch, n_q, n_kv, head_dim, rv;
   int32_t max_ctx, split_len, n_split, part_stride;
+  int32_t dyn, k_lo, cap;      // as in DecodeParams
   int32_t out_dtype, q_bf16, qmode;
   RowMap rmap;
   float score_scale;
