@@ -735,23 +735,25 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   // the subtile rotation (16*(2*tg + s)) times the column rotation (col), and
   // the rotation by one step (kStepTokens) for the query's base position.
   {
-    const double l2t = p.log2_theta;
-    for (int i = tid; i < HALF; i += kThreads) {
-      const double om = exp2(-(2.0 * i / D) * l2t);
+    // every table entry of this thread has frequency index j = tid % HALF
+    // (kThreads is a multiple of HALF), so one fp64 exp2 serves them all
+    static_assert(kThreads % HALF == 0, "table items of a thread share j");
+    const int j = tid % HALF;
+    const double om = exp2(-(2.0 * j / D) * p.log2_theta);
+    const float omf = (float)om;
+    if (tid < HALF) {
       float ss, cs;
       sincosf((float)(kStepTokens * om), &ss, &cs);
-      rot_s[i] = make_float2(cs, ss);
+      rot_s[j] = make_float2(cs, ss);
     }
     for (int i = tid; i < 16 * HALF; i += kThreads) {
-      const int c = i / HALF, j = i % HALF;
-      const float om = (float)exp2(-(2.0 * j / D) * l2t);
+      const int c = i / HALF;
       float ss, cs;
-      sincosf((float)c * om, &ss, &cs);
+      sincosf((float)c * omf, &ss, &cs);
       rope_col[c * 65 + j] = make_float2(cs, ss);
     }
     for (int i = tid; i < 8 * HALF; i += kThreads) {
-      const int k = i / HALF, j = i % HALF;
-      const double om = exp2(-(2.0 * j / D) * l2t);
+      const int k = i / HALF;
       float ss, cs;
       sincosf((float)(16.0 * k * om), &ss, &cs);
       rope_ws[k * 64 + j] = make_float2(cs, ss);
