@@ -1243,22 +1243,30 @@ __device__ float value_latent(const CombineParams& p, int b, int t, int r) {
                         h2f(reinterpret_cast<const uint16_t*>(m + 16)[slot]));
 }
 
+// floats of the combine kernel's LDS before its shared region (kept a multiple
+// of 4 so that the region is 16-byte aligned)
+__host__ __device__ constexpr int combine_head_floats(int rv) {
+  return (rv + 64 + 3 * kRescoreMax + 8 + 3) / 4 * 4;
+}
+
 __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   extern __shared__ __align__(16) float sm[];
   const int D = p.head_dim;
   float* a = sm;                         // [rv] merged value latent
-  float* wts = sm + p.rv;                // [n_split] split weights
-  float* red = wts + p.n_split;          // [32][D] partial up-projections
-  float* c_x = red + 32 * D;             // [kRescoreMax] approximate scores
+  float* wts = a + p.rv;                 // [64] split weights (one per lane of the weight wave)
+  float* c_x = wts + 64;                 // [kRescoreMax] approximate scores
   float* c_d = c_x + kRescoreMax;        // [kRescoreMax] weight corrections
   int* c_t = reinterpret_cast<int*>(c_d + kRescoreMax);   // [kRescoreMax] tokens
-  float* lat = reinterpret_cast<float*>(c_t + kRescoreMax); // [kRescoreMax][128] key latents
-  float* misc = lat + kRescoreMax * 128; // M, L, L', unused, wave counts [4]
+  float* misc = reinterpret_cast<float*>(c_t + kRescoreMax);  // M, L, L', unused, wave counts [4]
   int* cnt = reinterpret_cast<int*>(misc + 4);
-  // [r_g][D] the head's B_k block, 16-byte aligned
-  uint16_t* bks = reinterpret_cast<uint16_t*>(
-      sm + ((reinterpret_cast<uintptr_t>(misc + 8) - reinterpret_cast<uintptr_t>(sm) + 15) / 16) * 4);
-  float* red4 = reinterpret_cast<float*>(bks + D * D);   // [4][rv] per-wave split sums
+  // One region, 16-byte aligned, serves two phases: the merge (per-wave split
+  // sums, and the rescoring's key latents and B_k block) and, once the merged
+  // latent is in `a`, the up-projection's partial sums.
+  float* uni = sm + combine_head_floats(p.rv);
+  float* red4 = uni;                                   // [4][rv] per-wave split sums
+  float* lat = red4 + 4 * p.rv;                        // [kRescoreMax][rmax] key latents
+  uint16_t* bks = reinterpret_cast<uint16_t*>(lat + kRescoreMax * p.rmax);  // [rmax][D] fp16
+  float* red = uni;                                    // [256 / (D/8)][D] partial up-projections
   const int i = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int lane = tid & 63, w = tid >> 6;
   const int g = (int)(((int64_t)i * p.n_kv) / p.n_q);
@@ -1324,24 +1332,26 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   const uint32_t sbytes = (uint32_t)sstride * 4u;
   // Value-latent partials: wave w takes splits w, w + 4, .., lane l channels
   // 4l..4l+3 of each 256-channel chunk, one 16-byte load per (split, chunk), so
-  // a chunk of all splits is 64 loads of 1 KiB per workgroup.  Chunk 0 is
+  // a chunk of all splits is 64 loads of 1 KiB per workgroup.  A wave loads its
+  // splits in batches of 8 (splits w + 32h + 4k); the first batch of chunk 0 is
   // loaded now (it does not depend on the merge weights).
-  constexpr int kSplitsPerWave = kCombineMaxSplits / 4;
+  constexpr int kSplitBatch = 8;
   const int n_chunk = (p.rv + 255) / 256;
-  auto load_chunk = [&](int ch, f4 (&pv)[kSplitsPerWave]) {
+  auto load_batch = [&](int ch, int h, f4 (&pv)[kSplitBatch]) {
     const uint32_t o = (uint32_t)min(256 * ch + 4 * lane, p.rv - 4) * 4u;
 #pragma unroll
-    for (int k = 0; k < kSplitsPerWave; ++k)
-      pv[k] = *reinterpret_cast<const f4*>(pbase + o +
-                                           (uint32_t)min(w + 4 * k, ns - 1) * sbytes);
+    for (int k = 0; k < kSplitBatch; ++k)
+      pv[k] = *reinterpret_cast<const f4*>(
+          pbase + o + (uint32_t)min(w + 32 * h + 4 * k, ns - 1) * sbytes);
   };
-  f4 pv0[kSplitsPerWave];
-  load_chunk(0, pv0);
-  u4 w0[8];
+  f4 pv0[kSplitBatch];
+  load_batch(0, 0, pv0);
+  constexpr int kUpRows = 4;             // rows of U_V per thread per round of loads
+  u4 w0[kUpRows];
   {
     const uint16_t* bl = bv + (int64_t)rg * ldb;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
+    for (int k = 0; k < kUpRows; ++k) {
       w0[k] = (u4){0, 0, 0, 0};
       if (!to_lat && rg + k * groups < p.rv)
         w0[k] = *reinterpret_cast<const u4*>(bl + (int64_t)k * groups * ldb);
@@ -1363,19 +1373,29 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   __syncthreads();
   const float M = misc[0], Lsum = misc[1];
   // weighted sums of this wave's splits, per channel, into red4[w][r]
-  auto sum_chunk = [&](int ch, const f4 (&pv)[kSplitsPerWave]) {
-    f4 acc = (f4){0, 0, 0, 0};
+  auto add_batch = [&](int h, const f4 (&pv)[kSplitBatch], f4& acc) {
 #pragma unroll
-    for (int k = 0; k < kSplitsPerWave; ++k)
-      if (w + 4 * k < ns) acc += wts[w + 4 * k] * pv[k];
+    for (int k = 0; k < kSplitBatch; ++k) {
+      const int sp = w + 32 * h + 4 * k;
+      if (sp < ns) acc += wts[sp] * pv[k];
+    }
+  };
+  for (int ch = 0; ch < n_chunk; ++ch) {
+    f4 acc = (f4){0, 0, 0, 0};
+    if (ch == 0) {
+      add_batch(0, pv0, acc);
+    } else {
+      f4 pv[kSplitBatch];
+      load_batch(ch, 0, pv);
+      add_batch(0, pv, acc);
+    }
+    if (ns > 32) {                        // splits 32 .. 63
+      f4 pv[kSplitBatch];
+      load_batch(ch, 1, pv);
+      add_batch(1, pv, acc);
+    }
     const int r = 256 * ch + 4 * lane;
     if (r < p.rv) *reinterpret_cast<f4*>(red4 + w * p.rv + r) = acc;
-  };
-  sum_chunk(0, pv0);
-  for (int ch = 1; ch < n_chunk; ++ch) {
-    f4 pv[kSplitsPerWave];
-    load_chunk(ch, pv);
-    sum_chunk(ch, pv);
   }
 
   // ---- candidate selection: share x (1 + |x|) >= tau, tau raised until at most
@@ -1386,7 +1406,6 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
     const float x = ce[k].x;
     prio[k] = (x == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(x - M) / Lsum * (1.0f + fabsf(x));
   }
-  float vsel[kRescoreMax];   // candidates' value latents of the thread's first channel
   float tau = kRescoreTau;
   int n_sel = 0;
   for (int it = 0; it < 8; ++it) {
@@ -1422,8 +1441,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
       __syncthreads();
     }
     // one round of loads for the rescoring: the KV head's up-projection block
-    // B_k (r_g x D fp16, staged in LDS), the candidates' key latents and the
-    // candidates' value latents of this thread's first channel (used by the merge)
+    // B_k (r_g x D fp16, staged in LDS) and the candidates' key latents
     const int nbk = r_g * D / 8;           // 16-byte vectors
     u4 bkv[kBkVecPerThread];
     {
@@ -1431,11 +1449,6 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
 #pragma unroll
       for (int k = 0; k < kBkVecPerThread; ++k)
         bkv[k] = src[min(tid + k * 256, nbk - 1)];
-    }
-    if (tid < p.rv) {
-#pragma unroll
-      for (int j = 0; j < kRescoreMax; ++j)
-        if (j < n_sel) vsel[j] = value_latent(p, b, c_t[j], tid);
     }
 #pragma unroll
     for (int k = 0; k < kBkVecPerThread; ++k)
@@ -1446,7 +1459,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
     const int HALF = D / 2;
     for (int it = tid; it < n_sel * r_g; it += 256) {
       const int j = it / r_g, ch = it % r_g;
-      lat[j * 128 + ch] = key_latent(p, g, b, c_t[j], ch);
+      lat[j * p.rmax + ch] = key_latent(p, g, b, c_t[j], ch);
     }
     __syncthreads();
     const uint16_t* bk = bks;
@@ -1456,7 +1469,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
       const int j = it / HALF, l = it % HALF;
       float dot = 0.0f;
       if (j < n_sel) {
-        const float* lj = lat + j * 128;
+        const float* lj = lat + j * p.rmax;
         float klo = 0.0f, khi = 0.0f;
 #pragma unroll 8
         for (int ch = 0; ch < r_g; ++ch) {
@@ -1488,15 +1501,8 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   }
   __syncthreads();
   const float inv_l = 1.0f / misc[2];
-  auto merge_channel = [&](int r, bool first) {
+  auto merge_channel = [&](int r) {
     float acc = red4[r] + red4[p.rv + r] + red4[2 * p.rv + r] + red4[3 * p.rv + r];
-    if (first) {                              // the thread's first channel: loaded above
-#pragma unroll
-      for (int j = 0; j < kRescoreMax; ++j)
-        if (j < n_sel) acc = __builtin_fmaf(c_d[j], vsel[j], acc);
-      a[r] = acc * inv_l;
-      return;
-    }
     for (int j0 = 0; j0 < n_sel; j0 += 8) {   // eight candidates' loads in flight
       float vl[8];
 #pragma unroll
@@ -1507,8 +1513,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
     }
     a[r] = acc * inv_l;
   };
-  if (tid < p.rv) merge_channel(tid, true);
-  for (int r = tid + 256; r < p.rv; r += 256) merge_channel(r, false);
+  for (int r = tid; r < p.rv; r += 256) merge_channel(r);
   __syncthreads();
   if (to_lat) {                 // absorbed output: the latents go to the product pass
     for (int r = tid; r < p.rv; r += 256) {
@@ -1522,9 +1527,9 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   // o = a . U_V^T restricted to KV head g's d columns (the reordering of Sec. 3.3):
   // thread (rg, j8) covers rows rg, rg + groups, .. and columns 8*j8..8*j8+7
   float o[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  auto up_rows = [&](int r0, const u4 (&w8)[8]) {
+  auto up_rows = [&](int r0, const u4 (&w8)[kUpRows]) {
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
+    for (int k = 0; k < kUpRows; ++k) {
       const int r = r0 + k * groups;
       if (r < p.rv) {
         const _Float16* hw = reinterpret_cast<const _Float16*>(&w8[k]);
@@ -1535,11 +1540,11 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
     }
   };
   up_rows(rg, w0);
-  for (int r0 = rg + 8 * groups; r0 < p.rv; r0 += 8 * groups) {
-    u4 w8[8];
+  for (int r0 = rg + kUpRows * groups; r0 < p.rv; r0 += kUpRows * groups) {
+    u4 w8[kUpRows];
     const uint16_t* bl = bv + (int64_t)r0 * ldb;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
+    for (int k = 0; k < kUpRows; ++k) {
       w8[k] = (u4){0, 0, 0, 0};
       if (r0 + k * groups < p.rv) w8[k] = *reinterpret_cast<const u4*>(bl + (int64_t)k * groups * ldb);
     }
@@ -1647,11 +1652,12 @@ int launch_decode_split_ntw(const DecodeParams& p, int head_dim, int qmode, int 
 
 int launch_decode_combine(const CombineParams& p, void* stream) {
   if (p.n_split > kCombineMaxSplits) return (int)hipErrorInvalidValue;
-  const size_t lds =
-      (size_t)(p.rv + p.n_split + 32 * p.head_dim + 3 * kRescoreMax + kRescoreMax * 128 + 8 + 4) *
-          sizeof(float) +
-      (size_t)p.head_dim * p.head_dim * sizeof(uint16_t) +  // B_k block (rank <= head_dim)
-      (size_t)4 * p.rv * sizeof(float);                      // per-wave split sums
+  // the shared region: the merge phase (split sums, rescoring latents, B_k
+  // block) or the up-projection's 256 / (D/8) rows of D partial sums
+  const size_t merge = (size_t)4 * p.rv + (size_t)kRescoreMax * p.rmax + (size_t)p.rmax * p.head_dim / 2;
+  const size_t upproj = (size_t)256 / (p.head_dim / 8) * p.head_dim;
+  const size_t lds = ((size_t)combine_head_floats(p.rv) + (merge > upproj ? merge : upproj)) *
+                     sizeof(float);
   static bool attr = false;
   if (!attr) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(decode_combine_kernel),

@@ -616,6 +616,7 @@ static void combine_params(const starkv_plan* P, const void* cache, const void* 
     p.k_ng[g] = L.key_groups[g];
     p.k_rb[g] = L.key_row_bytes[g];
     p.k_bkrow[g] = P->bk_row[g];
+    p.rmax = std::max(p.rmax, P->key_rank[g]);
   }
   p.v_code_off = L.value_code_offset;
   p.v_meta_off = L.value_meta_offset;

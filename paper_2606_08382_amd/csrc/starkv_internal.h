@@ -113,6 +113,7 @@ struct CombineParams {
   int32_t max_ctx, split_len, n_split, part_stride;
   int32_t dyn, k_lo, cap;      // as in DecodeParams
   int32_t out_dtype, q_bf16, qmode;
+  int32_t rmax;                // largest key rank (sizes the rescoring buffers)
   RowMap rmap;
   float score_scale;
   double log2_theta;
