@@ -36,10 +36,12 @@ def _ocfg(w, inp, layer):
 
 @pytest.mark.parametrize("name,ctx,batch,P,ragged", [
     ("c3", 1100, 2, 128, None), ("c4", 900, 6, 256, (1, 900)), ("c3q", 700, 2, 512, None),
-    ("c1", 1024, None, 128, None), ("c5", 600, 2, 8192, None), ("c2", 1500, 3, 1024, (200, 1500))])
+    ("c1", 1024, None, 128, None), ("c5", 600, 2, 8192, None), ("c2", 1500, 3, 1024, (200, 1500)),
+    ("c1", 300, 70, 128, (5, 300))])
 def test_paged_pool_and_decode_match_oracle(name, ctx, batch, P, ragged):
     """Sequences scattered over a shuffled pool with spare pages; appends in chunks that cross
-    page boundaries; the whole pool bit-exact, decode and the absorbed output in tolerance."""
+    page boundaries; the whole pool bit-exact, decode and the absorbed output in tolerance.
+    More than 64 sequences take the per-sequence split grid instead of the work plan."""
     w = small(name, ctx, batch, ragged=ragged)
     inp = synth.generate(w, peaked=1)
     rng = np.random.default_rng(100 + P)

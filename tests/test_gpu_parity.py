@@ -97,6 +97,15 @@ def test_ragged_lengths_and_partial_splits():
     _run_case(w, inp)
 
 
+def test_work_plan_with_one_long_sequence_among_empty_ones():
+    """The device work plan with most sequences empty: every item goes to the one long
+    sequence (its splits shrink to fill the chip), the others get zero outputs."""
+    w = small("c3", ctx=3000, batch=6)
+    inp = synth.generate(w)
+    layer, got, _ = _run_case(w, inp, ctx_len=[0, 0, 2999, 0, 1, 0])
+    assert np.all(got[[0, 1, 3, 5]] == 0.0)
+
+
 def test_zero_length_and_clamped_lengths():
     w = small("c3", ctx=600, batch=3)
     inp = synth.generate(w)
