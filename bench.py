@@ -221,6 +221,7 @@ def main():
         ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
     absorbed = None if args.no_absorbed else time_absorbed(args, w, inp, layers, q, Bk, ctx, x,
                                                            pos_new, A, stream)
+    prefill = time_prefill(args, w, inp, layers[0], A, stream) if w.append_tokens > 1 else None
     tokens = int(inp.ctx_len.sum())
     layout = S.starkv_cache_layout(layers[0].plan)
     per_token = (sum(layout.key_row_bytes[g] + 4 * layout.key_groups[g]
@@ -279,6 +280,8 @@ def main():
     }
     if absorbed is not None:
         result["absorbed_output"] = absorbed
+    if prefill is not None:
+        result["prefill"] = prefill
     if tsum is not None:
         result["roofline"]["traffic_detail"] = {
             k: tsum[k] for k in ("fetch_bytes_per_launch", "write_bytes_per_launch",
@@ -350,6 +353,41 @@ def time_absorbed(args, w, inp, layers, q, Bk, ctx, x, pos_new, A, stream):
             "tokens_per_s": (B / (ms_step / 1e3)) if ms_step else None,
             "note": "append + split + merge to normalized latents + product with W'_out; "
                     "the output is the attention block's [B][d_out] (after the output projection)"}
+
+
+def time_prefill(args, w, inp, layer, A, stream):
+    """The workload's prefill append (w.append_tokens tokens per sequence from bf16 hidden
+    states): the down-projection GEMM (bf16 MFMA, fp32 accumulation) and the pack, timed with
+    HIP events on the launch stream.  It writes rows 0 .. n-1 of one layer's cache, after the
+    decode timing."""
+    import torch
+    from paper_2606_08382_amd import synth
+    from paper_2606_08382_amd.device import to_dev
+    n = w.append_tokens
+    rng = np.random.default_rng(w.seed + 31)
+    x = to_dev(synth.f32_to_bf16_bits(rng.standard_normal((w.batch, n, w.d_model),
+                                                         dtype=np.float32)))
+    pos = torch.zeros(w.batch, dtype=torch.int32, device="cuda")
+    reps = max(3, min(args.steps, 10))
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    layer.append(x, pos, A_all=A)            # warm-up (and workspace sizing)
+    torch.cuda.synchronize()
+    for a, b in ev:
+        a.record(stream)
+        layer.append(x, pos, A_all=A)
+        b.record(stream)
+    torch.cuda.synchronize()
+    us = float(np.median([a.elapsed_time(b) * 1e3 for a, b in ev]))
+    M, N, K = w.batch * n, inp.width, w.d_model
+    flops = 2.0 * M * N * K
+    tf = flops / (us * 1e-6) / 1e12
+    log(f"prefill: {M} rows x {N} x {K}: {us:.1f} us (down-projection and pack), {tf:.0f} TFLOP/s")
+    return {"tokens": M, "gemm": [M, N, K], "us": us, "flops": flops, "tflops": tf,
+            "peak_tflops": MFMA_F16_PEAK_TFLOPS, "frac": tf / MFMA_F16_PEAK_TFLOPS,
+            "note": "append of the prefill from bf16 hidden states: down-projection GEMM (bf16 "
+                    "operands, fp32 accumulation) plus the pack of every token; median of HIP "
+                    "events; frac against the dense bf16 MFMA peak"}
 
 
 _fill_plans = {}

@@ -385,6 +385,106 @@ __global__ __launch_bounds__(256) void downproj_small_kernel(DownprojParams p) {
   }
 }
 
+// ------------------------------------------------------------------ prefill down-projection
+// Large appends (a prefill): Z = X . A_all as one GEMM.  A_all [K][N] is first
+// transposed into the workspace (At [N][K]), so that both operands are
+// k-contiguous; the GEMM accumulates all of K in fp32 on
+// v_mfma_f32_16x16x32_bf16 and writes the fp16 latents directly (one rounding,
+// as the split-k path's pack does).  Tiles of 128 x 128 per workgroup (four
+// waves of 64 x 64), k steps of 64 staged in LDS with a padded row (conflict-free
+// 16-byte reads), double buffered: the next step's global loads are in flight
+// while the current step's MFMAs run.
+constexpr int GM = 128, GN = 128, GK = 64, GKP = GK + 8;
+
+__global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* a, uint16_t* at,
+                                                             int K, int N) {
+  __shared__ uint16_t t[64][66];
+  const int k0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
+  for (int i = threadIdx.x; i < 64 * 64; i += 256) {
+    const int r = i / 64, c = i % 64;             // r: k, c: n (coalesced reads)
+    const int k = k0 + r, n = n0 + c;
+    t[r][c] = (k < K && n < N) ? a[(int64_t)k * N + n] : (uint16_t)0;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < 64 * 64; i += 256) {
+    const int r = i / 64, c = i % 64;             // r: n, c: k (coalesced writes)
+    const int n = n0 + r, k = k0 + c;
+    if (n < N && k < K) at[(int64_t)n * K + k] = t[c][r];
+  }
+}
+
+__global__ __launch_bounds__(256) void gemm_bf16_nt_kernel(DownprojParams p) {
+  __shared__ __align__(16) uint16_t xs[2][GM * GKP];
+  __shared__ __align__(16) uint16_t bs[2][GN * GKP];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int n0 = blockIdx.x * GN, m0 = blockIdx.y * GM;
+  const int wm = (w >> 1) * 64, wn = (w & 1) * 64;
+  const int M = p.m, N = p.n, K = p.k;            // K is a multiple of GK (checked by the host)
+  // global -> register staging: chunk c = tid + 256 i (i < 4) of a 128 x 64 tile is
+  // row c / 8, k chunk c % 8 (16 bytes); rows past M or N read the last row
+  u4 rx[4], rb[4];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
+      const int m = min(m0 + row, M - 1), n = min(n0 + row, N - 1);
+      rx[i] = *reinterpret_cast<const u4*>(p.x + (int64_t)m * K + k0 + 8 * kc);
+      rb[i] = *reinterpret_cast<const u4*>(p.at + (int64_t)n * K + k0 + 8 * kc);
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
+      *reinterpret_cast<u4*>(&xs[buf][row * GKP + 8 * kc]) = rx[i];
+      *reinterpret_cast<u4*>(&bs[buf][row * GKP + 8 * kc]) = rb[i];
+    }
+  };
+  f4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = (f4){0, 0, 0, 0};
+  const int nk = K / GK;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  const int fr = lane & 15, fk = 8 * (lane >> 4);
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) gload((kt + 1) * GK);
+#pragma unroll
+    for (int kk = 0; kk < GK; kk += 32) {
+      b8 af[4], bf[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        af[i] = *reinterpret_cast<const b8*>(&xs[buf][(wm + 16 * i + fr) * GKP + kk + fk]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        bf[j] = *reinterpret_cast<const b8*>(&bs[buf][(wn + 16 * j + fr) * GKP + kk + fk]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < nk) sstore(buf ^ 1);
+    __syncthreads();
+  }
+  // C tile (16 x 16): lane holds rows 4*(lane/16)+e of column lane%16
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int m = m0 + wm + 16 * i + 4 * (lane >> 4) + e;
+        const int n = n0 + wn + 16 * j + fr;
+        if (m < M && n < N)
+          p.lat[(int64_t)m * N + n] = __builtin_bit_cast(uint16_t, (_Float16)acc[i][j][e]);
+      }
+}
+
 // ------------------------------------------------------------------ launchers
 int launch_append_pack(const AppendParams& p, void* stream) {
   const int64_t waves = (int64_t)p.batch * p.n_new * p.n_items;
@@ -394,6 +494,15 @@ int launch_append_pack(const AppendParams& p, void* stream) {
 }
 
 int launch_downproj(const DownprojParams& p, void* stream) {
+  if (p.at) {                       // the prefill GEMM: transpose A_all, then one pass over K
+    if (p.k % GK) return (int)hipErrorInvalidValue;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipLaunchKernelGGL(transpose_bf16_kernel, dim3((p.n + 63) / 64, (p.k + 63) / 64), dim3(256), 0,
+                       st, p.a, p.at, p.k, p.n);
+    hipLaunchKernelGGL(gemm_bf16_nt_kernel, dim3((p.n + GN - 1) / GN, (p.m + GM - 1) / GM),
+                       dim3(256), 0, st, p);
+    return (int)hipGetLastError();
+  }
   if (p.m <= kSmallM) {
     dim3 grid((p.n + kSmallCols - 1) / kSmallCols, p.k_split);
     const size_t lds = (size_t)16 * p.m * kSmallCols * sizeof(float);

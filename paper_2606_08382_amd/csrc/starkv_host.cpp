@@ -713,11 +713,21 @@ static void downproj_shape(const starkv_plan* P, int32_t n_new, int* k_split, in
   *k_split = (K + chunk - 1) / chunk;
 }
 
+// Appends of many tokens (a prefill) run the down-projection as one GEMM over
+// all of K, with A_all transposed into the workspace.
+static bool gemm_path(const starkv_plan* P, int32_t n_new) {
+  return (int64_t)P->cfg.batch * n_new >= kGemmMinM && P->cfg.d_model % 64 == 0;
+}
+
+// Workspace: the fp16 latents [B*n_new][width], then either the split-k fp32
+// partials or (prefill GEMM) A_all transposed, [width][d_model] bf16.
 size_t starkv_append_workspace_bytes(const starkv_plan* P, int32_t n_new) {
   if (!P || n_new < 1 || P->cfg.d_model == 0) return 0;
+  const int64_t mn = (int64_t)P->cfg.batch * n_new * P->width;
+  if (gemm_path(P, n_new))
+    return (size_t)(align256(mn * 2) + align256((int64_t)P->width * P->cfg.d_model * 2));
   int ks, kc;
   downproj_shape(P, n_new, &ks, &kc);
-  const int64_t mn = (int64_t)P->cfg.batch * n_new * P->width;
   return (size_t)(align256(mn * 2) + align256((int64_t)ks * mn * 4));
 }
 
@@ -749,10 +759,15 @@ starkv_status starkv_append(const starkv_plan* P, void* cache, const void* x_or_
     downproj_shape(P, n_new, &ks, &kc);
     const int64_t mn = (int64_t)c.batch * n_new * P->width;
     DownprojParams d;
+    std::memset(&d, 0, sizeof(d));
     d.x = static_cast<const uint16_t*>(x_or_latents);
     d.a = static_cast<const uint16_t*>(A_all);
     d.lat = static_cast<uint16_t*>(ws);
-    d.partial = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + align256(mn * 2));
+    const bool gemm = gemm_path(P, n_new);
+    if (gemm)
+      d.at = reinterpret_cast<uint16_t*>(static_cast<uint8_t*>(ws) + align256(mn * 2));
+    else
+      d.partial = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + align256(mn * 2));
     d.m = c.batch * n_new;
     d.n = P->width;
     d.k = c.d_model;
@@ -761,10 +776,14 @@ starkv_status starkv_append(const starkv_plan* P, void* cache, const void* x_or_
     d.x_bf16 = 1;
     starkv_status st = hip_status(launch_downproj(d, static_cast<void*>(stream)), "downproj launch");
     if (st != STARKV_OK) return st;
-    lat = nullptr;
-    partial = d.partial;
-    lat_out = d.lat;
-    k_split = ks;
+    if (gemm) {                 // the latents are final: the pack reads them
+      lat = d.lat;
+    } else {
+      lat = nullptr;
+      partial = d.partial;
+      lat_out = d.lat;
+      k_split = ks;
+    }
   } else if (reinterpret_cast<uintptr_t>(x_or_latents) % 2) {
     return fail(STARKV_ERR_ALIGNMENT, "latents not 2-byte aligned");
   }

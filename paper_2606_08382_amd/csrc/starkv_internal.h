@@ -161,6 +161,8 @@ struct AppendParams {
 struct DownprojParams {
   const uint16_t* x;           // [M][K] bf16 or fp16
   const uint16_t* a;           // [K][N] bf16
+  uint16_t* at;                // non-NULL: the prefill GEMM, A transposed here ([N][K] bf16)
+                               // and the latents written directly (no partials)
   float* partial;              // [ksplit][M][N]
   uint16_t* lat;               // [M][N] fp16
   int32_t m, n, k, k_split, k_chunk;
@@ -178,6 +180,8 @@ int launch_append_pack(const AppendParams& p, void* stream);
 // rows (B * n_new) up to which the down-projection streams A_all with the
 // small-M kernel: k blocks of 64 rows, one fp32 partial per block
 constexpr int kSmallM = 7;
+// rows from which (with d_model a multiple of 64) it is one GEMM over all of K
+constexpr int kGemmMinM = 512;
 int launch_downproj(const DownprojParams& p, void* stream);
 
 }  // namespace starkv
