@@ -87,59 +87,21 @@ __device__ __forceinline__ float wave_max32(float v) {
   return v;
 }
 
-__global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
-  const int lane = threadIdx.x & 63;
-  const int wid = blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
-  const int n_tok = p.batch * p.n_new;
-  if (wid >= n_tok * p.n_items) return;
-  const int tok = wid / p.n_items, item = wid % p.n_items;
-  const int b = tok / p.n_new, j = tok % p.n_new;
-  const int t = p.pos[b] + j;
-  const int bl = p.item_block[item], gi = p.item_group[item];
-  const int r = p.rank[bl], ro = p.ro[bl];
-  const bool is_v = (bl == p.n_kv);
-  // bits of the outlier (hb) and inlier (lb) regions
-  const int hb = p.qmode == STARKV_Q_MIX8_4 ? 8 : 4;
-  const int lb = p.qmode == STARKV_Q_MIX4_3 ? 3 : 4;
-  int c0, n, bits;
-  if (p.qmode == STARKV_Q_F16) {
-    c0 = 32 * gi; n = min(32, r - c0); bits = 16;
-  } else {
-    const int ngo = (ro + 31) / 32;
-    if (gi < ngo) { c0 = 32 * gi; n = min(32, ro - c0); bits = hb; }
-    else { c0 = ro + 32 * (gi - ngo); n = min(32, r - c0); bits = lb; }
-  }
-  const bool on = lane < n;
-  const int c = c0 + lane;
-  const int64_t li = (int64_t)tok * p.width + p.lat_off[bl] + c;
-  uint16_t xb = 0;
-  if (on) {
-    if (p.partial) {
-      // the split-k partial sums in a fixed order, up to 64 loads in flight
-      const int64_t mn = (int64_t)n_tok * p.width;
-      float acc = 0.0f;
-      int k = 0;
-      for (; k + 64 <= p.k_split; k += 64) {
-        float v[64];
-#pragma unroll
-        for (int u = 0; u < 64; ++u) v[u] = p.partial[(k + u) * mn + li];
-#pragma unroll
-        for (int u = 0; u < 64; ++u) acc += v[u];
-      }
-      for (; k + 16 <= p.k_split; k += 16) {
-        float v[16];
-#pragma unroll
-        for (int u = 0; u < 16; ++u) v[u] = p.partial[(k + u) * mn + li];
-#pragma unroll
-        for (int u = 0; u < 16; ++u) acc += v[u];
-      }
-      for (; k < p.k_split; ++k) acc += p.partial[k * mn + li];
-      xb = __builtin_bit_cast(uint16_t, (_Float16)acc);
-      p.lat_out[li] = xb;
-    } else {
-      xb = p.lat[li];
-    }
-  }
+// PARTIAL: the latents are summed here from the down-projection's split-k
+// partials (decode-sized appends); otherwise they are read as fp16.  Two
+// instances, so that the large prefill pack keeps a small register footprint.
+// Quantize and store one token's values of one group (lane i: channel c0 + i).
+struct PackGroup {
+  int bl, gi, c0, n, bits, ro, hb, lb, ngr, rb;
+  bool is_v;
+};
+
+__device__ __forceinline__ void pack_token(const AppendParams& p, const PackGroup& G, int lane,
+                                           int b, int t, uint16_t xb) {
+  const int bl = G.bl, gi = G.gi, bits = G.bits, ro = G.ro, hb = G.hb, lb = G.lb;
+  const bool is_v = G.is_v;
+  const bool on = lane < G.n;
+  const int c = G.c0 + lane;
   if (t < 0 || t >= p.capacity) return;     // rows outside the cache are dropped
   if (p.rmap.table) {                        // and rows on pages outside the pool
     const int pg = p.rmap.table[(int64_t)b * p.rmap.per_seq + (t >> p.rmap.shift)];
@@ -147,8 +109,8 @@ __global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
   }
   uint8_t* code_plane = p.cache + p.code_off[bl];
   uint8_t* meta_plane = p.cache + p.meta_off[bl];
-  const int rb = p.row_bytes[bl];
-  const int ngr = p.ng[bl];
+  const int rb = G.rb;
+  const int ngr = G.ngr;
   const int64_t row = cache_row(p.rmap, b, t);
   const int64_t kblk = row / 16;
   const int tau = t % 16;
@@ -245,6 +207,83 @@ __global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
       m[0] = s16;
       m[8] = z16;
     }
+  }
+}
+
+// PARTIAL: the latents are summed here from the down-projection's split-k
+// partials (decode-sized appends, one token per wave); otherwise they are read
+// as fp16 and a wave takes TPW tokens of one group, their loads issued together.
+// Two instances, so that the large prefill pack keeps a small register
+// footprint and several tokens' latency chains overlap.
+template <bool PARTIAL, int TPW>
+__global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
+  const int lane = threadIdx.x & 63;
+  const int wid = blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
+  const int n_tok = p.batch * p.n_new;
+  const int n_tb = (n_tok + TPW - 1) / TPW;
+  if (wid >= n_tb * p.n_items) return;
+  const int tb = wid / p.n_items, item = wid % p.n_items;
+  PackGroup G;
+  G.bl = p.item_block[item];
+  G.gi = p.item_group[item];
+  const int r = p.rank[G.bl];
+  G.ro = p.ro[G.bl];
+  G.is_v = (G.bl == p.n_kv);
+  G.ngr = p.ng[G.bl];
+  G.rb = p.row_bytes[G.bl];
+  // bits of the outlier (hb) and inlier (lb) regions
+  G.hb = p.qmode == STARKV_Q_MIX8_4 ? 8 : 4;
+  G.lb = p.qmode == STARKV_Q_MIX4_3 ? 3 : 4;
+  if (p.qmode == STARKV_Q_F16) {
+    G.c0 = 32 * G.gi; G.n = min(32, r - G.c0); G.bits = 16;
+  } else {
+    const int ngo = (G.ro + 31) / 32;
+    if (G.gi < ngo) { G.c0 = 32 * G.gi; G.n = min(32, G.ro - G.c0); G.bits = G.hb; }
+    else { G.c0 = G.ro + 32 * (G.gi - ngo); G.n = min(32, r - G.c0); G.bits = G.lb; }
+  }
+  const bool on = lane < G.n;
+  const int c = G.c0 + lane;
+  uint16_t xb[TPW];
+  int pos[TPW];
+#pragma unroll
+  for (int i = 0; i < TPW; ++i) {
+    const int tok = tb * TPW + i;
+    xb[i] = 0;
+    pos[i] = tok < n_tok ? p.pos[tok / p.n_new] : 0;
+    if (!on || tok >= n_tok) continue;
+    const int64_t li = (int64_t)tok * p.width + p.lat_off[G.bl] + c;
+    if (PARTIAL) {
+      // the split-k partial sums in a fixed order, up to 64 loads in flight
+      const int64_t mn = (int64_t)n_tok * p.width;
+      float acc = 0.0f;
+      int k = 0;
+      for (; k + 64 <= p.k_split; k += 64) {
+        float v[64];
+#pragma unroll
+        for (int u = 0; u < 64; ++u) v[u] = p.partial[(k + u) * mn + li];
+#pragma unroll
+        for (int u = 0; u < 64; ++u) acc += v[u];
+      }
+      for (; k + 16 <= p.k_split; k += 16) {
+        float v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) v[u] = p.partial[(k + u) * mn + li];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) acc += v[u];
+      }
+      for (; k < p.k_split; ++k) acc += p.partial[k * mn + li];
+      xb[i] = __builtin_bit_cast(uint16_t, (_Float16)acc);
+      p.lat_out[li] = xb[i];
+    } else {
+      xb[i] = p.lat[li];
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < TPW; ++i) {
+    const int tok = tb * TPW + i;
+    if (tok >= n_tok) break;
+    const int b = tok / p.n_new, j = tok % p.n_new;
+    pack_token(p, G, lane, b, pos[i] + j, xb[i]);
   }
 }
 
@@ -487,9 +526,14 @@ __global__ __launch_bounds__(256) void gemm_bf16_nt_kernel(DownprojParams p) {
 
 // ------------------------------------------------------------------ launchers
 int launch_append_pack(const AppendParams& p, void* stream) {
-  const int64_t waves = (int64_t)p.batch * p.n_new * p.n_items;
+  constexpr int kTpw = 4;            // tokens per wave without partials
+  const int64_t n_tok = (int64_t)p.batch * p.n_new;
+  const int64_t waves = (p.partial ? n_tok : (n_tok + kTpw - 1) / kTpw) * p.n_items;
   dim3 grid((unsigned)((waves + 3) / 4));
-  hipLaunchKernelGGL(pack_kernel, grid, dim3(256), 0, static_cast<hipStream_t>(stream), p);
+  if (p.partial)
+    hipLaunchKernelGGL((pack_kernel<true, 1>), grid, dim3(256), 0, static_cast<hipStream_t>(stream), p);
+  else
+    hipLaunchKernelGGL((pack_kernel<false, kTpw>), grid, dim3(256), 0, static_cast<hipStream_t>(stream), p);
   return (int)hipGetLastError();
 }
 
