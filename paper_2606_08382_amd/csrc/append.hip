@@ -429,11 +429,12 @@ __global__ __launch_bounds__(256) void downproj_small_kernel(DownprojParams p) {
 // transposed into the workspace (At [N][K]), so that both operands are
 // k-contiguous; the GEMM accumulates all of K in fp32 on
 // v_mfma_f32_16x16x32_bf16 and writes the fp16 latents directly (one rounding,
-// as the split-k path's pack does).  Tiles of 128 x 128 per workgroup (four
-// waves of 64 x 64), k steps of 64 staged in LDS with a padded row (conflict-free
-// 16-byte reads), double buffered: the next step's global loads are in flight
-// while the current step's MFMAs run.
-constexpr int GM = 128, GN = 128, GK = 64, GKP = GK + 8;
+// as the split-k path's pack does).  Tiles of 128 x GN per workgroup (four
+// waves of 64 x GN/2; GN = 128 or 96, whichever leaves fewer idle slots in the
+// last round of tiles), k steps of 64 staged in LDS with a padded row
+// (conflict-free 16-byte reads), double buffered: the next step's global loads
+// are in flight while the current step's MFMAs run.
+constexpr int GM = 128, GK = 64, GKP = GK + 8;
 
 __global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* a, uint16_t* at,
                                                              int K, int N) {
@@ -452,22 +453,30 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* a, 
   }
 }
 
+template <int GN>
 __global__ __launch_bounds__(256) void gemm_bf16_nt_kernel(DownprojParams p) {
+  constexpr int NT = GN / 32;                     // 16-column tiles per wave
+  constexpr int NB = GN * GK / 8 / 256;           // 16-byte chunks of the B tile per thread
   __shared__ __align__(16) uint16_t xs[2][GM * GKP];
   __shared__ __align__(16) uint16_t bs[2][GN * GKP];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int n0 = blockIdx.x * GN, m0 = blockIdx.y * GM;
-  const int wm = (w >> 1) * 64, wn = (w & 1) * 64;
+  const int wm = (w >> 1) * 64, wn = (w & 1) * (GN / 2);
   const int M = p.m, N = p.n, K = p.k;            // K is a multiple of GK (checked by the host)
-  // global -> register staging: chunk c = tid + 256 i (i < 4) of a 128 x 64 tile is
+  // global -> register staging: chunk c = tid + 256 i of a (rows x 64) tile is
   // row c / 8, k chunk c % 8 (16 bytes); rows past M or N read the last row
-  u4 rx[4], rb[4];
+  u4 rx[4], rb[NB];
   auto gload = [&](int k0) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
-      const int m = min(m0 + row, M - 1), n = min(n0 + row, N - 1);
+      const int m = min(m0 + row, M - 1);
       rx[i] = *reinterpret_cast<const u4*>(p.x + (int64_t)m * K + k0 + 8 * kc);
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
+      const int n = min(n0 + row, N - 1);
       rb[i] = *reinterpret_cast<const u4*>(p.at + (int64_t)n * K + k0 + 8 * kc);
     }
   };
@@ -476,14 +485,18 @@ __global__ __launch_bounds__(256) void gemm_bf16_nt_kernel(DownprojParams p) {
     for (int i = 0; i < 4; ++i) {
       const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
       *reinterpret_cast<u4*>(&xs[buf][row * GKP + 8 * kc]) = rx[i];
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
       *reinterpret_cast<u4*>(&bs[buf][row * GKP + 8 * kc]) = rb[i];
     }
   };
-  f4 acc[4][4];
+  f4 acc[4][NT];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = (f4){0, 0, 0, 0};
+    for (int j = 0; j < NT; ++j) acc[i][j] = (f4){0, 0, 0, 0};
   const int nk = K / GK;
   gload(0);
   sstore(0);
@@ -494,17 +507,17 @@ __global__ __launch_bounds__(256) void gemm_bf16_nt_kernel(DownprojParams p) {
     if (kt + 1 < nk) gload((kt + 1) * GK);
 #pragma unroll
     for (int kk = 0; kk < GK; kk += 32) {
-      b8 af[4], bf[4];
+      b8 af[4], bf[NT];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         af[i] = *reinterpret_cast<const b8*>(&xs[buf][(wm + 16 * i + fr) * GKP + kk + fk]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < NT; ++j)
         bf[j] = *reinterpret_cast<const b8*>(&bs[buf][(wn + 16 * j + fr) * GKP + kk + fk]);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < NT; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
     }
     if (kt + 1 < nk) sstore(buf ^ 1);
@@ -514,7 +527,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_nt_kernel(DownprojParams p) {
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < NT; ++j)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int m = m0 + wm + 16 * i + 4 * (lane >> 4) + e;
@@ -543,8 +556,16 @@ int launch_downproj(const DownprojParams& p, void* stream) {
     hipStream_t st = static_cast<hipStream_t>(stream);
     hipLaunchKernelGGL(transpose_bf16_kernel, dim3((p.n + 63) / 64, (p.k + 63) / 64), dim3(256), 0,
                        st, p.a, p.at, p.k, p.n);
-    hipLaunchKernelGGL(gemm_bf16_nt_kernel, dim3((p.n + GN - 1) / GN, (p.m + GM - 1) / GM),
-                       dim3(256), 0, st, p);
+    // the tile width whose last round of tiles (two workgroups per CU) leaves
+    // the fewest idle slots; time ~ rounds x tile width
+    const int64_t mt = (p.m + GM - 1) / GM;
+    const int64_t t128 = mt * ((p.n + 127) / 128), t96 = mt * ((p.n + 95) / 96);
+    const int64_t slots = 2 * 256;
+    const bool use96 = ((t96 + slots - 1) / slots) * 96 < ((t128 + slots - 1) / slots) * 128;
+    if (use96)
+      hipLaunchKernelGGL(gemm_bf16_nt_kernel<96>, dim3((p.n + 95) / 96, mt), dim3(256), 0, st, p);
+    else
+      hipLaunchKernelGGL(gemm_bf16_nt_kernel<128>, dim3((p.n + 127) / 128, mt), dim3(256), 0, st, p);
     return (int)hipGetLastError();
   }
   if (p.m <= kSmallM) {

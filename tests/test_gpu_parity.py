@@ -161,12 +161,14 @@ def test_incremental_appends_bit_exact(name):
 
 @pytest.mark.parametrize("name,n_new,d_model", [("c4", 1, 4096), ("c3", 1, 4096), ("c5", 96, 1024),
                                                  ("c3q", 1, 4096), ("c5q", 96, 1024),
-                                                 ("c5", 512, 1024), ("c3q", 300, 2048)])
+                                                 ("c5", 512, 1024), ("c3q", 300, 2048),
+                                                 ("c3", 2816, 64)])
 def test_append_from_hidden_states(name, n_new, d_model):
     """Down-projection then quantization: latents within 1 fp16 ulp of the oracle's fp64
     product plus the fp32 accumulation bound (which only matters where the sum cancels to
     a tiny latent); codes bit-exact when the oracle re-quantizes the GPU's fp16 latents.
-    512 and more rows (the last two cases) take the prefill GEMM."""
+    512 and more rows (the last three cases) take the prefill GEMM, with 96-column tiles
+    and (11264 rows x 512) with 128-column tiles."""
     w = small(name, ctx=256, batch=min(synth.WORKLOADS[name].batch, 4))
     w = w.with_(d_model=d_model)
     inp = synth.generate(w, with_hidden=True, n_hidden_tokens=n_new)
