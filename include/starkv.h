@@ -183,7 +183,9 @@ size_t        starkv_cache_bytes(const starkv_plan* plan);
 starkv_status starkv_cache_layout(const starkv_plan* plan, starkv_layout* out);
 
 /* Workspace sizes (bytes).  Append: the fp16 latents of the new tokens plus, when
- * d_model > 0, the down-projection's fp32 partial sums.  Decode: the split
+ * d_model > 0, the down-projection's fp32 partial sums (or, for 512 and more new
+ * rows B*n_new with d_model a multiple of 64, A_all transposed for the prefill
+ * GEMM).  Decode: the split
  * partials for contexts up to max_ctx, and the normalized value latents that
  * the absorbed output reads (the same size serves both decode entry points). */
 size_t        starkv_append_workspace_bytes(const starkv_plan* plan, int32_t n_new);
@@ -285,8 +287,12 @@ starkv_status starkv_decode_combine_absorbed(const starkv_plan* plan, const void
                                              int32_t max_ctx, void* out, void* ws,
                                              size_t ws_bytes, starkv_stream_t stream);
 
-/* Number of context splits used for max_ctx (tokens per split =
- * starkv_decode_split_tokens); informative. */
+/* Number of context splits and tokens per split for max_ctx tokens in every
+ * sequence; informative.  With up to 64 sequences the kernels choose the split
+ * length on the device from the actual lengths (the smallest multiple of 128
+ * tokens giving at most one work item per compute unit, at most 64 splits of at
+ * most 8192 tokens per sequence); these functions report that plan for equal
+ * lengths of max_ctx. */
 int32_t       starkv_decode_splits(const starkv_plan* plan, int32_t max_ctx);
 int32_t       starkv_decode_split_tokens(const starkv_plan* plan, int32_t max_ctx);
 
