@@ -126,8 +126,8 @@ def main():
                     help="skip the step variant with the weight-absorbed output")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(decode attention shards by batch or context; see the design notes).",
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(decode attention would shard by sequence or by context range).",
               file=sys.stderr)
         sys.exit(2)
 
