@@ -429,12 +429,14 @@ __global__ __launch_bounds__(256) void downproj_small_kernel(DownprojParams p) {
 // transposed into the workspace (At [N][K]), so that both operands are
 // k-contiguous; the GEMM accumulates all of K in fp32 on
 // v_mfma_f32_16x16x32_bf16 and writes the fp16 latents directly (one rounding,
-// as the split-k path's pack does).  Tiles of 128 x GN per workgroup (four
-// waves of 64 x GN/2; GN = 128 or 96, whichever leaves fewer idle slots in the
-// last round of tiles), k steps of 64 staged in LDS with a padded row
-// (conflict-free 16-byte reads), double buffered: the next step's global loads
-// are in flight while the current step's MFMAs run.
-constexpr int GM = 128, GK = 64, GKP = GK + 8;
+// as the split-k path's pack does).  A workgroup of WMW x WNW waves computes a
+// (64 WMW) x (TN WNW) tile, each wave 64 x TN; k steps of 64 are staged in LDS
+// with a padded row (conflict-free 16-byte reads), double buffered: the next
+// step's global loads are in flight while the current step's MFMAs run.  Large
+// problems take 256 x 192 tiles of eight 64 x 96 waves (LDS traffic per flop a
+// third lower than with 64 x 48 waves), smaller ones 128 x 96 tiles of four
+// waves.
+constexpr int GK = 64, GKP = GK + 8;
 
 __global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* a, uint16_t* at,
                                                              int K, int N) {
@@ -453,42 +455,46 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* a, 
   }
 }
 
-template <int GN>
-__global__ __launch_bounds__(256) void gemm_bf16_nt_kernel(DownprojParams p) {
-  constexpr int NT = GN / 32;                     // 16-column tiles per wave
-  constexpr int NB = GN * GK / 8 / 256;           // 16-byte chunks of the B tile per thread
+template <int WMW, int WNW, int TN>
+__global__ __launch_bounds__(64 * WMW * WNW) void gemm_bf16_nt_kernel(DownprojParams p) {
+  constexpr int NTH = 64 * WMW * WNW;             // threads
+  constexpr int GM = 64 * WMW, GN = TN * WNW;     // workgroup tile
+  constexpr int NT = TN / 16;                     // 16-column tiles per wave
+  constexpr int NA = GM * GK / 8 / NTH;           // 16-byte chunks of the X tile per thread
+  constexpr int NB = GN * GK / 8 / NTH;           // 16-byte chunks of the B tile per thread
+  static_assert(NA * NTH == GM * GK / 8 && NB * NTH == GN * GK / 8, "whole chunks per thread");
   __shared__ __align__(16) uint16_t xs[2][GM * GKP];
   __shared__ __align__(16) uint16_t bs[2][GN * GKP];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int n0 = blockIdx.x * GN, m0 = blockIdx.y * GM;
-  const int wm = (w >> 1) * 64, wn = (w & 1) * (GN / 2);
+  const int wm = (w / WNW) * 64, wn = (w % WNW) * TN;
   const int M = p.m, N = p.n, K = p.k;            // K is a multiple of GK (checked by the host)
-  // global -> register staging: chunk c = tid + 256 i of a (rows x 64) tile is
+  // global -> register staging: chunk c = tid + NTH i of a (rows x 64) tile is
   // row c / 8, k chunk c % 8 (16 bytes); rows past M or N read the last row
-  u4 rx[4], rb[NB];
+  u4 rx[NA], rb[NB];
   auto gload = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
+    for (int i = 0; i < NA; ++i) {
+      const int c = tid + NTH * i, row = c >> 3, kc = c & 7;
       const int m = min(m0 + row, M - 1);
       rx[i] = *reinterpret_cast<const u4*>(p.x + (int64_t)m * K + k0 + 8 * kc);
     }
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
-      const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
+      const int c = tid + NTH * i, row = c >> 3, kc = c & 7;
       const int n = min(n0 + row, N - 1);
       rb[i] = *reinterpret_cast<const u4*>(p.at + (int64_t)n * K + k0 + 8 * kc);
     }
   };
   auto sstore = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
+    for (int i = 0; i < NA; ++i) {
+      const int c = tid + NTH * i, row = c >> 3, kc = c & 7;
       *reinterpret_cast<u4*>(&xs[buf][row * GKP + 8 * kc]) = rx[i];
     }
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
-      const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
+      const int c = tid + NTH * i, row = c >> 3, kc = c & 7;
       *reinterpret_cast<u4*>(&bs[buf][row * GKP + 8 * kc]) = rb[i];
     }
   };
@@ -556,16 +562,15 @@ int launch_downproj(const DownprojParams& p, void* stream) {
     hipStream_t st = static_cast<hipStream_t>(stream);
     hipLaunchKernelGGL(transpose_bf16_kernel, dim3((p.n + 63) / 64, (p.k + 63) / 64), dim3(256), 0,
                        st, p.a, p.at, p.k, p.n);
-    // the tile width whose last round of tiles (two workgroups per CU) leaves
-    // the fewest idle slots; time ~ rounds x tile width
-    const int64_t mt = (p.m + GM - 1) / GM;
-    const int64_t t128 = mt * ((p.n + 127) / 128), t96 = mt * ((p.n + 95) / 96);
-    const int64_t slots = 2 * 256;
-    const bool use96 = ((t96 + slots - 1) / slots) * 96 < ((t128 + slots - 1) / slots) * 128;
-    if (use96)
-      hipLaunchKernelGGL(gemm_bf16_nt_kernel<96>, dim3((p.n + 95) / 96, mt), dim3(256), 0, st, p);
+    // 256 x 192 tiles when they give at least 96 workgroups (one per CU),
+    // else 128 x 96 tiles (then at most 4 x 96 of them: a single round at two
+    // workgroups per CU)
+    if (((p.m + 255) / 256) * ((p.n + 191) / 192) >= 96)
+      hipLaunchKernelGGL((gemm_bf16_nt_kernel<4, 2, 96>), dim3((p.n + 191) / 192, (p.m + 255) / 256),
+                         dim3(512), 0, st, p);
     else
-      hipLaunchKernelGGL(gemm_bf16_nt_kernel<128>, dim3((p.n + 127) / 128, mt), dim3(256), 0, st, p);
+      hipLaunchKernelGGL((gemm_bf16_nt_kernel<2, 2, 48>), dim3((p.n + 95) / 96, (p.m + 127) / 128),
+                         dim3(256), 0, st, p);
     return (int)hipGetLastError();
   }
   if (p.m <= kSmallM) {

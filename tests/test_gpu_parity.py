@@ -167,8 +167,8 @@ def test_append_from_hidden_states(name, n_new, d_model):
     """Down-projection then quantization: latents within 1 fp16 ulp of the oracle's fp64
     product plus the fp32 accumulation bound (which only matters where the sum cancels to
     a tiny latent); codes bit-exact when the oracle re-quantizes the GPU's fp16 latents.
-    512 and more rows (the last three cases) take the prefill GEMM, with 96-column tiles
-    and (11264 rows x 512) with 128-column tiles."""
+    512 and more rows (the last three cases) take the prefill GEMM: 128 x 96 tiles, and for
+    (11264 rows x 512) the 256 x 192 tiles of large problems."""
     w = small(name, ctx=256, batch=min(synth.WORKLOADS[name].batch, 4))
     w = w.with_(d_model=d_model)
     inp = synth.generate(w, with_hidden=True, n_hidden_tokens=n_new)
