@@ -162,13 +162,15 @@ def test_incremental_appends_bit_exact(name):
 @pytest.mark.parametrize("name,n_new,d_model", [("c4", 1, 4096), ("c3", 1, 4096), ("c5", 96, 1024),
                                                  ("c3q", 1, 4096), ("c5q", 96, 1024),
                                                  ("c5", 512, 1024), ("c3q", 300, 2048),
-                                                 ("c3", 2816, 64)])
+                                                 ("c3", 2816, 64), ("c3", 3000, 128),
+                                                 ("c5", 6144, 256)])
 def test_append_from_hidden_states(name, n_new, d_model):
     """Down-projection then quantization: latents within 1 fp16 ulp of the oracle's fp64
     product plus the fp32 accumulation bound (which only matters where the sum cancels to
     a tiny latent); codes bit-exact when the oracle re-quantizes the GPU's fp16 latents.
-    512 and more rows (the last three cases) take the prefill GEMM: 128 x 96 tiles, and for
-    (11264 rows x 512) the 256 x 192 tiles of large problems."""
+    512 and more rows (the last five cases) take the prefill GEMM: 128 x 96 tiles, and for
+    the last three (11264 x 512 x 64, 12000 x 512 x 128 with ragged row and column tiles,
+    12288 x 1056 x 256) the 256 x 192 tiles of large problems."""
     w = small(name, ctx=256, batch=min(synth.WORKLOADS[name].batch, 4))
     w = w.with_(d_model=d_model)
     inp = synth.generate(w, with_hidden=True, n_hidden_tokens=n_new)
