@@ -649,14 +649,18 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   // (jj, kq): 8 halves = B_k[row][16*mt + jj] for the 8 channels of chunk
   // 4*kb + kq, in the order the key operand delivers them (4-bit chunks:
   // channels 0,2,4,6,1,3,5,7; 8-bit and fp16 chunks in order); channels at or
-  // beyond the rank are zero.  Wave w gathers fragments w, w + 8, ... in
-  // batches whose loads are all issued before the first 16-byte LDS store.
+  // beyond the rank are zero.  Wave w builds fragments w, w + 8, ... in batches
+  // whose loads are all issued first.  A fragment's 32 x 16 block of B_k
+  // arrives as one 16-byte load per lane (block row l/2, columns 8*(l%2)..),
+  // is written row-major into the fragment's own 1 KiB of LDS, and is read
+  // back in operand order by the same wave, whose LDS operations complete in
+  // issue order.
   constexpr int kBatch = 5;
   const int n_fr = p.hg_frags[hg];
-  // rows beyond the rank (and fragments beyond the group) load a valid
-  // element and are zeroed when stored, so no load sits behind a branch
-  auto frag_load = [&](int f0, uint16_t (&ld)[kBatch][8], uint32_t (&live)[kBatch]) {
-    const int jj = lane & 15, kq = lane >> 4;
+  // rows beyond the rank (and fragments beyond the group) load a valid row and
+  // are zeroed when stored, so no load sits behind a branch; info = row live
+  // (bit 0) | element order of the chunk this lane reads back (bits 1..)
+  auto frag_load = [&](int f0, u4 (&ld)[kBatch], uint32_t (&info)[kBatch]) {
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) {
       const int f = min(f0 + k * kWaves, n_fr - 1);
@@ -669,39 +673,52 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       const int bk_row = __builtin_amdgcn_readlane(l_row, hs);
       const int fl = f - fb;
       const int mt = fl / nkb, kb = fl % nkb;
-      const int c = 4 * kb + kq;
+      const int row = 32 * kb + (lane >> 1);
+      ld[k] = *reinterpret_cast<const u4*>(p.bk + (int64_t)(bk_row + min(row, rank - 1)) * D +
+                                           16 * mt + 8 * (lane & 1));
       // element order of the chunk's key operand: 8-bit and fp16 in order,
       // 4-bit 0,2,4,6,1,3,5,7, 3-bit 0,4,1,5,2,6,3,7
+      const int c = 4 * kb + (lane >> 4);
       const int ord = QM == STARKV_Q_F16 ? 0
                       : QM == STARKV_Q_MIX4_3 ? (c < n8 ? 1 : 2) : (c < n8 ? 0 : 1);
-      const uint16_t* src = p.bk + (int64_t)bk_row * D + 16 * mt + jj;
-      live[k] = 0;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int wi = ord == 0 ? e : ord == 1 ? (e < 4 ? 2 * e : 2 * (e - 4) + 1)
-                                               : (e % 2 == 0 ? e / 2 : 4 + e / 2);
-        const int row = 8 * c + wi;
-        live[k] |= row < rank ? 1u << e : 0u;
-        ld[k][e] = src[(int64_t)min(row, rank - 1) * D];
-      }
+      info[k] = (row < rank ? 1u : 0u) | ((uint32_t)ord << 1);
     }
   };
-  auto frag_store = [&](int f0, const uint16_t (&ld)[kBatch][8], const uint32_t (&live)[kBatch]) {
+  auto wave_sync = [] {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
+  auto frag_store = [&](int f0, const u4 (&ld)[kBatch], const uint32_t (&info)[kBatch]) {
+    const int jj = lane & 15, kq = lane >> 4;
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) {
-      const int f = f0 + k * kWaves;
-      u4 v;
+      const int f = f0 + k * kWaves;          // wave-uniform
+      if (f < n_fr) {
+        u4* slot = reinterpret_cast<u4*>(frag + f * 64);
+        slot[lane] = (info[k] & 1u) ? ld[k] : (u4){0, 0, 0, 0};
+        wave_sync();
+        const uint16_t* blk = reinterpret_cast<const uint16_t*>(slot);   // [32][16]
+        const int ord = (int)(info[k] >> 1);
+        uint32_t e8[8];
 #pragma unroll
-      for (int h = 0; h < 4; ++h)
-        v[h] = ((live[k] >> (2 * h)) & 1u ? (uint32_t)ld[k][2 * h] : 0u) |
-               ((live[k] >> (2 * h + 1)) & 1u ? (uint32_t)ld[k][2 * h + 1] << 16 : 0u);
-      if (f < n_fr) frag[f * 64 + lane] = __builtin_bit_cast(h8, v);
+        for (int e = 0; e < 8; ++e) {
+          const int wi = ord == 0 ? e : ord == 1 ? (e < 4 ? 2 * e : 2 * (e - 4) + 1)
+                                                 : (e % 2 == 0 ? e / 2 : 4 + e / 2);
+          e8[e] = blk[(8 * kq + wi) * 16 + jj];
+        }
+        wave_sync();
+        u4 v;
+#pragma unroll
+        for (int h = 0; h < 4; ++h) v[h] = e8[2 * h] | (e8[2 * h + 1] << 16);
+        slot[lane] = v;
+      }
     }
   };
   // the fragment area is free from the start: batch 0 is loaded here and
   // stored after the RoPE tables are computed, batch 1 is loaded then and
   // stored after the key rotations, and any further batches follow
-  uint16_t ld0[kBatch][8], ld1[kBatch][8];
+  u4 ld0[kBatch], ld1[kBatch];
   uint32_t live0[kBatch], live1[kBatch];
   frag_load(w, ld0, live0);
 
@@ -785,7 +802,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   frag_store(w + kBatch * kWaves, ld1, live1);
   __syncthreads();   // RoPE tables are dead from here on (the value staging reuses them)
   for (int f0 = w + 2 * kBatch * kWaves; f0 < n_fr; f0 += kBatch * kWaves) {
-    uint16_t ld[kBatch][8];
+    u4 ld[kBatch];
     uint32_t live[kBatch];
     frag_load(f0, ld, live);
     frag_store(f0, ld, live);
