@@ -288,7 +288,12 @@ __global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
 }
 
 // ------------------------------------------------------------------ down-projection
-constexpr int BM = 64, BN = 64, BK = 32;
+// Split-k tiles of 64 rows x 64 columns; each workgroup covers k_chunk (a
+// multiple of BK) of K in steps of BK = kDownprojK = 128, so a decode-sized
+// append costs one or two rounds of loads per workgroup.  Per step, thread t
+// loads four 16-byte vectors of A_all (k rows t/8 + 32 i, columns 8 (t%8)..)
+// and four of x (rows t/16 + 16 i, k 8 (t%16)..); A is stored transposed.
+constexpr int BM = 64, BN = 64, BK = kDownprojK;
 
 __global__ __launch_bounds__(256) void downproj_kernel(DownprojParams p) {
   __shared__ __align__(16) __bf16 xs[BM][BK + 8];
@@ -298,44 +303,57 @@ __global__ __launch_bounds__(256) void downproj_kernel(DownprojParams p) {
   const int k_lo = ks * p.k_chunk;
   const int k_hi = min(p.k, k_lo + p.k_chunk);
   const int wm = (w >> 1) * 32, wn = (w & 1) * 32;
+  const bool vec_a = (p.n & 7) == 0;                 // 16-byte rows of A_all
   f4 acc[2][2];
   for (int i = 0; i < 2; ++i)
     for (int j = 0; j < 2; ++j) acc[i][j] = (f4){0, 0, 0, 0};
   for (int k0 = k_lo; k0 < k_hi; k0 += BK) {
-    // x tile: 64 rows x 32 k, 8 elements per thread
-    {
-      const int r = tid / 4, kk = (tid % 4) * 8;
-      const int m = m0 + r;
-      u4 v = (u4){0, 0, 0, 0};
-      if (m < p.m && k0 + kk + 8 <= k_hi) {
-        v = *reinterpret_cast<const u4*>(p.x + (int64_t)m * p.k + k0 + kk);
+    u4 xv[4], av[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {         // x: rows tid/16 + 16 i, k 8 (tid%16) ..
+      const int r = tid / 16 + 16 * i, kk = (tid % 16) * 8;
+      const int m = m0 + r, k = k0 + kk;
+      xv[i] = (u4){0, 0, 0, 0};
+      if (m < p.m && k + 8 <= k_hi) {
+        xv[i] = *reinterpret_cast<const u4*>(p.x + (int64_t)m * p.k + k);
       } else if (m < p.m) {
         uint16_t tmp[8];
-        for (int e = 0; e < 8; ++e)
-          tmp[e] = (k0 + kk + e < k_hi) ? p.x[(int64_t)m * p.k + k0 + kk + e] : (uint16_t)0;
-        v = *reinterpret_cast<u4*>(tmp);
+        for (int e = 0; e < 8; ++e) tmp[e] = (k + e < k_hi) ? p.x[(int64_t)m * p.k + k + e] : (uint16_t)0;
+        xv[i] = *reinterpret_cast<u4*>(tmp);
       }
-      *reinterpret_cast<u4*>(&xs[r][kk]) = v;
     }
-    // A tile: 32 k x 64 n, stored transposed
-    {
-      const int kr = tid / 8, nn = (tid % 8) * 8;
-      const int k = k0 + kr;
-      uint16_t tmp[8];
-      for (int e = 0; e < 8; ++e) {
-        const int n = n0 + nn + e;
-        tmp[e] = (k < k_hi && n < p.n) ? p.a[(int64_t)k * p.n + n] : (uint16_t)0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {         // A: k rows tid/8 + 32 i, columns 8 (tid%8) ..
+      const int kr = tid / 8 + 32 * i, nn = (tid % 8) * 8;
+      const int k = k0 + kr, n = n0 + nn;
+      av[i] = (u4){0, 0, 0, 0};
+      if (k < k_hi && vec_a && n + 8 <= p.n) {
+        av[i] = *reinterpret_cast<const u4*>(p.a + (int64_t)k * p.n + n);
+      } else if (k < k_hi) {
+        uint16_t tmp[8];
+        for (int e = 0; e < 8; ++e) tmp[e] = (n + e < p.n) ? p.a[(int64_t)k * p.n + n + e] : (uint16_t)0;
+        av[i] = *reinterpret_cast<u4*>(tmp);
       }
-      for (int e = 0; e < 8; ++e) as[nn + e][kr] = __builtin_bit_cast(__bf16, tmp[e]);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      *reinterpret_cast<u4*>(&xs[tid / 16 + 16 * i][(tid % 16) * 8]) = xv[i];
+      const int kr = tid / 8 + 32 * i, nn = (tid % 8) * 8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        as[nn + e][kr] = __builtin_bit_cast(__bf16, (uint16_t)(av[i][e / 2] >> (16 * (e & 1))));
     }
     __syncthreads();
     const int row = lane & 15, kq = lane >> 4;
-    b8 af[2], bf[2];
-    for (int i = 0; i < 2; ++i) af[i] = *reinterpret_cast<const b8*>(&xs[wm + 16 * i + row][8 * kq]);
-    for (int j = 0; j < 2; ++j) bf[j] = *reinterpret_cast<const b8*>(&as[wn + 16 * j + row][8 * kq]);
-    for (int i = 0; i < 2; ++i)
-      for (int j = 0; j < 2; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 32) {
+      b8 af[2], bf[2];
+      for (int i = 0; i < 2; ++i) af[i] = *reinterpret_cast<const b8*>(&xs[wm + 16 * i + row][kk + 8 * kq]);
+      for (int j = 0; j < 2; ++j) bf[j] = *reinterpret_cast<const b8*>(&as[wn + 16 * j + row][kk + 8 * kq]);
+      for (int i = 0; i < 2; ++i)
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+    }
     __syncthreads();
   }
   // C tile (16x16): lane holds rows 4*(lane/16)+e of column lane%16

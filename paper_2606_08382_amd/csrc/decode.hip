@@ -25,6 +25,8 @@
 //   query head (Sec. 3.3), casting to the output type.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
+
 #include <type_traits>
 
 #include "starkv_internal.h"
@@ -1594,17 +1596,26 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
 // The file is compiled once per (head_dim, cache precision) with SK_D and SK_QM
 // set, producing the split-kernel instances for that pair, and once with
 // SK_COMMON for the combine kernel and the dispatcher.
+// Raises a kernel's dynamic LDS limit to 160 KiB once per device: `done` holds
+// one bit per device index (indices past 63 set it on every launch).
+static int allow_lds(const void* fn, std::atomic<uint64_t>& done) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return (int)e;
+  const uint64_t bit = dev < 64 ? 1ull << dev : 0;
+  if (bit && (done.load(std::memory_order_acquire) & bit)) return 0;
+  e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  if (e != hipSuccess) return (int)e;
+  done.fetch_or(bit, std::memory_order_release);
+  return 0;
+}
+
 #if defined(SK_D) && defined(SK_QM)
 template <int D, int QM, int CT, int NTW>
 static int launch_split_t(const DecodeParams& p, size_t lds, hipStream_t st) {
   auto k = decode_split_kernel<D, QM, CT, NTW>;
-  static bool attr = false;
-  if (!attr) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (e != hipSuccess) return (int)e;
-    attr = true;
-  }
+  static std::atomic<uint64_t> attr{0};
+  if (const int e = allow_lds(reinterpret_cast<const void*>(k), attr)) return e;
   dim3 grid(p.dyn ? p.cap : p.n_split, p.dyn ? 1 : p.batch, p.n_hg);
   hipLaunchKernelGGL(k, grid, dim3(kThreads), lds, st, p);
   return (int)hipGetLastError();
@@ -1675,13 +1686,8 @@ int launch_decode_combine(const CombineParams& p, void* stream) {
   const size_t upproj = (size_t)256 / (p.head_dim / 8) * p.head_dim;
   const size_t lds = ((size_t)combine_head_floats(p.rv) + (merge > upproj ? merge : upproj)) *
                      sizeof(float);
-  static bool attr = false;
-  if (!attr) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(decode_combine_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (e != hipSuccess) return (int)e;
-    attr = true;
-  }
+  static std::atomic<uint64_t> attr{0};
+  if (const int e = allow_lds(reinterpret_cast<const void*>(decode_combine_kernel), attr)) return e;
   dim3 grid(p.n_q, p.batch);
   hipLaunchKernelGGL(decode_combine_kernel, grid, dim3(256), lds,
                      static_cast<hipStream_t>(stream), p);

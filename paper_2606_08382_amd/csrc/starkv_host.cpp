@@ -707,8 +707,7 @@ static void downproj_shape(const starkv_plan* P, int32_t n_new, int* k_split, in
   int ks = 256 / tiles;
   if (ks < 1) ks = 1;
   int chunk = (K + ks - 1) / ks;
-  chunk = (chunk + 31) / 32 * 32;
-  if (chunk < 32) chunk = 32;
+  chunk = (chunk + kDownprojK - 1) / kDownprojK * kDownprojK;
   *k_chunk = chunk;
   *k_split = (K + chunk - 1) / chunk;
 }

@@ -182,6 +182,8 @@ int launch_append_pack(const AppendParams& p, void* stream);
 constexpr int kSmallM = 7;
 // rows from which (with d_model a multiple of 64) it is one GEMM over all of K
 constexpr int kGemmMinM = 512;
+// k step (and k-chunk granule) of the split-k down-projection tiles
+constexpr int kDownprojK = 128;
 int launch_downproj(const DownprojParams& p, void* stream);
 
 }  // namespace starkv

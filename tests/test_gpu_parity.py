@@ -160,6 +160,7 @@ def test_incremental_appends_bit_exact(name):
 
 
 @pytest.mark.parametrize("name,n_new,d_model", [("c4", 1, 4096), ("c3", 1, 4096), ("c5", 96, 1024),
+                                                 ("c4", 8, 4096), ("c3", 16, 1000),
                                                  ("c3q", 1, 4096), ("c5q", 96, 1024),
                                                  ("c5", 512, 1024), ("c3q", 300, 2048),
                                                  ("c3", 2816, 64), ("c3", 3000, 128),
@@ -168,6 +169,8 @@ def test_append_from_hidden_states(name, n_new, d_model):
     """Down-projection then quantization: latents within 1 fp16 ulp of the oracle's fp64
     product plus the fp32 accumulation bound (which only matters where the sum cancels to
     a tiny latent); codes bit-exact when the oracle re-quantizes the GPU's fp16 latents.
+    Up to 7 rows take the streaming kernel; 8 to 511 rows the split-k tiles (32 rows at
+    d_model 4096; 64 rows at d_model 1000, whose last k step is partial; 192 rows).
     512 and more rows (the last five cases) take the prefill GEMM: 128 x 96 tiles, and for
     the last three (11264 x 512 x 64, 12000 x 512 x 128 with ragged row and column tiles,
     12288 x 1056 x 256) the 256 x 192 tiles of large problems."""
