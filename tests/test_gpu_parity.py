@@ -239,6 +239,33 @@ def test_full_size_128k_sampled_heads(name):
     say(f"  absorbed output ok, last max err {e:.3e} |y| {s:.3e}")
 
 
+def test_longest_context_single_sequence():
+    """One sequence at the longest supported context, 524288 tokens: the work plan gives it
+    64 splits of 8192 tokens (the longest split, the most splits the combine merges). The
+    whole cache bit-exact and sampled query heads of the first and last KV heads within
+    tolerance."""
+    w = small("c3", ctx=524288, batch=1)
+    inp = synth.generate(w)
+    say(f"longest context {w.name}")
+    layer = _layer(w, inp)
+    pos = torch.zeros(1, dtype=torch.int32, device="cuda")
+    for b0 in range(0, w.ctx, 65536):
+        layer.append(_dev(np.ascontiguousarray(inp.latents[:, b0:b0 + 65536])), pos + b0)
+    layer.decode(_dev(inp.q), _dev(inp.Bk), _dev(inp.Bv), _dev(inp.ctx_len))
+    torch.cuda.synchronize()
+    cfg = oracle_cfg(w, inp)
+    cache = O.new_cache(cfg)
+    O.append(cfg, cache, inp.latents, [0])
+    assert np.array_equal(layer.cache.cpu().numpy(), cache)
+    sel = [(0, 1), (0, 30)]
+    ref, _ = O.decode_attn(cfg, cache, inp.q, w.q_dtype == synth.DT_BF16, inp.Bk, inp.Bv,
+                           inp.ctx_len, sel=sel)
+    got = layer.out_float()
+    for (b, i) in sel:
+        e, s_ = assert_close(got[b, i], ref[b, i], f"head={i}", w.out_dtype)
+    say(f"  sampled heads ok, last max err {e:.3e} |o| {s_:.3e}")
+
+
 def _absorbed_case(w, inp, d_out, ctx_len=None, max_ctx=None, capacity=None):
     """Append at row 0, decode with the absorbed output, compare with the oracle's y."""
     say(f"absorbed {w.name} B={w.batch} ctx={w.ctx} d_out={d_out} qmode={w.qmode}")
