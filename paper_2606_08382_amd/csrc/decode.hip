@@ -1287,6 +1287,9 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   uint16_t* bks = reinterpret_cast<uint16_t*>(lat + kRescoreMax * p.rmax);  // [rmax][D] fp16
   float* red = uni;                                    // [256 / (D/8)][D] partial up-projections
   const int i = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  // output columns c_0 .. c_0 + Dc - 1 of this workgroup (the merge and the
+  // rescoring are repeated by each of the col_split workgroups of the head)
+  const int Dc = D / p.col_split, c_0 = blockIdx.z * Dc;
   const int lane = tid & 63, w = tid >> 6;
   const int g = (int)(((int64_t)i * p.n_kv) / p.n_q);
   // this sequence's splits: under the work plan, items first .. first + ns - 1
@@ -1313,7 +1316,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
       for (int r = tid; r < p.rv; r += 256) p.lat[lat_row + r] = p.lat[lat_lo + lat_row + r] = 0;
       return;
     }
-    for (int j = tid; j < D; j += 256) {
+    for (int j = c_0 + tid; j < c_0 + Dc; j += 256) {
       if (p.out_dtype == STARKV_DT_F32) static_cast<float*>(p.out)[out_row + j] = 0.0f;
       else static_cast<uint16_t*>(p.out)[out_row + j] = 0;
     }
@@ -1340,11 +1343,11 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   }
   // the value-latent partials of this thread's first channel and its first
   // rows of U_V do not depend on the merge weights: load them now as well
-  const int D8 = D / 8;                  // 16 (D = 128) or 8 (D = 64)
+  const int D8 = Dc / 8;                 // 16, 8 or 4 column vectors
   const int groups = 256 / D8;           // row groups of the up-projection
   const int j8 = tid % D8, rg = tid / D8;
   const int64_t ldb = (int64_t)p.n_kv * D;
-  const uint16_t* bv = p.bv + (int64_t)g * D + 8 * j8;
+  const uint16_t* bv = p.bv + (int64_t)g * D + c_0 + 8 * j8;
   // 32-bit byte offsets from the (b, head) partials: the region spans
   // n_split * sstride floats, far below 4 GiB
   const uint8_t* pbase = reinterpret_cast<const uint8_t*>(part);
@@ -1544,7 +1547,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
     return;
   }
   // o = a . U_V^T restricted to KV head g's d columns (the reordering of Sec. 3.3):
-  // thread (rg, j8) covers rows rg, rg + groups, .. and columns 8*j8..8*j8+7
+  // thread (rg, j8) covers rows rg, rg + groups, .. and columns c_0 + 8*j8 ..+7
   float o[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   auto up_rows = [&](int r0, const u4 (&w8)[kUpRows]) {
 #pragma unroll
@@ -1570,13 +1573,13 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
     up_rows(r0, w8);
   }
 #pragma unroll
-  for (int e = 0; e < 8; ++e) red[rg * D + 8 * j8 + e] = o[e];
+  for (int e = 0; e < 8; ++e) red[rg * Dc + 8 * j8 + e] = o[e];
   __syncthreads();
-  if (tid < D) {
+  if (tid < Dc) {
     float ov = 0.0f;
-    for (int k = 0; k < groups; ++k) ov += red[k * D + tid];
+    for (int k = 0; k < groups; ++k) ov += red[k * Dc + tid];
     if (p.out_dtype == STARKV_DT_F32) {
-      static_cast<float*>(p.out)[out_row + tid] = ov;
+      static_cast<float*>(p.out)[out_row + c_0 + tid] = ov;
     } else {
       uint16_t bits;
       if (p.out_dtype == STARKV_DT_BF16) {
@@ -1586,7 +1589,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
       } else {
         bits = __builtin_bit_cast(uint16_t, (_Float16)ov);
       }
-      static_cast<uint16_t*>(p.out)[out_row + tid] = bits;
+      static_cast<uint16_t*>(p.out)[out_row + c_0 + tid] = bits;
     }
   }
 }
@@ -1683,12 +1686,14 @@ int launch_decode_combine(const CombineParams& p, void* stream) {
   // the shared region: the merge phase (split sums, rescoring latents, B_k
   // block) or the up-projection's 256 / (D/8) rows of D partial sums
   const size_t merge = (size_t)4 * p.rv + (size_t)kRescoreMax * p.rmax + (size_t)p.rmax * p.head_dim / 2;
-  const size_t upproj = (size_t)256 / (p.head_dim / 8) * p.head_dim;
+  if (p.col_split != 1 && (p.col_split != 2 || p.lat)) return (int)hipErrorInvalidValue;
+  const int dc = p.head_dim / p.col_split;
+  const size_t upproj = (size_t)256 / (dc / 8) * dc;
   const size_t lds = ((size_t)combine_head_floats(p.rv) + (merge > upproj ? merge : upproj)) *
                      sizeof(float);
   static std::atomic<uint64_t> attr{0};
   if (const int e = allow_lds(reinterpret_cast<const void*>(decode_combine_kernel), attr)) return e;
-  dim3 grid(p.n_q, p.batch);
+  dim3 grid(p.n_q, p.batch, p.col_split);
   hipLaunchKernelGGL(decode_combine_kernel, grid, dim3(256), lds,
                      static_cast<hipStream_t>(stream), p);
   return (int)hipGetLastError();

@@ -602,6 +602,9 @@ static void combine_params(const starkv_plan* P, const void* cache, const void* 
     if (wp.dyn) p.n_split = kMaxSplits;   // a sequence has at most this many splits
   }
   p.part_stride = part_stride(P);
+  // two workgroups per (sequence, query head), each up-projecting half of the
+  // output columns, while that still leaves at least one compute unit for each
+  p.col_split = 2 * (int64_t)c.batch * c.n_q_heads <= kComputeUnits ? 2 : 1;
   p.out_dtype = c.out_dtype;
   p.q_bf16 = c.q_dtype == STARKV_DT_BF16;
   p.qmode = c.qmode;
@@ -665,6 +668,7 @@ starkv_status starkv_decode_combine_absorbed(const starkv_plan* P, const void* c
   CombineParams cp;
   combine_params(P, cache, q, B_k, nullptr, ctx_len_dev, max_ctx, nullptr, ws, cp);
   cp.lat = lat;
+  cp.col_split = 1;                         // one workgroup writes a head's latents
   st = hip_status(launch_decode_combine(cp, static_cast<void*>(stream)), "decode_combine launch");
   if (st != STARKV_OK) return st;
   AbsorbParams ap;

@@ -114,6 +114,8 @@ struct CombineParams {
   int32_t dyn, k_lo, cap;      // as in DecodeParams
   int32_t out_dtype, q_bf16, qmode;
   int32_t rmax;                // largest key rank (sizes the rescoring buffers)
+  int32_t col_split;           // workgroups per (sequence, query head), each taking
+                               // head_dim / col_split output columns (1 or 2; 1 with lat)
   RowMap rmap;
   float score_scale;
   double log2_theta;
