@@ -56,6 +56,7 @@ int row_bytes(int qmode, int r) {
 
 constexpr int kLdsLimit = 160 * 1024;
 constexpr int kMaxSplits = 64;          // context splits per sequence merged by the combine pass
+constexpr int kComputeUnits = 256;
 constexpr int kMaxSplitTokens = 8192;   // tokens per split (bounds the RoPE rotation recurrence)
 
 }  // namespace
@@ -295,6 +296,26 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
     delete P;
     return fail(STARKV_ERR_UNSUPPORTED, "no workgroup shape fits the ranks in LDS");
   }
+  // A sequence has at most kMaxSplits work items per head group, so with few
+  // sequences some compute units would idle: split the groups with the most KV
+  // heads in two until batch * kMaxSplits * n_hg covers the compute units (a
+  // part of a group that fits the LDS fits too).  Every group streams the
+  // shared value latent again, more HBM bytes on a pass that is bound by
+  // instruction issue.
+  {
+    const int want = std::min(c->n_kv_heads, (kComputeUnits + kMaxSplits * c->batch - 1) /
+                                                 (kMaxSplits * c->batch));
+    while (P->n_hg < want) {
+      int gi = 0;
+      for (int h = 1; h < P->n_hg; ++h)
+        if (P->hg_first[h + 1] - P->hg_first[h] > P->hg_first[gi + 1] - P->hg_first[gi]) gi = h;
+      const int a = P->hg_first[gi], b = P->hg_first[gi + 1];
+      if (b - a < 2) break;
+      for (int h = P->n_hg; h > gi; --h) P->hg_first[h + 1] = P->hg_first[h];
+      P->hg_first[gi + 1] = a + (b - a) / 2;
+      ++P->n_hg;
+    }
+  }
   P->ct = best_ct;
   P->lds_bytes = 0;
   int pos = 0;
@@ -384,7 +405,6 @@ starkv_status starkv_cache_layout(const starkv_plan* plan, starkv_layout* out) {
 // compute unit's workgroup per item and head group (or more items where even
 // 8192-token splits need them).  Larger batches split every sequence alike
 // for max_ctx.
-constexpr int kComputeUnits = 256;
 constexpr int kMaxPlanBatch = 64;
 struct WorkPlan {
   bool dyn;
