@@ -1177,7 +1177,8 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 
 // ---------------------------------------------------------------------- combine
 #ifdef SK_COMMON
-// One workgroup per (query head, sequence).  Merges the splits with weights
+// One workgroup per (query head, sequence), or two that each up-project half
+// of the output columns when the grid is small.  Merges the splits with weights
 // 2^(m_s - M), corrects the few tokens that dominate the softmax with exactly
 // recomputed scores, and applies the value up-projection of the head's KV group.
 // All loads of a phase are issued before their results are used, so each phase
