@@ -225,7 +225,7 @@ starkv_status starkv_append(const starkv_plan* plan, void* cache, const void* x_
  *                key t is rotated by RoPE at position t.  Values are clamped to
  *                [0, max_ctx]; 0 gives a zero output.
  *   max_ctx      host upper bound of ctx_len, 1 <= max_ctx <= capacity, and at most
- *                524288 (64 context splits of at most 8192 tokens; UNSUPPORTED beyond).
+ *                524288 tokens (UNSUPPORTED beyond).
  *   out          device [B][H_q][d] in out_dtype, 16-byte aligned; 16-bit types are
  *                rounded to nearest even from the fp32 result.
  *   ws           device, starkv_decode_workspace_bytes(plan, max_ctx) bytes,
@@ -290,8 +290,8 @@ starkv_status starkv_decode_combine_absorbed(const starkv_plan* plan, const void
 /* Number of context splits and tokens per split for max_ctx tokens in every
  * sequence; informative.  With up to 64 sequences the kernels choose the split
  * length on the device from the actual lengths (the smallest multiple of 128
- * tokens giving at most one work item per compute unit, at most 64 splits of at
- * most 8192 tokens per sequence); these functions report that plan for equal
+ * tokens giving at most one work item per compute unit and head group, at most
+ * 256 splits of at most 8192 tokens per sequence); these functions report that plan for equal
  * lengths of max_ctx. */
 int32_t       starkv_decode_splits(const starkv_plan* plan, int32_t max_ctx);
 int32_t       starkv_decode_split_tokens(const starkv_plan* plan, int32_t max_ctx);

@@ -94,7 +94,7 @@ __device__ __forceinline__ int div_up_small(int x, int k, float rk) {
 
 // Work plan of one decode step for up to 64 sequences of ragged lengths: the
 // split length S = kStepTokens * k is the smallest with at most `cap` work
-// items sum_b ceil(L_b / S) (k >= k_lo keeps every sequence at <= 64 splits,
+// items sum_b ceil(L_b / S) (k >= k_lo keeps every sequence at <= 256 splits,
 // k <= 64 keeps S <= 8192), and the items are the sequences' splits in order.
 // Every wave that calls this gets the same plan.  len: the clamped length held
 // by lane b (lanes >= B hold 0).  Returns k; *cnt gets the split count of
@@ -1194,11 +1194,13 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 // reconstruction, RoPE angle reduced in fp64), and their contribution to the
 // normalizer and to the merged value latent is moved from the approximate to the
 // exact weight.
-constexpr int kCombineMaxSplits = 64;   // one split per lane of the weight wave
+constexpr int kCombineMaxSplits = 256;  // one split per thread of the weight pass
 constexpr int kRescoreMax = 32;                        // tokens rescored per query head
 constexpr float kRescoreTau = 1.0f / 64.0f;
 constexpr int kBkVecPerThread = 8;   // B_k block of up to 128 x 128 fp16: 2048 vectors / 256 threads
-constexpr int kCandPerThread = kCombineMaxSplits * kCand / 256;
+// candidate entries are read in chunks of 64 splits, kCandPerThread per thread
+constexpr int kCandChunk = 64 * kCand;
+constexpr int kCandPerThread = kCandChunk / 256;
 
 __device__ __forceinline__ float h2f(uint16_t u) { return (float)__builtin_bit_cast(_Float16, u); }
 
@@ -1266,19 +1268,20 @@ __device__ float value_latent(const CombineParams& p, int b, int t, int r) {
 // floats of the combine kernel's LDS before its shared region (kept a multiple
 // of 4 so that the region is 16-byte aligned)
 __host__ __device__ constexpr int combine_head_floats(int rv) {
-  return (rv + 64 + 3 * kRescoreMax + 8 + 3) / 4 * 4;
+  return (rv + kCombineMaxSplits + 3 * kRescoreMax + 12 + 3) / 4 * 4;
 }
 
 __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   extern __shared__ __align__(16) float sm[];
   const int D = p.head_dim;
   float* a = sm;                         // [rv] merged value latent
-  float* wts = a + p.rv;                 // [64] split weights (one per lane of the weight wave)
-  float* c_x = wts + 64;                 // [kRescoreMax] approximate scores
+  float* wts = a + p.rv;                 // [kCombineMaxSplits] split weights
+  float* c_x = wts + kCombineMaxSplits;  // [kRescoreMax] approximate scores
   float* c_d = c_x + kRescoreMax;        // [kRescoreMax] weight corrections
   int* c_t = reinterpret_cast<int*>(c_d + kRescoreMax);   // [kRescoreMax] tokens
-  float* misc = reinterpret_cast<float*>(c_t + kRescoreMax);  // M, L, L', unused, wave counts [4]
-  int* cnt = reinterpret_cast<int*>(misc + 4);
+  float* misc = reinterpret_cast<float*>(c_t + kRescoreMax);  // M, L, L', unused
+  float* wmax = misc + 4;                // [4] per-wave split maxima
+  float* wsum = misc + 8;                // [4] per-wave weighted sums
   // One region, 16-byte aligned, serves two phases: the merge (per-wave split
   // sums, and the rescoring's key latents and B_k block) and, once the merged
   // latent is in `a`, the up-projection's partial sums.
@@ -1332,18 +1335,22 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   // sequence's splits are masked where they are used)
   // (addresses are a per-lane base plus wave-uniform offsets; entries beyond
   // the sequence's splits are masked where they are used)
-  float2 ce[kCandPerThread];
-  {
-    const float2* cl = cand + (int64_t)(tid / kCand) * p.n_q * kCand + tid % kCand;
+  // entry e = 32 s + j of chunk c (split 64 c + s, slot j); thread tid holds
+  // entries k * 256 + tid of a chunk
+  auto load_cand = [&](int c, float2 (&ce)[kCandPerThread]) {
+    const float2* cl = cand + (int64_t)(64 * c + tid / kCand) * p.n_q * kCand + tid % kCand;
     const int64_t cstep = (int64_t)(256 / kCand) * p.n_q * kCand;
 #pragma unroll
     for (int k = 0; k < kCandPerThread; ++k) {
       ce[k] = make_float2(-INFINITY, 0.0f);
-      if (k * 256 + tid < n_ent) ce[k] = cl[k * cstep];
+      if (c * kCandChunk + k * 256 + tid < n_ent) ce[k] = cl[k * cstep];
     }
-  }
-  // the value-latent partials of this thread's first channel and its first
-  // rows of U_V do not depend on the merge weights: load them now as well
+  };
+  const int n_cchunk = (n_ent + kCandChunk - 1) / kCandChunk;
+  float2 ce0[kCandPerThread];            // chunk 0 stays in registers
+  load_cand(0, ce0);
+  // the value-latent partials of this thread's first channel do not depend on
+  // the merge weights: load them now as well
   const int D8 = Dc / 8;                 // 16, 8 or 4 column vectors
   const int groups = 256 / D8;           // row groups of the up-projection
   const int j8 = tid % D8, rg = tid / D8;
@@ -1370,30 +1377,29 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   f4 pv0[kSplitBatch];
   load_batch(0, 0, pv0);
   constexpr int kUpRows = 4;             // rows of U_V per thread per round of loads
-  u4 w0[kUpRows];
-  {
-    const uint16_t* bl = bv + (int64_t)rg * ldb;
-#pragma unroll
-    for (int k = 0; k < kUpRows; ++k) {
-      w0[k] = (u4){0, 0, 0, 0};
-      if (!to_lat && rg + k * groups < p.rv)
-        w0[k] = *reinterpret_cast<const u4*>(bl + (int64_t)k * groups * ldb);
-    }
-  }
   const int r_g = p.k_rank[g];
-  if (tid < 64) {                 // split weights: one wave, one split per lane
+  {                               // split weights: one split per thread
     const int s = min(tid, ns - 1);
-    const float mv = tid < ns ? part[s * sstride + p.rv] : -INFINITY;
-    const float lv = part[s * sstride + p.rv + 1];
-    float m = mv;
+    // m_s and l_s wait in LDS (lat is free here) across the barrier
+    float* lsp = lat;
+    const float mv0 = tid < ns ? part[s * sstride + p.rv] : -INFINITY;
+    lsp[tid] = part[s * sstride + p.rv + 1];
+    wts[tid] = mv0;
+    float m = mv0;
     for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    if (lane == 0) wmax[w] = m;
+    __syncthreads();
+    m = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
+    const float mv = wts[tid], lv = lsp[tid];
     const float wv = tid < ns ? __builtin_amdgcn_exp2f(mv - m) : 0.0f;
     wts[tid] = wv;
     float l = tid < ns ? wv * lv : 0.0f;
     for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o);
-    if (tid == 0) { misc[0] = m; misc[1] = l; }
+    if (lane == 0) wsum[w] = l;
+    __syncthreads();
+    if (tid == 0) { misc[0] = m; misc[1] = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3]; }
+    __syncthreads();
   }
-  __syncthreads();
   const float M = misc[0], Lsum = misc[1];
   // weighted sums of this wave's splits, per channel, into red4[w][r]
   auto add_batch = [&](int h, const f4 (&pv)[kSplitBatch], f4& acc) {
@@ -1420,49 +1426,125 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
     const int r = 256 * ch + 4 * lane;
     if (r < p.rv) *reinterpret_cast<f4*>(red4 + w * p.rv + r) = acc;
   }
+  // splits beyond 64 (long sequences): further batches added to the wave's own
+  // partial sums, in the same order
+  for (int h = 2; 32 * h < ns; ++h)
+    for (int ch = 0; ch < n_chunk; ++ch) {
+      f4 pv[kSplitBatch];
+      load_batch(ch, h, pv);
+      const int r = 256 * ch + 4 * lane;
+      if (r < p.rv) {
+        f4 acc = *reinterpret_cast<const f4*>(red4 + w * p.rv + r);
+        add_batch(h, pv, acc);
+        *reinterpret_cast<f4*>(red4 + w * p.rv + r) = acc;
+      }
+    }
 
-  // ---- candidate selection: share x (1 + |x|) >= tau, tau raised until at most
-  // kRescoreMax remain; compaction in entry order (deterministic)
-  float prio[kCandPerThread];
-#pragma unroll
-  for (int k = 0; k < kCandPerThread; ++k) {
-    const float x = ce[k].x;
-    prio[k] = (x == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(x - M) / Lsum * (1.0f + fabsf(x));
-  }
-  float tau = kRescoreTau;
-  int n_sel = 0;
-  for (int it = 0; it < 8; ++it) {
-    int c = 0;
-#pragma unroll
-    for (int k = 0; k < kCandPerThread; ++k) c += prio[k] >= tau;
-    for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o);
-    if (lane == 0) cnt[w] = c;
-    __syncthreads();
-    n_sel = cnt[0] + cnt[1] + cnt[2] + cnt[3];
-    __syncthreads();
-    if (n_sel <= kRescoreMax) break;
-    tau *= 4.0f;
-  }
-  if (n_sel > kRescoreMax) n_sel = 0;   // too flat to matter at any threshold tried
-  if (n_sel > 0) {
-    int base = 0;
+  // ---- candidate selection: share x (1 + |x|) >= tau, tau raised by 4 until
+  // at most kRescoreMax remain (at most 8 thresholds); compaction in entry
+  // order (deterministic).  Up to 64 splits the entries stay in registers;
+  // beyond, one pass over the chunks counts the entries above each threshold
+  // and a second compacts, reading the chunks again.
+  constexpr int kLevels = 8;
+  auto priorities = [&](const float2 (&ce)[kCandPerThread], float (&prio)[kCandPerThread]) {
 #pragma unroll
     for (int k = 0; k < kCandPerThread; ++k) {
-      const bool sel = prio[k] >= tau;
-      const uint64_t bal = __ballot(sel);
-      const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
-                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
-      if (lane == 0) cnt[w] = __builtin_popcountll(bal);
-      __syncthreads();
+      const float x = ce[k].x;
+      prio[k] = (x == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(x - M) / Lsum * (1.0f + fabsf(x));
+    }
+  };
+  int* kcnt = reinterpret_cast<int*>(lat);   // [kCandPerThread][4] wave counts (lat is free here)
+  // one chunk's entries with prio >= tau go to c_x / c_t from `base` on, in
+  // entry order; returns the next base
+  auto compact = [&](const float2 (&ce)[kCandPerThread], const float (&prio)[kCandPerThread],
+                     float tau, int base) {
+    uint64_t bal[kCandPerThread];
+#pragma unroll
+    for (int k = 0; k < kCandPerThread; ++k) {
+      bal[k] = __ballot(prio[k] >= tau);
+      if (lane == 0) kcnt[4 * k + w] = __builtin_popcountll(bal[k]);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kCandPerThread; ++k) {
       int off = base;
-      for (int ww = 0; ww < w; ++ww) off += cnt[ww];
-      if (sel) {
+      for (int ww = 0; ww < w; ++ww) off += kcnt[4 * k + ww];
+      if (prio[k] >= tau) {
+        const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal[k] >> 32),
+                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)bal[k], 0));
         c_x[off + rank] = ce[k].x;
         c_t[off + rank] = __float_as_int(ce[k].y);
       }
-      base += cnt[0] + cnt[1] + cnt[2] + cnt[3];
-      __syncthreads();
+      base += kcnt[4 * k] + kcnt[4 * k + 1] + kcnt[4 * k + 2] + kcnt[4 * k + 3];
     }
+    __syncthreads();                     // kcnt is rewritten by the next chunk
+    return base;
+  };
+  float tau = kRescoreTau;
+  int n_sel = 0;
+  if (n_cchunk == 1) {
+    float prio[kCandPerThread];
+    priorities(ce0, prio);
+    for (int it = 0; it < kLevels; ++it) {
+      int c = 0;
+#pragma unroll
+      for (int k = 0; k < kCandPerThread; ++k) c += prio[k] >= tau;
+      for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o);
+      if (lane == 0) kcnt[w] = c;
+      __syncthreads();
+      n_sel = kcnt[0] + kcnt[1] + kcnt[2] + kcnt[3];
+      __syncthreads();
+      if (n_sel <= kRescoreMax) break;
+      tau *= 4.0f;
+    }
+    if (n_sel > kRescoreMax) n_sel = 0;   // too flat to matter at any threshold tried
+    if (n_sel > 0) compact(ce0, prio, tau, 0);
+  } else {
+    // entries at or above threshold j, per thread, in 16-bit fields (field j % 2
+    // of word j / 2; at most 32 per thread and 2048 per wave)
+    uint32_t lv[kLevels / 2];
+#pragma unroll
+    for (int j = 0; j < kLevels / 2; ++j) lv[j] = 0;
+    for (int c = 0; c < n_cchunk; ++c) {
+      float2 ce[kCandPerThread];
+      load_cand(c, ce);
+      float prio[kCandPerThread];
+      priorities(ce, prio);
+#pragma unroll
+      for (int k = 0; k < kCandPerThread; ++k) {
+        float t = kRescoreTau;
+#pragma unroll
+        for (int j = 0; j < kLevels; ++j, t *= 4.0f)
+          lv[j / 2] += prio[k] >= t ? 1u << (16 * (j % 2)) : 0u;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kLevels / 2; ++j) {
+      uint32_t v = lv[j];
+      for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+      if (lane == 0) kcnt[4 * j + w] = (int)v;
+    }
+    __syncthreads();
+    for (int j = 0; j < kLevels; ++j) {
+      n_sel = 0;
+      for (int ww = 0; ww < 4; ++ww) n_sel += ((uint32_t)kcnt[4 * (j / 2) + ww] >> (16 * (j % 2))) & 0xFFFFu;
+      if (n_sel <= kRescoreMax) break;
+      tau *= 4.0f;
+    }
+    if (n_sel > kRescoreMax) n_sel = 0;
+    __syncthreads();                     // the counts are read before kcnt is rewritten
+    if (n_sel > 0) {
+      int base = 0;
+      for (int c = 0; c < n_cchunk; ++c) {
+        float2 ce[kCandPerThread];
+        load_cand(c, ce);
+        float prio[kCandPerThread];
+        priorities(ce, prio);
+        base = compact(ce, prio, tau, base);
+      }
+    }
+  }
+  if (n_sel > 0) {
     // one round of loads for the rescoring: the KV head's up-projection block
     // B_k (r_g x D fp16, staged in LDS) and the candidates' key latents
     const int nbk = r_g * D / 8;           // 16-byte vectors
@@ -1536,6 +1618,17 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
     }
     a[r] = acc * inv_l;
   };
+  // the first rows of U_V, in flight while the rescored tokens' value latents load
+  u4 w0[kUpRows];
+  {
+    const uint16_t* bl = bv + (int64_t)rg * ldb;
+#pragma unroll
+    for (int k = 0; k < kUpRows; ++k) {
+      w0[k] = (u4){0, 0, 0, 0};
+      if (!to_lat && rg + k * groups < p.rv)
+        w0[k] = *reinterpret_cast<const u4*>(bl + (int64_t)k * groups * ldb);
+    }
+  }
   for (int r = tid; r < p.rv; r += 256) merge_channel(r);
   __syncthreads();
   if (to_lat) {                 // absorbed output: the latents go to the product pass

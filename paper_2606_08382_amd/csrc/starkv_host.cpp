@@ -55,9 +55,10 @@ int row_bytes(int qmode, int r) {
 }
 
 constexpr int kLdsLimit = 160 * 1024;
-constexpr int kMaxSplits = 64;          // context splits per sequence merged by the combine pass
+constexpr int kMaxSplits = 256;         // context splits per sequence merged by the combine pass
 constexpr int kComputeUnits = 256;
 constexpr int kMaxSplitTokens = 8192;   // tokens per split (bounds the RoPE rotation recurrence)
+constexpr int kMaxCtx = 64 * kMaxSplitTokens;   // longest context (524288 tokens)
 
 }  // namespace
 
@@ -296,26 +297,6 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
     delete P;
     return fail(STARKV_ERR_UNSUPPORTED, "no workgroup shape fits the ranks in LDS");
   }
-  // A sequence has at most kMaxSplits work items per head group, so with few
-  // sequences some compute units would idle: split the groups with the most KV
-  // heads in two until batch * kMaxSplits * n_hg covers the compute units (a
-  // part of a group that fits the LDS fits too).  Every group streams the
-  // shared value latent again, more HBM bytes on a pass that is bound by
-  // instruction issue.
-  {
-    const int want = std::min(c->n_kv_heads, (kComputeUnits + kMaxSplits * c->batch - 1) /
-                                                 (kMaxSplits * c->batch));
-    while (P->n_hg < want) {
-      int gi = 0;
-      for (int h = 1; h < P->n_hg; ++h)
-        if (P->hg_first[h + 1] - P->hg_first[h] > P->hg_first[gi + 1] - P->hg_first[gi]) gi = h;
-      const int a = P->hg_first[gi], b = P->hg_first[gi + 1];
-      if (b - a < 2) break;
-      for (int h = P->n_hg; h > gi; --h) P->hg_first[h + 1] = P->hg_first[h];
-      P->hg_first[gi + 1] = a + (b - a) / 2;
-      ++P->n_hg;
-    }
-  }
   P->ct = best_ct;
   P->lds_bytes = 0;
   int pos = 0;
@@ -428,14 +409,16 @@ int32_t starkv_decode_split_tokens(const starkv_plan* P, int32_t max_ctx) {
   if (wp.dyn) {
     // the device plan for max_ctx tokens in every sequence
     const int64_t steps = ((int64_t)max_ctx + kStepTokens - 1) / kStepTokens;
-    for (int k = wp.k_lo; k < kMaxSplits; ++k)
+    for (int k = wp.k_lo; k < kMaxSplitTokens / kStepTokens; ++k)
       if (P->cfg.batch * ((steps + k - 1) / k) <= wp.cap) return k * kStepTokens;
-    return kMaxSplits * kStepTokens;
+    return kMaxSplitTokens;
   }
   // enough splits to give every compute unit a workgroup, at most kMaxSplits
   // per sequence (the combine pass merges up to that many)
   const int64_t wgs_per_split = (int64_t)P->cfg.batch * P->n_hg;
-  int64_t splits = (256 + wgs_per_split - 1) / wgs_per_split;
+  int64_t splits = (kComputeUnits + wgs_per_split - 1) / wgs_per_split;
+  // and enough that no split exceeds kMaxSplitTokens
+  splits = std::max<int64_t>(splits, ((int64_t)max_ctx + kMaxSplitTokens - 1) / kMaxSplitTokens);
   if (splits > kMaxSplits) splits = kMaxSplits;
   int64_t len = ((int64_t)max_ctx + splits - 1) / splits;
   len = (len + kStepTokens - 1) / kStepTokens * kStepTokens;
@@ -483,9 +466,8 @@ static starkv_status check_common(const starkv_plan* P, int32_t max_ctx, size_t 
   if (max_ctx < 1) return fail(STARKV_ERR_INVALID_ARG, "max_ctx %d < 1", max_ctx);
   if (max_ctx > P->cfg.capacity)
     return fail(STARKV_ERR_CAPACITY, "max_ctx %d > capacity %d", max_ctx, P->cfg.capacity);
-  if (starkv_decode_split_tokens(P, max_ctx) > kMaxSplitTokens ||
-      (int64_t)max_ctx > (int64_t)kMaxSplits * kMaxSplitTokens)
-    return fail(STARKV_ERR_UNSUPPORTED, "max_ctx %d > %d", max_ctx, kMaxSplits * kMaxSplitTokens);
+  if (starkv_decode_split_tokens(P, max_ctx) > kMaxSplitTokens || max_ctx > kMaxCtx)
+    return fail(STARKV_ERR_UNSUPPORTED, "max_ctx %d > %d", max_ctx, kMaxCtx);
   const size_t need = starkv_decode_workspace_bytes(P, max_ctx);
   if (!ws || ws_bytes < need)
     return fail(STARKV_ERR_WORKSPACE, "decode workspace %zu bytes < %zu", ws_bytes, need);

@@ -156,6 +156,22 @@ def test_bytes_per_token_of_the_128k_workload():
     assert S.starkv_decode_splits(plan, 131072) * S.starkv_decode_split_tokens(plan, 131072) >= 131072
 
 
+@pytest.mark.parametrize("batch,max_ctx,splits_max", [(1, 524288, 256), (1, 1000, 8),
+                                                      (2, 131072, 128), (70, 100000, 256),
+                                                      (200, 524288, 256)])
+def test_split_plan_limits(batch, max_ctx, splits_max):
+    """Every split at most 8192 tokens, at most 256 splits per sequence, the splits cover
+    max_ctx; larger batches (the per-sequence split grid) also at long contexts."""
+    w = synth.WORKLOADS["c3"]
+    inp = synth.generate(synth.shrink(w, ctx=64), with_latents=False)
+    plan = S.starkv_plan_create(S.make_config(batch, 32, 8, 128, max_ctx, inp.key_rank, 256,
+                                              S.Q_MIX8_4, 5e5))
+    n, t = S.starkv_decode_splits(plan, max_ctx), S.starkv_decode_split_tokens(plan, max_ctx)
+    assert t % 128 == 0 and 128 <= t <= 8192
+    assert n * t >= max_ctx and (n - 1) * t < max_ctx and n <= splits_max
+    assert S.starkv_decode_workspace_bytes(plan, max_ctx) > 0
+
+
 def test_workspace_sizes():
     plan = S.starkv_plan_create(_cfg(d_model=256))
     assert S.starkv_append_workspace_bytes(plan, 5) >= 2 * 5 * (80 + 64) * 2

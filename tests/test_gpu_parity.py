@@ -241,9 +241,9 @@ def test_full_size_128k_sampled_heads(name):
 
 def test_longest_context_single_sequence():
     """One sequence at the longest supported context, 524288 tokens: the work plan gives it
-    64 splits of 8192 tokens (the longest split, the most splits the combine merges). The
-    whole cache bit-exact and sampled query heads of the first and last KV heads within
-    tolerance."""
+    256 splits of 2048 tokens (the most splits the combine merges, candidates read in four
+    chunks). The whole cache bit-exact and sampled query heads of the first and last KV
+    heads within tolerance."""
     w = small("c3", ctx=524288, batch=1)
     inp = synth.generate(w)
     say(f"longest context {w.name}")
