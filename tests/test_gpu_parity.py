@@ -239,6 +239,15 @@ def test_full_size_128k_sampled_heads(name):
     say(f"  absorbed output ok, last max err {e:.3e} |y| {s:.3e}")
 
 
+def test_large_batch_long_context():
+    """More than 64 sequences take the per-sequence split grid; at 40000 tokens each
+    sequence needs five splits of at most 8192 tokens (four would fill the chip). Ragged
+    lengths, the whole cache and every output against the oracle."""
+    w = small("c1", ctx=40000, batch=70, ragged=(30000, 40000))
+    inp = synth.generate(w)
+    _run_case(w, inp)
+
+
 def test_longest_context_single_sequence():
     """One sequence at the longest supported context, 524288 tokens: the work plan gives it
     256 splits of 2048 tokens (the most splits the combine merges, candidates read in four
