@@ -1328,15 +1328,12 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   }
   const float* part = p.part + ((int64_t)first * p.n_q + i) * p.part_stride;
   const int64_t sstride = (int64_t)p.n_q * p.part_stride;
-  // candidates of all splits, loaded ahead of the split weights
+  // rescoring candidates of the splits: the first 64 splits' entries are loaded
+  // ahead of the split weights.  Entry e = 32 s + j of chunk c is split 64 c + s,
+  // slot j; thread tid holds entries k * 256 + tid of a chunk, and entries past
+  // the sequence's splits are not loaded (-inf scores, never selected)
   const int n_ent = ns * kCand;
   const float2* cand = p.cand + ((int64_t)first * p.n_q + i) * kCand;
-  // (every load below reads a clamped, valid address; entries beyond the
-  // sequence's splits are masked where they are used)
-  // (addresses are a per-lane base plus wave-uniform offsets; entries beyond
-  // the sequence's splits are masked where they are used)
-  // entry e = 32 s + j of chunk c (split 64 c + s, slot j); thread tid holds
-  // entries k * 256 + tid of a chunk
   auto load_cand = [&](int c, float2 (&ce)[kCandPerThread]) {
     const float2* cl = cand + (int64_t)(64 * c + tid / kCand) * p.n_q * kCand + tid % kCand;
     const int64_t cstep = (int64_t)(256 / kCand) * p.n_q * kCand;
