@@ -374,7 +374,9 @@ int orc_append(const orc_cfg* cfg, uint8_t* cache, const uint16_t* latents,
                const int32_t* pos, int n_new) {
   append_job jobs[1024];
   pthread_t th[1024];
-  int nb = cfg->batch < 1024 ? cfg->batch : 1024;
+  /* one thread per sequence: larger batches are refused, not truncated */
+  if (cfg->batch < 0 || cfg->batch > 1024 || n_new < 0) return -1;
+  int nb = cfg->batch;
   for (int b = 0; b < nb; ++b) {
     append_job J = {cfg, cache, latents, pos, n_new, b};
     jobs[b] = J;
@@ -512,9 +514,8 @@ static void attn_task(attn_job* J, int b, int g) {
   for (int i = g * G; i < (g + 1) * G; ++i)
     if (J->want[b * Hq + i]) heads[nh++] = i;
   if (nh == 0) return;
-  int L = J->ctx_len[b];
-  if (L > cfg->capacity) L = cfg->capacity;
-  if (L <= 0) {
+  int L = J->ctx_len[b];           /* 0 <= L <= capacity (checked by run_attn) */
+  if (L == 0) {
     for (int h = 0; h < nh; ++h) {
       if (J->out)
         for (int j = 0; j < d; ++j) J->out[((int64_t)b * Hq + heads[h]) * d + j] = 0.0;
@@ -590,6 +591,12 @@ static int run_attn(const orc_cfg* cfg, const uint8_t* cache, const uint16_t* q,
                     const int32_t* ctx_len, const int32_t* sel, int n_sel,
                     double* out, double* lat, int n_threads) {
   int Hq = cfg->n_q_heads;
+  /* a context longer than the cache (or negative) is an error, not clamped */
+  for (int b = 0; b < cfg->batch; ++b)
+    if (ctx_len[b] < 0 || ctx_len[b] > cfg->capacity) return -1;
+  for (int k = 0; sel && k < n_sel; ++k)
+    if (sel[2 * k] < 0 || sel[2 * k] >= cfg->batch || sel[2 * k + 1] < 0 || sel[2 * k + 1] >= Hq)
+      return -1;
   unsigned char* want = calloc((size_t)cfg->batch * Hq, 1);
   if (sel) {
     for (int k = 0; k < n_sel; ++k) want[sel[2 * k] * Hq + sel[2 * k + 1]] = 1;

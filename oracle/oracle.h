@@ -68,7 +68,9 @@ int64_t orc_cache_bytes(const orc_cfg* cfg);
 /* byte offsets of the planes (for cross-checking the library's layout query) */
 int64_t orc_plane_offset(const orc_cfg* cfg, int which, int head);  /* which: 0 K codes, 1 K meta, 2 V codes, 3 V meta */
 
-/* append n_new tokens of latents [B][n_new][sum_r + r_v] fp16 at rows pos[b]+j */
+/* append n_new tokens of latents [B][n_new][sum_r + r_v] fp16 at rows pos[b]+j
+ * (rows outside the cache are dropped).  Returns 0, or -1 (nothing written) for a
+ * batch above 1024 or a negative n_new. */
 int orc_append(const orc_cfg* cfg, uint8_t* cache, const uint16_t* latents,
                const int32_t* pos, int n_new);
 
@@ -93,14 +95,17 @@ void orc_rope(double* v, int d, double t, double theta);
 /* decode attention.  q [B][H_q][d] (bf16 if q_is_bf16 else fp16), Bk [sum_r][d] fp16,
  * Bv [r_v][H_kv*d] fp16, ctx_len [B].  out [B][H_q][d] fp64.  If sel != NULL only the
  * n_sel (b, query head) pairs sel[2k], sel[2k+1] are computed (others untouched).
- * n_threads <= 0 means one thread per hardware core. Returns threads used. */
+ * n_threads <= 0 means one thread per hardware core. Returns threads used, or -1
+ * (nothing computed) when a ctx_len is negative or above the capacity, or a
+ * selected pair is out of range. */
 int orc_decode_attn(const orc_cfg* cfg, const uint8_t* cache, const uint16_t* q,
                     int q_is_bf16, const uint16_t* Bk, const uint16_t* Bv,
                     const int32_t* ctx_len, const int32_t* sel, int n_sel,
                     double* out, int n_threads);
 
 /* the same pass up to the normalized value latent: lat [B][H_q][r_v] fp64 gets
- * a_i / l_i (zero for ctx_len <= 0) for the selected (b, head) pairs. */
+ * a_i / l_i (zero for ctx_len == 0) for the selected (b, head) pairs; errors as
+ * for orc_decode_attn. */
 int orc_decode_latent(const orc_cfg* cfg, const uint8_t* cache, const uint16_t* q,
                       int q_is_bf16, const uint16_t* Bk, const int32_t* ctx_len,
                       const int32_t* sel, int n_sel, double* lat, int n_threads);

@@ -155,7 +155,8 @@ def append(cfg: OrcCfg, cache: np.ndarray, latents_bits: np.ndarray, pos) -> Non
     lat = np.ascontiguousarray(latents_bits, dtype=np.uint16)
     pos = np.ascontiguousarray(pos, dtype=np.int32)
     n_new = lat.shape[1]
-    lib().orc_append(C.byref(cfg), _p(cache), _p(lat), _p(pos), n_new)
+    if lib().orc_append(C.byref(cfg), _p(cache), _p(lat), _p(pos), n_new) != 0:
+        raise ValueError(f"oracle append refused: batch {cfg.batch} (at most 1024), n_new {n_new}")
 
 
 def downproj(cfg: OrcCfg, x_bits: np.ndarray, x_is_bf16: bool, A_bits: np.ndarray):
@@ -209,6 +210,9 @@ def decode_attn(cfg: OrcCfg, cache, q_bits, q_is_bf16, Bk_bits, Bv_bits, ctx_len
     nt = lib().orc_decode_attn(C.byref(cfg), _p(cache), _p(q_bits), int(q_is_bf16),
                                _p(Bk_bits), _p(Bv_bits), _p(ctx), sp, n_sel, _p(out),
                                int(n_threads))
+    if nt < 0:
+        raise ValueError("oracle decode refused: a context length outside [0, capacity] "
+                         "or a selected pair out of range")
     return out, nt
 
 
@@ -227,6 +231,9 @@ def decode_latent(cfg: OrcCfg, cache, q_bits, q_is_bf16, Bk_bits, ctx_len, sel=N
         s, n_sel, sp = None, 0, None
     nt = lib().orc_decode_latent(C.byref(cfg), _p(cache), _p(q_bits), int(q_is_bf16),
                                  _p(Bk_bits), _p(ctx), sp, n_sel, _p(lat), int(n_threads))
+    if nt < 0:
+        raise ValueError("oracle decode refused: a context length outside [0, capacity] "
+                         "or a selected pair out of range")
     return lat, nt
 
 

@@ -422,6 +422,28 @@ def test_selected_heads_match_full_run():
     assert np.array_equal(part[1, 5], full[1, 5]) and np.array_equal(part[0, 2], full[0, 2])
 
 
+def test_out_of_range_inputs_are_refused_not_truncated():
+    """A context longer than the cache, a negative one, a selected pair outside the batch, or a
+    batch above the oracle's 1024 sequences is an error: a test at those sizes cannot pass
+    vacuously on a silently shortened computation."""
+    rng = np.random.default_rng(16)
+    cfg, cache, _ = _build(O.Q_MIX8_4, 2, 8, 2, 32, 50, [16, 48], 64, rng)
+    Bk = O.f16_bits(rng.standard_normal((64, 32)) / 6)
+    Bv = O.f16_bits(rng.standard_normal((64, 64)) / 8)
+    q = O.f16_bits(rng.standard_normal((2, 8, 32)))
+    for ctx in ([51, 3], [5, -1]):
+        with pytest.raises(ValueError):
+            O.decode_attn(cfg, cache, q, False, Bk, Bv, ctx)
+        with pytest.raises(ValueError):
+            O.decode_latent(cfg, cache, q, False, Bk, ctx)
+    with pytest.raises(ValueError):
+        O.decode_attn(cfg, cache, q, False, Bk, Bv, [50, 3], sel=[(2, 0)])
+    big = O.make_cfg(1025, 1, 1, 32, 4, [16], 16, O.Q_INT4, 1e4)
+    lat = np.zeros((1025, 1, 32), np.uint16)
+    with pytest.raises(ValueError):
+        O.append(big, O.new_cache(big), lat, np.zeros(1025, np.int32))
+
+
 # ---------------------------------------------------------------- weight absorption
 
 def _dyadic(rng, shape, step):
