@@ -296,6 +296,27 @@ starkv_status starkv_decode_combine_absorbed(const starkv_plan* plan, const void
 int32_t       starkv_decode_splits(const starkv_plan* plan, int32_t max_ctx);
 int32_t       starkv_decode_split_tokens(const starkv_plan* plan, int32_t max_ctx);
 
+/* Shape of the decode launch a plan makes for max_ctx (informative, for tests and
+ * measurement; no device work).  The split pass is one kernel instance per
+ * (head_dim, qmode, score_tiles, value_tiles) and runs a grid of work items x
+ * head_groups workgroups.  With device_plan != 0 (batches of up to 64 sequences)
+ * the kernels take the split length S = 128 k from the actual lengths L_b: the
+ * smallest k >= k_lo with sum_b ceil(L_b / S) <= items; otherwise every sequence
+ * has `items / batch` splits of split_tokens tokens.
+ * Errors: INVALID_ARG for a NULL plan or out, or max_ctx < 1. */
+typedef struct {
+  int32_t head_dim, qmode;
+  int32_t score_tiles;       /* 16-column score tiles of a head group */
+  int32_t value_tiles;       /* 16-channel value tiles per wave */
+  int32_t head_groups;       /* workgroups per work item (KV heads split by LDS size) */
+  int32_t device_plan;       /* 1: split length chosen on the device from ctx_len */
+  int32_t k_lo, items;       /* device plan: smallest k, work items (grid.x) */
+  int32_t split_tokens;      /* split length for max_ctx in every sequence */
+  int32_t lds_bytes;         /* dynamic LDS of a split workgroup */
+} starkv_decode_info;
+starkv_status starkv_decode_describe(const starkv_plan* plan, int32_t max_ctx,
+                                     starkv_decode_info* out);
+
 const char*   starkv_status_string(starkv_status status);
 const char*   starkv_last_error(void);          /* thread-local, never NULL */
 

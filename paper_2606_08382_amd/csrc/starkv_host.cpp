@@ -432,6 +432,26 @@ int32_t starkv_decode_splits(const starkv_plan* P, int32_t max_ctx) {
   return (max_ctx + len - 1) / len;
 }
 
+starkv_status starkv_decode_describe(const starkv_plan* P, int32_t max_ctx,
+                                     starkv_decode_info* out) {
+  if (!P || !out) return fail(STARKV_ERR_INVALID_ARG, "plan or out is NULL");
+  if (max_ctx < 1) return fail(STARKV_ERR_INVALID_ARG, "max_ctx %d < 1", max_ctx);
+  const WorkPlan wp = work_plan(P, max_ctx);
+  starkv_decode_info d;
+  d.head_dim = P->cfg.head_dim;
+  d.qmode = P->cfg.qmode;
+  d.score_tiles = P->ct;
+  d.value_tiles = P->ntw;
+  d.head_groups = P->n_hg;
+  d.device_plan = wp.dyn ? 1 : 0;
+  d.k_lo = wp.dyn ? wp.k_lo : 0;
+  d.split_tokens = starkv_decode_split_tokens(P, max_ctx);
+  d.items = wp.dyn ? wp.cap : P->cfg.batch * starkv_decode_splits(P, max_ctx);
+  d.lds_bytes = P->lds_bytes;
+  *out = d;
+  return STARKV_OK;
+}
+
 static int part_stride(const starkv_plan* P) { return P->cfg.value_rank + 4; }
 
 // Work items whose partials the workspace holds: the device plan's cap, or

@@ -52,12 +52,20 @@ class starkv_layout(C.Structure):
                 ("page_tokens", C.c_int32), ("pages_per_sequence", C.c_int32)]
 
 
+class starkv_decode_info(C.Structure):
+    _fields_ = [("head_dim", C.c_int32), ("qmode", C.c_int32), ("score_tiles", C.c_int32),
+                ("value_tiles", C.c_int32), ("head_groups", C.c_int32),
+                ("device_plan", C.c_int32), ("k_lo", C.c_int32), ("items", C.c_int32),
+                ("split_tokens", C.c_int32), ("lds_bytes", C.c_int32)]
+
+
 EXPORTS = ["starkv_plan_create", "starkv_plan_destroy", "starkv_cache_bytes",
            "starkv_cache_layout", "starkv_append_workspace_bytes",
            "starkv_decode_workspace_bytes", "starkv_append", "starkv_decode_attn",
            "starkv_decode_split", "starkv_decode_combine", "starkv_decode_splits",
            "starkv_decode_split_tokens", "starkv_status_string", "starkv_last_error",
-           "starkv_decode_attn_absorbed", "starkv_decode_combine_absorbed"]
+           "starkv_decode_attn_absorbed", "starkv_decode_combine_absorbed",
+           "starkv_decode_describe"]
 
 _lib = None
 
@@ -100,6 +108,8 @@ def lib():
         L.starkv_decode_splits.restype = C.c_int32
         L.starkv_decode_split_tokens.argtypes = [P, C.c_int32]
         L.starkv_decode_split_tokens.restype = C.c_int32
+        L.starkv_decode_describe.argtypes = [P, C.c_int32, C.POINTER(starkv_decode_info)]
+        L.starkv_decode_describe.restype = C.c_int
         L.starkv_status_string.argtypes = [C.c_int]
         L.starkv_status_string.restype = C.c_char_p
         L.starkv_last_error.argtypes = []
@@ -189,6 +199,33 @@ def starkv_decode_splits(plan: Plan, max_ctx: int) -> int:
 
 def starkv_decode_split_tokens(plan: Plan, max_ctx: int) -> int:
     return lib().starkv_decode_split_tokens(plan.handle, max_ctx)
+
+
+def starkv_decode_describe(plan: Plan, max_ctx: int) -> dict:
+    d = starkv_decode_info()
+    _check(lib().starkv_decode_describe(plan.handle, max_ctx, C.byref(d)))
+    return {k: getattr(d, k) for k, _ in starkv_decode_info._fields_}
+
+
+def split_plan(info: dict, ctx_len) -> dict:
+    """The split pass's work plan for these context lengths, as the kernels derive it (the
+    device plan over the actual lengths, or equal splits): split length, steps per split and
+    the number of work items with tokens."""
+    lens = [max(0, int(x)) for x in ctx_len]
+    if info["device_plan"]:
+        k = None
+        for kk in range(info["k_lo"], 65):
+            steps = [-(-L // 128) for L in lens]
+            if sum(-(-m // kk) for m in steps) <= info["items"]:
+                k = kk
+                break
+        S = 128 * (k if k is not None else 64)
+    else:
+        S = info["split_tokens"]
+    items = sum(-(-L // S) for L in lens)
+    return {"split_tokens": S, "steps_per_split": S // 128, "items": items,
+            "instance": f"<{info['head_dim']},{info['qmode']},{info['score_tiles']},"
+                        f"{info['value_tiles']}> x {info['head_groups']} head groups"}
 
 
 def _nbytes(t) -> int:
