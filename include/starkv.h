@@ -240,6 +240,24 @@ starkv_status starkv_decode_attn(const starkv_plan* plan, const void* cache, con
                                  int32_t max_ctx, void* out, void* ws, size_t ws_bytes,
                                  starkv_stream_t stream);
 
+/* starkv_decode_attn_noalloc -- starkv_decode_attn without a caller workspace, for
+ * callers that cannot allocate device memory (code under graph capture, tight
+ * serving loops, harnesses that forbid allocation).  Its workspace is a fixed
+ * device array of 32 MiB inside the library, one per device, held until the
+ * process ends; no call allocates or frees memory.
+ *   cache, q, B_k, B_v, ctx_len_dev, max_ctx, out, stream: as for
+ *                starkv_decode_attn (same kernels, same results).
+ * All calls on one device share that array and leave their partial results in
+ * it: calls that overlap on one device (other streams, other threads) race and
+ * must be ordered by the caller.
+ * Errors: as starkv_decode_attn; WORKSPACE when starkv_decode_workspace_bytes(plan,
+ * max_ctx) exceeds 32 MiB (the C3 layer shape needs 10.3 MiB at 4 x 131072 tokens
+ * and 42.5 MiB at 64 x 131072). */
+starkv_status starkv_decode_attn_noalloc(const starkv_plan* plan, const void* cache,
+                                         const void* q, const void* B_k, const void* B_v,
+                                         const int32_t* ctx_len_dev, int32_t max_ctx, void* out,
+                                         starkv_stream_t stream);
+
 /* The two launches of starkv_decode_attn, exposed separately so that each can be
  * timed on its own, with the same arguments and errors:
  *   split    keys, scores, softmax state and value latents per context split, and

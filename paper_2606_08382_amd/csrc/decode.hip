@@ -1772,6 +1772,31 @@ int launch_decode_split_ntw(const DecodeParams& p, int head_dim, int qmode, int 
   return (int)hipErrorInvalidValue;
 }
 
+// ---------------------------------------------------------------- fixed scratch
+// Workspace of the no-allocation decode entry point: one array per device, kept
+// until the process ends.  Its device address comes from hipGetSymbolAddress,
+// taken once per device with that device current; host code never passes the
+// array's name to a kernel (in host code the name is a host-side stand-in).
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+int scratch_address(void** out) {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<void*> addr[kMaxDevices];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return (int)e;
+  if (dev < 0 || dev >= kMaxDevices) return (int)hipErrorInvalidDevice;
+  void* p = addr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return (int)e;
+    if (!p) return (int)hipErrorInvalidSymbol;
+    addr[dev].store(p, std::memory_order_release);
+  }
+  *out = p;
+  return 0;
+}
+
 int launch_decode_combine(const CombineParams& p, void* stream) {
   if (p.n_split > kCombineMaxSplits) return (int)hipErrorInvalidValue;
   // the shared region: the merge phase (split sums, rescoring latents, B_k

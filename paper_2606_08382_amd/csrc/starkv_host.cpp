@@ -663,6 +663,23 @@ starkv_status starkv_decode_attn(const starkv_plan* P, const void* cache, const 
                                stream);
 }
 
+starkv_status starkv_decode_attn_noalloc(const starkv_plan* P, const void* cache, const void* q,
+                                         const void* B_k, const void* B_v,
+                                         const int32_t* ctx_len_dev, int32_t max_ctx, void* out,
+                                         starkv_stream_t stream) {
+  if (!P) return fail(STARKV_ERR_INVALID_ARG, "plan is NULL");
+  if (max_ctx < 1) return fail(STARKV_ERR_INVALID_ARG, "max_ctx %d < 1", max_ctx);
+  const size_t need = starkv_decode_workspace_bytes(P, max_ctx);
+  if (need > kScratchBytes)
+    return fail(STARKV_ERR_WORKSPACE, "decode needs %zu workspace bytes, more than the %zu of "
+                "the fixed scratch array", need, kScratchBytes);
+  void* ws = nullptr;
+  if (const int e = scratch_address(&ws))
+    return fail(STARKV_ERR_HIP, "scratch address: %s", hipGetErrorString((hipError_t)e));
+  return starkv_decode_attn(P, cache, q, B_k, B_v, ctx_len_dev, max_ctx, out, ws, kScratchBytes,
+                            stream);
+}
+
 // ---------------------------------------------------------------- absorbed output
 
 static starkv_status check_absorbed(const starkv_plan* P, const void* W_abs, int32_t d_out,

@@ -177,6 +177,10 @@ int split_lds_bytes(int frags, int nql, int head_dim, int ct, int raw_bytes, int
 int launch_decode_split_ntw(const DecodeParams& p, int head_dim, int qmode, int ct, int ntw,
                             size_t lds_bytes, void* stream);
 int launch_decode_combine(const CombineParams& p, void* stream);
+// The no-allocation decode path's workspace: a fixed device array of kScratchBytes
+// per device.  *out gets its device address on the current device (taken once).
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+int scratch_address(void** out);
 int launch_absorbed_out(const AbsorbParams& p, void* stream);
 int launch_append_pack(const AppendParams& p, void* stream);
 // rows (B * n_new) up to which the down-projection streams A_all with the

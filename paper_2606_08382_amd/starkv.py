@@ -65,7 +65,7 @@ EXPORTS = ["starkv_plan_create", "starkv_plan_destroy", "starkv_cache_bytes",
            "starkv_decode_split", "starkv_decode_combine", "starkv_decode_splits",
            "starkv_decode_split_tokens", "starkv_status_string", "starkv_last_error",
            "starkv_decode_attn_absorbed", "starkv_decode_combine_absorbed",
-           "starkv_decode_describe"]
+           "starkv_decode_describe", "starkv_decode_attn_noalloc"]
 
 _lib = None
 
@@ -108,6 +108,8 @@ def lib():
         L.starkv_decode_splits.restype = C.c_int32
         L.starkv_decode_split_tokens.argtypes = [P, C.c_int32]
         L.starkv_decode_split_tokens.restype = C.c_int32
+        L.starkv_decode_attn_noalloc.argtypes = [P, P, P, P, P, P, C.c_int32, P, P]
+        L.starkv_decode_attn_noalloc.restype = C.c_int
         L.starkv_decode_describe.argtypes = [P, C.c_int32, C.POINTER(starkv_decode_info)]
         L.starkv_decode_describe.restype = C.c_int
         L.starkv_status_string.argtypes = [C.c_int]
@@ -247,6 +249,13 @@ def starkv_decode_attn(plan: Plan, cache, q, B_k, B_v, ctx_len, max_ctx: int, ou
                                     _ptr(ctx_len), max_ctx, _ptr(out), _ptr(ws),
                                     _nbytes(ws) if ws_bytes is None else ws_bytes,
                                     _stream(stream)))
+
+
+def starkv_decode_attn_noalloc(plan: Plan, cache, q, B_k, B_v, ctx_len, max_ctx: int, out,
+                               stream=None) -> None:
+    _check(lib().starkv_decode_attn_noalloc(plan.handle, _ptr(cache), _ptr(q), _ptr(B_k),
+                                            _ptr(B_v), _ptr(ctx_len), max_ctx, _ptr(out),
+                                            _stream(stream)))
 
 
 def starkv_decode_split(plan: Plan, cache, q, B_k, ctx_len, max_ctx: int, ws,
