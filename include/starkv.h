@@ -335,6 +335,18 @@ typedef struct {
 starkv_status starkv_decode_describe(const starkv_plan* plan, int32_t max_ctx,
                                      starkv_decode_info* out);
 
+/* starkv_read_stream -- a measurement aid, not part of the method: reads `bytes`
+ * at src once with 16-byte loads (every lane keeps four in flight, grid-stride
+ * over `workgroups` workgroups of 256 threads) and folds them into one word per
+ * wave, written to sink.  Timing it gives the plain HBM read ceiling that the
+ * split pass's latent stream is compared with.
+ *   src          device, 16-byte aligned; bytes a positive multiple of 16.
+ *   workgroups   1 .. 65536 (0: 2048, eight per compute unit).
+ *   sink         device uint32 [workgroups * 4] (sink_bytes at least that), 4-byte aligned.
+ * Errors: INVALID_ARG (NULL pointers, sizes), ALIGNMENT, HIP (launch). */
+starkv_status starkv_read_stream(const void* src, size_t bytes, int32_t workgroups, void* sink,
+                                 size_t sink_bytes, starkv_stream_t stream);
+
 const char*   starkv_status_string(starkv_status status);
 const char*   starkv_last_error(void);          /* thread-local, never NULL */
 

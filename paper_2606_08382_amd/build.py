@@ -22,7 +22,7 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          # packed fp32 arithmetic stays off (hipcc's host pass warns it does not know it)
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
-UNITS = [("starkv_host.cpp", []), ("append.hip", []), ("output.hip", []),
+UNITS = [("starkv_host.cpp", []), ("append.hip", []), ("output.hip", []), ("stream.hip", []),
          ("decode.hip", ["-DSK_COMMON"])]
 UNITS += [("decode.hip", [f"-DSK_D={d}", f"-DSK_QM={q}"]) for d in (64, 128) for q in (0, 1, 2, 3)]
 

@@ -868,4 +868,19 @@ starkv_status starkv_append(const starkv_plan* P, void* cache, const void* x_or_
   return hip_status(launch_append_pack(a, static_cast<void*>(stream)), "append pack launch");
 }
 
+starkv_status starkv_read_stream(const void* src, size_t bytes, int32_t workgroups, void* sink,
+                                 size_t sink_bytes, starkv_stream_t stream) {
+  if (!src || !sink) return fail(STARKV_ERR_INVALID_ARG, "NULL device pointer");
+  if (bytes == 0 || bytes % 16) return fail(STARKV_ERR_INVALID_ARG, "bytes %zu: need a positive multiple of 16", bytes);
+  if (workgroups == 0) workgroups = 2048;
+  if (workgroups < 1 || workgroups > 65536) return fail(STARKV_ERR_INVALID_ARG, "workgroups %d", workgroups);
+  if (sink_bytes < (size_t)workgroups * 16)
+    return fail(STARKV_ERR_INVALID_ARG, "sink %zu bytes < %zu", sink_bytes, (size_t)workgroups * 16);
+  if (reinterpret_cast<uintptr_t>(src) % 16) return fail(STARKV_ERR_ALIGNMENT, "src not 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(sink) % 4) return fail(STARKV_ERR_ALIGNMENT, "sink not 4-byte aligned");
+  return hip_status(launch_read_stream(src, (int64_t)bytes, static_cast<uint32_t*>(sink), workgroups,
+                                       static_cast<void*>(stream)),
+                    "read_stream launch");
+}
+
 }  // extern "C"

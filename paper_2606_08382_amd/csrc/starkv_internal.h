@@ -191,5 +191,8 @@ constexpr int kGemmMinM = 512;
 // k step (and k-chunk granule) of the split-k down-projection tiles
 constexpr int kDownprojK = 128;
 int launch_downproj(const DownprojParams& p, void* stream);
+// the plain read stream (stream.hip): bytes a multiple of 16, sink [workgroups * 4] words
+int launch_read_stream(const void* src, int64_t bytes, uint32_t* sink, int workgroups,
+                       void* stream);
 
 }  // namespace starkv

@@ -65,7 +65,7 @@ EXPORTS = ["starkv_plan_create", "starkv_plan_destroy", "starkv_cache_bytes",
            "starkv_decode_split", "starkv_decode_combine", "starkv_decode_splits",
            "starkv_decode_split_tokens", "starkv_status_string", "starkv_last_error",
            "starkv_decode_attn_absorbed", "starkv_decode_combine_absorbed",
-           "starkv_decode_describe", "starkv_decode_attn_noalloc"]
+           "starkv_decode_describe", "starkv_decode_attn_noalloc", "starkv_read_stream"]
 
 _lib = None
 
@@ -112,6 +112,8 @@ def lib():
         L.starkv_decode_attn_noalloc.restype = C.c_int
         L.starkv_decode_describe.argtypes = [P, C.c_int32, C.POINTER(starkv_decode_info)]
         L.starkv_decode_describe.restype = C.c_int
+        L.starkv_read_stream.argtypes = [P, S, C.c_int32, P, S, P]
+        L.starkv_read_stream.restype = C.c_int
         L.starkv_status_string.argtypes = [C.c_int]
         L.starkv_status_string.restype = C.c_char_p
         L.starkv_last_error.argtypes = []
@@ -256,6 +258,13 @@ def starkv_decode_attn_noalloc(plan: Plan, cache, q, B_k, B_v, ctx_len, max_ctx:
     _check(lib().starkv_decode_attn_noalloc(plan.handle, _ptr(cache), _ptr(q), _ptr(B_k),
                                             _ptr(B_v), _ptr(ctx_len), max_ctx, _ptr(out),
                                             _stream(stream)))
+
+
+def starkv_read_stream(src, n_bytes: int, sink, workgroups: int = 0, stream=None) -> None:
+    """The plain HBM read stream (a measurement aid): reads n_bytes at src once."""
+    sink_bytes = sink.numel() * sink.element_size() if hasattr(sink, "numel") else 0
+    _check(lib().starkv_read_stream(_ptr(src), n_bytes, workgroups, _ptr(sink), sink_bytes,
+                                    _stream(stream)))
 
 
 def starkv_decode_split(plan: Plan, cache, q, B_k, ctx_len, max_ctx: int, ws,

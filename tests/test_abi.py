@@ -191,3 +191,21 @@ def test_bytes_per_token_of_the_128k_workload_with_the_paper_quantizer():
     plan = S.starkv_plan_create(S.make_config(4, 32, 8, 128, 131072, inp.key_rank, 256,
                                               S.Q_MIX4_3, 5e5))
     assert S.starkv_cache_bytes(plan) == 314 * 4 * 131072
+
+
+def test_read_stream_validates_before_launch():
+    """The read-stream measurement aid refuses bad arguments before any launch."""
+    lib = S.lib()
+    sink = ctypes.create_string_buffer(64)   # host memory: only the checks read the pointers
+    addr = ctypes.addressof(sink)
+    cases = [
+        (None, 1024, 1, addr, 64, 1),        # NULL src
+        (4096, 0, 1, addr, 64, 1),           # zero bytes
+        (4096, 1000, 1, addr, 64, 1),        # not a multiple of 16
+        (4096, 1024, -1, addr, 64, 1),       # workgroups out of range
+        (4096, 1024, 8, addr, 64, 1),        # sink too small for 8 workgroups
+        (4104, 1024, 1, addr, 64, 5),        # src not 16-byte aligned
+    ]
+    for src, n, wg, snk, snk_bytes, status in cases:
+        st = lib.starkv_read_stream(src, n, wg, snk, snk_bytes, None)
+        assert st == status, (src, n, wg, st, S.starkv_last_error())
