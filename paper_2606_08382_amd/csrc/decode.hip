@@ -423,6 +423,217 @@ __device__ __forceinline__ void key_head(const HeadRt& kh, const uint8_t* raw, c
   }
 }
 
+// Dequantize a pair of codes placed in the low mantissa bits of fp16 1024 (see
+// deq_pair) with the (scale, zero) pair packed in one word: the scale and the
+// zero reach both halves of the fma through its operand selects.
+__device__ __forceinline__ uint32_t deq_pair_mz(uint32_t magic_pair, uint32_t mz) {
+  const h2 c = as_h2(magic_pair) - (h2){(_Float16)1024.0f, (_Float16)1024.0f};
+  const h2 m = as_h2(mz);
+  return as_u32(__builtin_elementwise_fma(c, __builtin_shufflevector(m, m, 0, 0),
+                                          __builtin_shufflevector(m, m, 1, 1)));
+}
+
+// The last score k-block of a head, rebuilt but not yet rotated and scored: the
+// next head finishes it after issuing its own LDS reads, so that this work
+// covers their latency and the next head's first matrix work (key_head_q).
+template <int CTH>
+struct KeyPending {
+  f4 lo[2], hi[2];   // reconstructed rows 16*kq.. and 16*kq + D/2.. per subtile
+  h8 q;              // query operand of that k-block
+  int ct;            // score tile of the head within the half
+};
+
+// Rotate one k-block of rebuilt keys (rows j and j + D/2 of the lane's token, in
+// fp32) by the lane's fixed RoPE rotation, in packed fp16, and accumulate the
+// scores of the head's query columns.
+template <int CTH>
+__device__ __forceinline__ void rotate_score(const f4& a, const f4& bb, const CS4& r, const h8& qf,
+                                             int ct, f4 (&acc)[CTH]) {
+  const h2 a01 = __builtin_convertvector((f2){a[0], a[1]}, h2);
+  const h2 a23 = __builtin_convertvector((f2){a[2], a[3]}, h2);
+  const h2 b01 = __builtin_convertvector((f2){bb[0], bb[1]}, h2);
+  const h2 b23 = __builtin_convertvector((f2){bb[2], bb[3]}, h2);
+  u4 kr;
+  kr[0] = as_u32(__builtin_elementwise_fma(a01, r.c01, -(b01 * r.s01)));
+  kr[1] = as_u32(__builtin_elementwise_fma(a23, r.c23, -(b23 * r.s23)));
+  kr[2] = as_u32(__builtin_elementwise_fma(b01, r.c01, a01 * r.s01));
+  kr[3] = as_u32(__builtin_elementwise_fma(b23, r.c23, a23 * r.s23));
+  const h8 kop = __builtin_bit_cast(h8, kr);
+#pragma unroll
+  for (int c = 0; c < CTH; ++c)
+    if (CTH == 1 || c == ct) acc[c] = mfma16(kop, qf, acc[c]);
+}
+
+template <int D, int CTH>
+__device__ __forceinline__ void key_drain(const KeyPending<CTH>& pd, const CS4 (&cs)[2][D / 32],
+                                          f4 (&acc_s)[2][CTH]) {
+#pragma unroll
+  for (int s = 0; s < 2; ++s) rotate_score<CTH>(pd.lo[s], pd.hi[s], cs[s][D / 32 - 1], pd.q, pd.ct, acc_s[s]);
+}
+
+// key_head for the 4-bit and the 8-bit/4-bit caches.  In these formats a head
+// with KB k-blocks has exactly KB 8-bit chunks (8 * ceil(r / 32) outlier
+// channels) or none, so only k-block 0 mixes the two widths (lanes of chunk quad
+// < KB read 8 bytes, the others 4), and every LDS offset is a per-lane constant
+// plus a compile-time part: lc4 = 64 quad + 4 tcol (4-bit chunk layout), lc8 =
+// 128 quad + 8 tcol (8-bit).  A lane reads two words of k-block 0 (8-bit lanes
+// the two words of their 8 codes, 4-bit lanes the same word twice) and spreads
+// them into bytes with a per-lane shift and mask, so both widths run the same
+// instructions.  The head runs as a pipeline over its score k-blocks: the
+// matrix cores rebuild k-block kbs while the rotation and scores of kbs - 1 run
+// on the vector ALUs, the fragments of kbs + 1 and the query operand of kbs are
+// read one stage ahead, and the last k-block is left pending for the next head
+// (or the caller's drain).
+template <int D, int QM, int CTH, int KB>
+__device__ __forceinline__ void key_head_q(const HeadRt& kh, const uint8_t* raw, const h8* frag,
+                                           const _Float16* qc, int qzero, int gl, int ct0, int G,
+                                           int lane, int col, int tcol, int quad, int lc4, int lc8,
+                                           const CS4 (&cs)[2][D / 32], f4 (&acc_s)[2][CTH],
+                                           KeyPending<CTH>& pend) {
+  constexpr bool MIX = QM == STARKV_Q_MIX8_4;
+  constexpr int NKBS = D / 32;
+  constexpr int QS = D + 8;
+  constexpr int X4 = MIX ? 64 * KB : 0;      // first 4-bit chunk of a 16-token block
+  const bool is8 = MIX && quad < KB;          // k-block 0 chunk of this lane is 8-bit
+  const int rb16 = 16 * kh.row_bytes;         // bytes of one 16-token block
+  const int mg64 = 64 * kh.ngroups;           // meta bytes of one 16-token block
+  const uint8_t* rc = raw + kh.raw_code;
+  // group of chunk 4 kb + quad: kb + 1 for the 4-bit chunks of a mixed head, kb otherwise
+  const uint8_t* rm = raw + kh.raw_meta + 4 * tcol + ((MIX && quad >= KB) ? 64 : 0);
+  // Lanes whose chunk of the last k-block lies beyond the rank read the codes and
+  // group 0's meta of chunk 0 instead: finite values that meet zero fragment rows.
+  const bool vlast = 8 * (4 * (KB - 1) + quad) < kh.rank;
+  const uint8_t* rm0 = raw + kh.raw_meta + 4 * tcol;
+  const uint8_t* rml = vlast ? rm : rm0;
+  const int a0 = (KB > 1 || vlast) ? (is8 ? lc8 : lc4 + X4) : 8 * tcol;
+  const int a0b = (KB > 1 || vlast) ? (is8 ? lc8 + 4 : lc4 + X4) : 8 * tcol;
+  const int alast = vlast ? lc4 + X4 + 256 * (KB - 1) : 8 * tcol;
+  const uint32_t mk0 = is8 ? 0xFFFFFFFFu : 0x0F0F0F0Fu;
+  const uint32_t sh0 = is8 ? 0u : 4u;
+  const int ct_g = (gl * G) / 16 - ct0;      // score tile of this head within the half
+  const int c_lo = (gl * G) % 16;
+  const bool mine = col >= c_lo && col < c_lo + G;
+  const _Float16* qb = qc + (mine ? (((gl * G) / 16) * 16 + col) * QS : qzero) + quad * 8;
+  const h8* fr = frag + kh.frag_base * 64 + lane;
+  // the codes and meta of this head's tokens
+  uint32_t w0[2], w1[2], wk[2][KB], mz[2][KB];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      if (kb == 0) {
+        w0[s] = *reinterpret_cast<const uint32_t*>(rc + s * rb16 + a0);
+        w1[s] = *reinterpret_cast<const uint32_t*>(rc + s * rb16 + a0b);
+      } else {
+        const int a = kb == KB - 1 ? alast : lc4 + X4 + 256 * kb;
+        wk[s][kb] = *reinterpret_cast<const uint32_t*>(rc + s * rb16 + a);
+      }
+      mz[s][kb] = kb == KB - 1
+          ? *reinterpret_cast<const uint32_t*>(rml + s * mg64 + (vlast ? 64 * kb : 0))
+          : *reinterpret_cast<const uint32_t*>(rm + s * mg64 + 64 * kb);
+    }
+  }
+  // heads of up to two k-blocks read the next stage's fragments one stage ahead
+  // (two buffers); larger ones read a stage's fragments at its start.  The
+  // query operand of a stage is read one stage ahead.
+  constexpr bool kAhead = KB <= 2;
+  h8 alo[KB], ahi[KB];
+  if (kAhead) {
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      alo[kb] = fr[kb * 64];
+      ahi[kb] = fr[(NKBS * KB + kb) * 64];
+    }
+  }
+  h8 qcur = *reinterpret_cast<const h8*>(qb);
+  __builtin_amdgcn_sched_barrier(0);
+  // the previous head's last k-block while these reads are in flight
+  key_drain<D, CTH>(pend, cs, acc_s);
+  __builtin_amdgcn_sched_barrier(0);
+  h8 xop[2][KB];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      uint32_t lo, hi;
+      if (kb == 0) {
+        lo = w0[s] & mk0;
+        hi = (w1[s] >> sh0) & mk0;
+      } else {
+        lo = wk[s][kb] & 0x0F0F0F0Fu;
+        hi = (wk[s][kb] >> 4) & 0x0F0F0F0Fu;
+      }
+      u4 v;
+      v.x = deq_pair_mz(perm(0x64646464u, lo, 0x05010400u), mz[s][kb]);
+      v.y = deq_pair_mz(perm(0x64646464u, lo, 0x05030402u), mz[s][kb]);
+      v.z = deq_pair_mz(perm(0x64646464u, hi, 0x05010400u), mz[s][kb]);
+      v.w = deq_pair_mz(perm(0x64646464u, hi, 0x05030402u), mz[s][kb]);
+      xop[s][kb] = __builtin_bit_cast(h8, v);
+    }
+  }
+  f4 klo[2][2], khi[2][2];   // [buffer][subtile]
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int kbs = 0; kbs < NKBS; ++kbs) {
+    h8 nlo[KB], nhi[KB], qnext;
+    if (kbs > 0) qnext = *reinterpret_cast<const h8*>(qb + kbs * 32);
+    const int ks = kAhead ? kbs + 1 : kbs;   // stage whose fragments are read now
+    if (ks < NKBS) {
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        nlo[kb] = fr[(ks * KB + kb) * 64];
+        nhi[kb] = fr[((ks + NKBS) * KB + kb) * 64];
+      }
+    }
+    if (!kAhead) {
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        alo[kb] = nlo[kb];
+        ahi[kb] = nhi[kb];
+      }
+    }
+    // keep the fragment reads ahead of this stage's matrix work
+    __builtin_amdgcn_sched_barrier(0);
+    {                        // reconstruct rows 16*kbs.. and 16*kbs + D/2..
+      const int bufn = kbs & 1;
+#pragma unroll
+      for (int s = 0; s < 2; ++s) { klo[bufn][s] = (f4){0, 0, 0, 0}; khi[bufn][s] = (f4){0, 0, 0, 0}; }
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+          klo[bufn][s] = mfma16(alo[kb], xop[s][kb], klo[bufn][s]);
+          khi[bufn][s] = mfma16(ahi[kb], xop[s][kb], khi[bufn][s]);
+          // in this order, first: left to itself the scheduler sinks them to the
+          // end of the stage, where the next stage's rotation waits on them
+          __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+    if (kbs > 0) {           // rotate and score k-block kbs-1
+      const int kq = kbs - 1, buf = kq & 1;
+#pragma unroll
+      for (int s = 0; s < 2; ++s) rotate_score<CTH>(klo[buf][s], khi[buf][s], cs[s][kq], qcur, ct_g, acc_s[s]);
+    }
+    if (kAhead && kbs + 1 < NKBS) {
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        alo[kb] = nlo[kb];
+        ahi[kb] = nhi[kb];
+      }
+    }
+    if (kbs > 0) qcur = qnext;
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  // the last k-block waits for the next head (or the caller's drain)
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    pend.lo[s] = klo[(NKBS - 1) & 1][s];
+    pend.hi[s] = khi[(NKBS - 1) & 1][s];
+  }
+  pend.q = qcur;
+  pend.ct = ct_g;
+}
+
 // The group's query heads rotated to the step's base position t (RoPE applied to
 // the query as R(t)^T q, so that q . R(t + u) k = (R(t)^T q) . (R(u) k)), one
 // padded fp16 row per head, permuted so that lane (col, quad) of score k-block
@@ -472,8 +683,11 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int tg = w & (kTokenGroups - 1);   // token group: tokens 32*tg.. of each step
-  const int hh = w / kTokenGroups;         // half of the group's KV heads
+  // Waves w and w + 4 share a SIMD; they take the same half of the heads (and
+  // so the same work) on different tokens, so that neither runs alone on its
+  // SIMD at the end of the key phase.
+  const int hh = w & 1;                    // half of the group's KV heads
+  const int tg = w >> 1;                   // token group: tokens 32*tg.. of each step
   const int col = lane & 15, quad = lane >> 4;
   // Token order of the score tiles: row 4*quad + e of a 16-token subtile is
   // token 4*e + quad, so a lane's rows are tokens quad, quad+4, quad+8,
@@ -482,6 +696,8 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   // reconstruction reads token tcol into MFMA column col, and the value chunks
   // hold their slots in the same order.
   const int tcol = 4 * (col & 3) + (col >> 2);
+  // LDS offsets of this lane's key codes inside a 16-token block (4-bit and 8-bit chunk layouts)
+  const int lc4 = 64 * quad + 4 * tcol, lc8 = 128 * quad + 8 * tcol;
   const int hg = blockIdx.z;
   const int g0 = p.hg_first[hg], g1 = p.hg_first[hg + 1], gm = p.hg_mid[hg];
   const int G = p.group_q;
@@ -581,7 +797,6 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   float* red = reinterpret_cast<float*>(smem + LL.red);
   float* alpha_s = reinterpret_cast<float*>(smem + LL.alpha);
   int* flag_s = reinterpret_cast<int*>(smem + LL.flag);
-  int* prog_s = reinterpret_cast<int*>(smem + LL.prog);   // key-phase progress per wave
   float2* rot_s = reinterpret_cast<float2*>(smem + LL.rot);        // [64] step rotations
   int* qmap = reinterpret_cast<int*>(smem + LL.qmap);             // slot-local -> query head
   uint8_t* raw = smem + LL.raw + w * raw_bytes;
@@ -877,16 +1092,6 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 #pragma unroll
     for (int t = 0; t < NTW; ++t) acc_v[c][t] = (f4){0, 0, 0, 0};
 
-  // key cost per step of this wave's half and of the other half (units of
-  // 2 + k-blocks per head, as the host balances them)
-  int cost_me = 0, cost_other = 0;
-#pragma unroll
-  for (int k = 1; k <= NKBS; ++k) {
-    cost_me += (p.cls[hg][hh][k] - p.cls[hg][hh][k - 1]) * (2 + k);
-    cost_other += (p.cls[hg][1 - hh][k] - p.cls[hg][1 - hh][k - 1]) * (2 + k);
-  }
-  int prog = 0;
-  if (lane == 0) prog_s[w] = 0;
   load_v(0);
   __syncthreads();   // rotated queries of step 0 and the fragments visible
 
@@ -905,33 +1110,34 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     for (int s = 0; s < 2; ++s)
 #pragma unroll
       for (int c = 0; c < CTH; ++c) acc_s[s][c] = (f4){0, 0, 0, 0};
+    // nothing pending before the first head: a zero k-block adds nothing
+    KeyPending<CTH> pend;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) { pend.lo[s] = (f4){0, 0, 0, 0}; pend.hi[s] = (f4){0, 0, 0, 0}; }
+    pend.q = (h8){0, 0, 0, 0, 0, 0, 0, 0};
+    pend.ct = 0;
 
-    // The two waves sharing a SIMD (w and w ^ 4, one per head half) split its
-    // issue slots unevenly: at equal priority the older wave (w < 4) wins, and
-    // the younger ends up running its last heads alone.  After every head a
-    // wave compares its share of the key work done (cumulative cost over the
-    // half's cost per step) with its partner's and takes the higher priority
-    // while it is behind; the younger also takes it on a tie.
 #pragma unroll
     for (int k = 1; k <= NKBS; ++k) {
       for (int i = cls_end[k - 1]; i < cls_end[k]; ++i) {
-        const int partner = prog_s[w ^ 4];
         const HeadRt kh = head_rt(i);
-        if (k == 1) key_head<D, QM, CTH, 1>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, cs, acc_s);
-        if (k == 2) key_head<D, QM, CTH, 2>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, cs, acc_s);
-        if (NKBS > 2 && k == 3) key_head<D, QM, CTH, (NKBS > 2 ? 3 : 1)>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, cs, acc_s);
-        if (NKBS > 3 && k == 4) key_head<D, QM, CTH, (NKBS > 3 ? 4 : 1)>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, cs, acc_s);
+        if constexpr (QM == STARKV_Q_INT4 || QM == STARKV_Q_MIX8_4) {
+          if (k == 1) key_head_q<D, QM, CTH, 1>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, lc4, lc8, cs, acc_s, pend);
+          if (k == 2) key_head_q<D, QM, CTH, 2>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, lc4, lc8, cs, acc_s, pend);
+          if (NKBS > 2 && k == 3) key_head_q<D, QM, CTH, (NKBS > 2 ? 3 : 1)>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, lc4, lc8, cs, acc_s, pend);
+          if (NKBS > 3 && k == 4) key_head_q<D, QM, CTH, (NKBS > 3 ? 4 : 1)>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, lc4, lc8, cs, acc_s, pend);
+        } else {
+          if (k == 1) key_head<D, QM, CTH, 1>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, cs, acc_s);
+          if (k == 2) key_head<D, QM, CTH, 2>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, cs, acc_s);
+          if (NKBS > 2 && k == 3) key_head<D, QM, CTH, (NKBS > 2 ? 3 : 1)>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, cs, acc_s);
+          if (NKBS > 3 && k == 4) key_head<D, QM, CTH, (NKBS > 3 ? 4 : 1)>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, cs, acc_s);
+        }
         // the head's staging has been read (its values are consumed): copy
         // the next step's codes and meta of this head into it
         if (step + 1 < n_steps) copy_head(kh, kblk_next);
-        prog += 2 + k;
-        if (lane == 0) prog_s[w] = prog;
-        const int mine_n = prog * cost_other, part_n = partner * cost_me;
-        if (part_n > mine_n || (hh == 1 && part_n == mine_n)) __builtin_amdgcn_s_setprio(1);
-        else __builtin_amdgcn_s_setprio(0);
       }
     }
-    __builtin_amdgcn_s_setprio(0);
+    if constexpr (QM == STARKV_Q_INT4 || QM == STARKV_Q_MIX8_4) key_drain<D, CTH>(pend, cs, acc_s);
 
     // ------------------------------------------ online softmax (log2 domain)
     // scores are already in log2 units (the query carries log2(e)/sqrt(d))
