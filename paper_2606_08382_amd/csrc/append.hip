@@ -194,11 +194,17 @@ __device__ __forceinline__ void pack_token(const AppendParams& p, const PackGrou
         unsigned int* wp = reinterpret_cast<unsigned int*>(p.cache) + abit / 32;
         const int s0 = (int)(abit % 32);
         const uint32_t fmask = (1u << bits) - 1;
-        atomicAnd(wp, ~(fmask << s0));
-        atomicOr(wp, code << s0);
-        if (s0 + bits > 32) {                // the field's high bits in the next word
-          atomicAnd(wp + 1, ~(fmask >> (32 - s0)));
-          atomicOr(wp + 1, code >> (32 - s0));
+        if (p.single_writer && bits == 4) {
+          // at most four new tokens per sequence: every 4-bit word (eight tokens
+          // four apart) has one writer in this launch
+          *wp = (*wp & ~(fmask << s0)) | (code << s0);
+        } else {
+          atomicAnd(wp, ~(fmask << s0));
+          atomicOr(wp, code << s0);
+          if (s0 + bits > 32) {                // the field's high bits in the next word
+            atomicAnd(wp + 1, ~(fmask >> (32 - s0)));
+            atomicOr(wp + 1, code >> (32 - s0));
+          }
         }
       }
     }
@@ -215,14 +221,9 @@ __device__ __forceinline__ void pack_token(const AppendParams& p, const PackGrou
 // as fp16 and a wave takes TPW tokens of one group, their loads issued together.
 // Two instances, so that the large prefill pack keeps a small register
 // footprint and several tokens' latency chains overlap.
-template <bool PARTIAL, int TPW>
-__global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
-  const int lane = threadIdx.x & 63;
-  const int wid = blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
-  const int n_tok = p.batch * p.n_new;
-  const int n_tb = (n_tok + TPW - 1) / TPW;
-  if (wid >= n_tb * p.n_items) return;
-  const int tb = wid / p.n_items, item = wid % p.n_items;
+// The quantization group of work item `item`: its block (a key head or the
+// value latent), region, channels c0 .. c0 + n - 1 of the block and bit width.
+__device__ __forceinline__ PackGroup make_group(const AppendParams& p, int item) {
   PackGroup G;
   G.bl = p.item_block[item];
   G.gi = p.item_group[item];
@@ -241,6 +242,18 @@ __global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
     if (G.gi < ngo) { G.c0 = 32 * G.gi; G.n = min(32, G.ro - G.c0); G.bits = G.hb; }
     else { G.c0 = G.ro + 32 * (G.gi - ngo); G.n = min(32, r - G.c0); G.bits = G.lb; }
   }
+  return G;
+}
+
+template <bool PARTIAL, int TPW>
+__global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
+  const int lane = threadIdx.x & 63;
+  const int wid = blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
+  const int n_tok = p.batch * p.n_new;
+  const int n_tb = (n_tok + TPW - 1) / TPW;
+  if (wid >= n_tb * p.n_items) return;
+  const int tb = wid / p.n_items, item = wid % p.n_items;
+  const PackGroup G = make_group(p, item);
   const bool on = lane < G.n;
   const int c = G.c0 + lane;
   uint16_t xb[TPW];

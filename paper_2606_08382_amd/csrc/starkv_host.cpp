@@ -793,6 +793,41 @@ starkv_status starkv_append(const starkv_plan* P, void* cache, const void* x_or_
   const float* partial = nullptr;
   uint16_t* lat_out = nullptr;
   int k_split = 0;
+  AppendParams a;
+  std::memset(&a, 0, sizeof(a));
+  a.cache = static_cast<uint8_t*>(cache);
+  a.pos = pos_dev;
+  a.batch = c.batch;
+  a.n_new = n_new;
+  a.width = P->width;
+  a.capacity = c.capacity;
+  a.rmap = P->rmap;
+  a.qmode = c.qmode;
+  a.single_writer = n_new <= 4;
+  a.n_kv = c.n_kv_heads;
+  {
+    int lo = 0;
+    a.n_items = 0;
+    for (int bl = 0; bl <= c.n_kv_heads; ++bl) {
+      const bool v = bl == c.n_kv_heads;
+      const int r = v ? c.value_rank : c.key_rank[bl];
+      a.rank[bl] = r;
+      a.lat_off[bl] = lo;
+      lo += r;
+      a.ro[bl] = v ? P->layout.value_outlier_channels : P->layout.key_outlier_channels[bl];
+      a.ng[bl] = v ? P->layout.value_groups : P->layout.key_groups[bl];
+      a.row_bytes[bl] = v ? P->layout.value_row_bytes : P->layout.key_row_bytes[bl];
+      a.code_off[bl] = v ? P->layout.value_code_offset : P->layout.key_code_offset[bl];
+      a.meta_off[bl] = v ? P->layout.value_meta_offset : P->layout.key_meta_offset[bl];
+      const int items = c.qmode == STARKV_Q_F16 ? (r + 31) / 32 : a.ng[bl];
+      for (int i = 0; i < items; ++i) {
+        if (a.n_items >= 128) return fail(STARKV_ERR_UNSUPPORTED, "too many quantization groups");
+        a.item_block[a.n_items] = bl;
+        a.item_group[a.n_items] = i;
+        ++a.n_items;
+      }
+    }
+  }
   if (c.d_model > 0) {
     if (reinterpret_cast<uintptr_t>(x_or_latents) % 16)
       return fail(STARKV_ERR_ALIGNMENT, "x not 16-byte aligned");
@@ -829,42 +864,10 @@ starkv_status starkv_append(const starkv_plan* P, void* cache, const void* x_or_
   } else if (reinterpret_cast<uintptr_t>(x_or_latents) % 2) {
     return fail(STARKV_ERR_ALIGNMENT, "latents not 2-byte aligned");
   }
-  AppendParams a;
-  std::memset(&a, 0, sizeof(a));
-  a.cache = static_cast<uint8_t*>(cache);
   a.lat = lat;
   a.partial = partial;
   a.lat_out = lat_out;
   a.k_split = k_split;
-  a.pos = pos_dev;
-  a.batch = c.batch;
-  a.n_new = n_new;
-  a.width = P->width;
-  a.capacity = c.capacity;
-  a.rmap = P->rmap;
-  a.qmode = c.qmode;
-  a.n_kv = c.n_kv_heads;
-  int lo = 0;
-  a.n_items = 0;
-  for (int bl = 0; bl <= c.n_kv_heads; ++bl) {
-    const bool v = bl == c.n_kv_heads;
-    const int r = v ? c.value_rank : c.key_rank[bl];
-    a.rank[bl] = r;
-    a.lat_off[bl] = lo;
-    lo += r;
-    a.ro[bl] = v ? P->layout.value_outlier_channels : P->layout.key_outlier_channels[bl];
-    a.ng[bl] = v ? P->layout.value_groups : P->layout.key_groups[bl];
-    a.row_bytes[bl] = v ? P->layout.value_row_bytes : P->layout.key_row_bytes[bl];
-    a.code_off[bl] = v ? P->layout.value_code_offset : P->layout.key_code_offset[bl];
-    a.meta_off[bl] = v ? P->layout.value_meta_offset : P->layout.key_meta_offset[bl];
-    const int items = c.qmode == STARKV_Q_F16 ? (r + 31) / 32 : a.ng[bl];
-    for (int i = 0; i < items; ++i) {
-      if (a.n_items >= 128) return fail(STARKV_ERR_UNSUPPORTED, "too many quantization groups");
-      a.item_block[a.n_items] = bl;
-      a.item_group[a.n_items] = i;
-      ++a.n_items;
-    }
-  }
   return hip_status(launch_append_pack(a, static_cast<void*>(stream)), "append pack launch");
 }
 

@@ -144,6 +144,7 @@ struct AppendParams {
   int32_t k_split;
   const int32_t* pos;
   int32_t batch, n_new, width, capacity, qmode;
+  int32_t single_writer;       // every 4-bit value word has one writer (n_new <= 4)
   RowMap rmap;
   int32_t n_kv;
   // per block: 0..n_kv-1 key heads, n_kv = values
