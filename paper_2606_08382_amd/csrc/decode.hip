@@ -1074,18 +1074,18 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 
   // ---------------------------------------------------------------- main loop
   float m_run[CTH], l_part[CTH];
-  // the largest score this lane has seen per tile and subtile, with its token
-  // (offset from t_begin minus the lane's 32*tg + 4*quad): the combine pass
-  // rescores the dominant tokens exactly
-  float bx[CTH][2];
-  int bt[CTH][2];
+  // The two largest scores this lane has seen per tile and subtile (its slot:
+  // the tokens 32*tg + 16*s + quad + 4*e of every step), each carrying its
+  // token as 4*step + e in the low 8 bits: the combine pass rescores the
+  // dominant tokens exactly.
+  float b1[CTH][2], b2[CTH][2];
   f4 acc_v[CT][NTW];
 #pragma unroll
   for (int c = 0; c < CTH; ++c) {
     m_run[c] = -INFINITY;
     l_part[c] = 0.0f;
-    bx[c][0] = bx[c][1] = -INFINITY;
-    bt[c][0] = bt[c][1] = 0;
+    b1[c][0] = b1[c][1] = -INFINITY;
+    b2[c][0] = b2[c][1] = -INFINITY;
   }
 #pragma unroll
   for (int c = 0; c < CT; ++c)
@@ -1141,13 +1141,18 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 
     // ------------------------------------------ online softmax (log2 domain)
     // scores are already in log2 units (the query carries log2(e)/sqrt(d))
+    // the token of a score (4*step + e, below 256: a split has at most 64
+    // steps) replaces the low 8 of its 24 significand bits, a change far below
+    // the score's fp16 error; the softmax and the rescoring both use the result
     float x[CTH][2][4];
 #pragma unroll
     for (int c = 0; c < CTH; ++c)
 #pragma unroll
       for (int s = 0; s < 2; ++s)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) x[c][s][e] = acc_s[s][c][e];
+        for (int e = 0; e < 4; ++e)
+          x[c][s][e] = __uint_as_float((__float_as_uint(acc_s[s][c][e]) & 0xFFFFFF00u) |
+                                       (uint32_t)(4 * step + e));
     if (!full) {
 #pragma unroll
       for (int s = 0; s < 2; ++s)
@@ -1177,9 +1182,8 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
         for (int e = 0; e < 4; ++e) {
           const float v = x[c][s][e];
           mx = fmaxf(mx, v);
-          const bool gt = v > bx[c][s];
-          bt[c][s] = gt ? step * kStepTokens + 16 * s + 4 * e : bt[c][s];
-          bx[c][s] = fmaxf(bx[c][s], v);
+          b2[c][s] = fmaxf(b2[c][s], fminf(b1[c][s], v));   // the slot's top two
+          b1[c][s] = fmaxf(b1[c][s], v);
         }
       mx = wave_max16(mx);
       if (quad == 0) red[(ct * 16 + col) * kTokenGroups + tg] = mx;
@@ -1345,10 +1349,17 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     if (c >= ctn) break;
     const int il = (ct0 + c) * 16 + col;
     if (il < nql) {
-      float2* cd = p.cand + (pbase + qmap[il]) * kCand + (tg * 4 + quad) * 2;
+      float2* cd = p.cand + (pbase + qmap[il]) * kCand + (tg * 4 + quad) * 4;
+      auto token = [&](float v, int s) {
+        const uint32_t k = __float_as_uint(v) & 0xFFu;
+        return __int_as_float(t_begin + (int)(k >> 2) * kStepTokens + 4 * (int)(k & 3u) + 16 * s +
+                              32 * tg + quad);
+      };
 #pragma unroll
-      for (int s = 0; s < 2; ++s)
-        cd[s] = make_float2(bx[c][s], __int_as_float(t_begin + bt[c][s] + 32 * tg + quad));
+      for (int s = 0; s < 2; ++s) {
+        cd[2 * s] = make_float2(b1[c][s], token(b1[c][s], s));
+        cd[2 * s + 1] = make_float2(b2[c][s], token(b2[c][s], s));
+      }
     }
   }
   if (tg == 0 && quad == 0) {
@@ -1401,7 +1412,8 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 // normalizer and to the merged value latent is moved from the approximate to the
 // exact weight.
 constexpr int kCombineMaxSplits = 256;  // one split per thread of the weight pass
-constexpr int kRescoreMax = 32;                        // tokens rescored per query head
+constexpr int kRescoreMax = 128;                       // tokens rescored per query head
+constexpr int kRescoreBatch = 32;                      // of them with key latents in LDS at once
 constexpr float kRescoreTau = 1.0f / 64.0f;
 constexpr int kBkVecPerThread = 8;   // B_k block of up to 128 x 128 fp16: 2048 vectors / 256 threads
 // candidate entries are read in chunks of 64 splits, kCandPerThread per thread
@@ -1493,8 +1505,8 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   // latent is in `a`, the up-projection's partial sums.
   float* uni = sm + combine_head_floats(p.rv);
   float* red4 = uni;                                   // [4][rv] per-wave split sums
-  float* lat = red4 + 4 * p.rv;                        // [kRescoreMax][rmax] key latents
-  uint16_t* bks = reinterpret_cast<uint16_t*>(lat + kRescoreMax * p.rmax);  // [rmax][D] fp16
+  float* lat = red4 + 4 * p.rv;                        // [kRescoreBatch][rmax] key latents
+  uint16_t* bks = reinterpret_cast<uint16_t*>(lat + kRescoreBatch * p.rmax);  // [rmax][D] fp16
   float* red = uni;                                    // [256 / (D/8)][D] partial up-projections
   const int i = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   // output columns c_0 .. c_0 + Dc - 1 of this workgroup (the merge and the
@@ -1675,8 +1687,10 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
       if (prio[k] >= tau) {
         const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal[k] >> 32),
                                                    __builtin_amdgcn_mbcnt_lo((uint32_t)bal[k], 0));
-        c_x[off + rank] = ce[k].x;
-        c_t[off + rank] = __float_as_int(ce[k].y);
+        if (off + rank < kRescoreMax) {
+          c_x[off + rank] = ce[k].x;
+          c_t[off + rank] = __float_as_int(ce[k].y);
+        }
       }
       base += kcnt[4 * k] + kcnt[4 * k + 1] + kcnt[4 * k + 2] + kcnt[4 * k + 3];
     }
@@ -1697,11 +1711,13 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
       __syncthreads();
       n_sel = kcnt[0] + kcnt[1] + kcnt[2] + kcnt[3];
       __syncthreads();
-      if (n_sel <= kRescoreMax) break;
+      if (n_sel <= kRescoreMax || it == kLevels - 1) break;
       tau *= 4.0f;
     }
-    if (n_sel > kRescoreMax) n_sel = 0;   // too flat to matter at any threshold tried
+    // past the cap at every threshold tried (at least kRescoreMax tokens each
+    // holding that much): the first kRescoreMax of the last one, in entry order
     if (n_sel > 0) compact(ce0, prio, tau, 0);
+    n_sel = min(n_sel, kRescoreMax);
   } else {
     // entries at or above threshold j, per thread, in 16-bit fields (field j % 2
     // of word j / 2; at most 32 per thread and 2048 per wave)
@@ -1731,10 +1747,9 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
     for (int j = 0; j < kLevels; ++j) {
       n_sel = 0;
       for (int ww = 0; ww < 4; ++ww) n_sel += ((uint32_t)kcnt[4 * (j / 2) + ww] >> (16 * (j % 2))) & 0xFFFFu;
-      if (n_sel <= kRescoreMax) break;
+      if (n_sel <= kRescoreMax || j == kLevels - 1) break;
       tau *= 4.0f;
     }
-    if (n_sel > kRescoreMax) n_sel = 0;
     __syncthreads();                     // the counts are read before kcnt is rewritten
     if (n_sel > 0) {
       int base = 0;
@@ -1746,6 +1761,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
         base = compact(ce, prio, tau, base);
       }
     }
+    n_sel = min(n_sel, kRescoreMax);
   }
   if (n_sel > 0) {
     // one round of loads for the rescoring: the KV head's up-projection block
@@ -1761,23 +1777,27 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
 #pragma unroll
     for (int k = 0; k < kBkVecPerThread; ++k)
       if (tid + k * 256 < nbk) reinterpret_cast<u4*>(bks)[tid + k * 256] = bkv[k];
-    // ---- exact scores: dequantized key latents of every candidate, then one
-    // (candidate, RoPE pair) item per thread; the items of a candidate are
-    // consecutive lanes of one wave and are summed with shuffles
+    // ---- exact scores, kRescoreBatch candidates at a time: their dequantized
+    // key latents, then one (candidate, RoPE pair) item per thread; the items of
+    // a candidate are consecutive lanes of one wave and are summed with shuffles
     const int HALF = D / 2;
-    for (int it = tid; it < n_sel * r_g; it += 256) {
-      const int j = it / r_g, ch = it % r_g;
-      lat[j * p.rmax + ch] = key_latent(p, g, b, c_t[j], ch);
-    }
-    __syncthreads();
     const uint16_t* bk = bks;
     const uint16_t* qs = static_cast<const uint16_t*>(p.q) + ((int64_t)b * p.n_q + i) * D;
-    for (int it0 = 0; it0 < n_sel * HALF; it0 += 256) {
+    for (int j0 = 0; j0 < n_sel; j0 += kRescoreBatch) {
+    const int nb = min(kRescoreBatch, n_sel - j0);
+    if (j0 > 0) __syncthreads();         // the previous batch's latents are read
+    for (int it = tid; it < nb * r_g; it += 256) {
+      const int j = it / r_g, ch = it % r_g;
+      lat[j * p.rmax + ch] = key_latent(p, g, b, c_t[j0 + j], ch);
+    }
+    __syncthreads();
+    for (int it0 = 0; it0 < nb * HALF; it0 += 256) {
       const int it = it0 + tid;
-      const int j = it / HALF, l = it % HALF;
+      const int jb = it / HALF, l = it % HALF;
+      const int j = j0 + jb;
       float dot = 0.0f;
-      if (j < n_sel) {
-        const float* lj = lat + j * p.rmax;
+      if (jb < nb) {
+        const float* lj = lat + jb * p.rmax;
         float klo = 0.0f, khi = 0.0f;
 #pragma unroll 8
         for (int ch = 0; ch < r_g; ++ch) {
@@ -1794,8 +1814,9 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
         dot = q_lo * (klo * cf - khi * sf) + q_hi * (khi * cf + klo * sf);
       }
       for (int o = HALF / 2; o > 0; o >>= 1) dot += __shfl_xor(dot, o);
-      if (l == 0 && j < n_sel)
+      if (l == 0 && jb < nb)
         c_d[j] = __builtin_amdgcn_exp2f(dot * p.score_scale - M) - __builtin_amdgcn_exp2f(c_x[j] - M);
+    }
     }
     __syncthreads();
     if (tid == 0) {
@@ -2007,7 +2028,7 @@ int launch_decode_combine(const CombineParams& p, void* stream) {
   if (p.n_split > kCombineMaxSplits) return (int)hipErrorInvalidValue;
   // the shared region: the merge phase (split sums, rescoring latents, B_k
   // block) or the up-projection's 256 / (D/8) rows of D partial sums
-  const size_t merge = (size_t)4 * p.rv + (size_t)kRescoreMax * p.rmax + (size_t)p.rmax * p.head_dim / 2;
+  const size_t merge = (size_t)4 * p.rv + (size_t)kRescoreBatch * p.rmax + (size_t)p.rmax * p.head_dim / 2;
   if (p.col_split != 1 && (p.col_split != 2 || p.lat)) return (int)hipErrorInvalidValue;
   const int dc = p.head_dim / p.col_split;
   const size_t upproj = (size_t)256 / (dc / 8) * dc;

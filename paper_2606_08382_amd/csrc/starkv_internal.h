@@ -94,7 +94,8 @@ struct DecodeParams {
   uint32_t o_code[STARKV_MAX_KV_HEADS], o_meta[STARKV_MAX_KV_HEADS];
 };
 
-constexpr int kCand = 32;      // rescoring candidates per (sequence, split, query head)
+constexpr int kCand = 64;      // rescoring candidates per (sequence, split, query head):
+                               // the top two scores of each of 32 lane slots
 
 struct CombineParams {
   const float* part;
