@@ -1344,11 +1344,34 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   }
   __syncthreads();
   const int64_t pbase = (int64_t)pitem * p.n_q;
+  // Candidates of a query head, in blocks of the 16 entries of one wave.  With
+  // m and l this split's maximum and normalizer and M, L the merged ones, a
+  // score x has the rescoring priority 2^(x - M) (1 + |x|) / L, at most
+  // 2^(m - M) q / L with q = max over the block of 2^(x - m) (1 + |x|), and at
+  // most q / l (L >= 2^(m - M) l).  So a block whose q misses half the
+  // threshold times l is never rescored and is not written; partial slot
+  // rv + 2 holds a byte per block saying whether it was, rv + 4 + tg the
+  // block's q, from which the merge bounds the block before loading it.
 #pragma unroll
   for (int c = 0; c < CTH; ++c) {
     if (c >= ctn) break;
     const int il = (ct0 + c) * 16 + col;
-    if (il < nql) {
+    const f4 lg = *reinterpret_cast<const f4*>(red + il * kTokenGroups);
+    const float bar = 0.5f * kRescoreTau * (((lg[0] + lg[1]) + lg[2]) + lg[3]);
+    const float mr = m_run[c];
+    auto bound = [&](float v) {
+      return v == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(v - mr) * (1.0f + fabsf(v));
+    };
+    float qb = fmaxf(fmaxf(bound(b1[c][0]), bound(b2[c][0])), fmaxf(bound(b1[c][1]), bound(b2[c][1])));
+    qb = fmaxf(qb, __shfl_xor(qb, 16));
+    qb = fmaxf(qb, __shfl_xor(qb, 32));
+    const bool any = qb >= bar;
+    if (il < nql && quad == 0) {
+      float* slot = p.part + (pbase + qmap[il]) * p.part_stride + p.rv;
+      reinterpret_cast<uint8_t*>(slot + 2)[tg] = any ? 1 : 0;
+      slot[4 + tg] = qb;
+    }
+    if (il < nql && any) {
       float2* cd = p.cand + (pbase + qmap[il]) * kCand + (tg * 4 + quad) * 4;
       auto token = [&](float v, int s) {
         const uint32_t k = __float_as_uint(v) & 0xFFu;
@@ -1414,7 +1437,6 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
 constexpr int kCombineMaxSplits = 256;  // one split per thread of the weight pass
 constexpr int kRescoreMax = 128;                       // tokens rescored per query head
 constexpr int kRescoreBatch = 32;                      // of them with key latents in LDS at once
-constexpr float kRescoreTau = 1.0f / 64.0f;
 constexpr int kBkVecPerThread = 8;   // B_k block of up to 128 x 128 fp16: 2048 vectors / 256 threads
 // candidate entries are read in chunks of 64 splits, kCandPerThread per thread
 constexpr int kCandChunk = 64 * kCand;
@@ -1486,7 +1508,7 @@ __device__ float value_latent(const CombineParams& p, int b, int t, int r) {
 // floats of the combine kernel's LDS before its shared region (kept a multiple
 // of 4 so that the region is 16-byte aligned)
 __host__ __device__ constexpr int combine_head_floats(int rv) {
-  return (rv + kCombineMaxSplits + 3 * kRescoreMax + 12 + 3) / 4 * 4;
+  return (rv + 2 * kCombineMaxSplits + 3 * kRescoreMax + 16 + 3) / 4 * 4;
 }
 
 __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
@@ -1497,9 +1519,11 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   float* c_x = wts + kCombineMaxSplits;  // [kRescoreMax] approximate scores
   float* c_d = c_x + kRescoreMax;        // [kRescoreMax] weight corrections
   int* c_t = reinterpret_cast<int*>(c_d + kRescoreMax);   // [kRescoreMax] tokens
-  float* misc = reinterpret_cast<float*>(c_t + kRescoreMax);  // M, L, L', unused
+  uint32_t* sfl = reinterpret_cast<uint32_t*>(c_t + kRescoreMax);  // [kCombineMaxSplits] flags
+  float* misc = reinterpret_cast<float*>(sfl + kCombineMaxSplits);  // M, L, L', unused
   float* wmax = misc + 4;                // [4] per-wave split maxima
   float* wsum = misc + 8;                // [4] per-wave weighted sums
+  int* wfl = reinterpret_cast<int*>(misc + 12);   // [4] per-wave: a split flagged candidates
   // One region, 16-byte aligned, serves two phases: the merge (per-wave split
   // sums, and the rescoring's key latents and B_k block) and, once the merged
   // latent is in `a`, the up-projection's partial sums.
@@ -1546,26 +1570,18 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   }
   const float* part = p.part + ((int64_t)first * p.n_q + i) * p.part_stride;
   const int64_t sstride = (int64_t)p.n_q * p.part_stride;
-  // rescoring candidates of the splits: the first 64 splits' entries are loaded
-  // ahead of the split weights.  Entry e = 32 s + j of chunk c is split 64 c + s,
-  // slot j; thread tid holds entries k * 256 + tid of a chunk, and entries past
-  // the sequence's splits are not loaded (-inf scores, never selected)
-  const int n_ent = ns * kCand;
-  const float2* cand = p.cand + ((int64_t)first * p.n_q + i) * kCand;
-  auto load_cand = [&](int c, float2 (&ce)[kCandPerThread]) {
-    const float2* cl = cand + (int64_t)(64 * c + tid / kCand) * p.n_q * kCand + tid % kCand;
-    const int64_t cstep = (int64_t)(256 / kCand) * p.n_q * kCand;
-#pragma unroll
-    for (int k = 0; k < kCandPerThread; ++k) {
-      ce[k] = make_float2(-INFINITY, 0.0f);
-      if (c * kCandChunk + k * 256 + tid < n_ent) ce[k] = cl[k * cstep];
-    }
-  };
-  const int n_cchunk = (n_ent + kCandChunk - 1) / kCandChunk;
-  float2 ce0[kCandPerThread];            // chunk 0 stays in registers
-  load_cand(0, ce0);
-  // the value-latent partials of this thread's first channel do not depend on
-  // the merge weights: load them now as well
+  // Every load that does not depend on the split weights is issued at once so
+  // that they share one memory round trip: each split's maximum, normalizer and
+  // candidate flags (one split per thread), the value-latent partials of the
+  // first 64 splits and this thread's first rows of U_V.
+  // (m, l, flags, unused) and the four block bounds: two 16-byte loads from a
+  // valid split, not in a branch, so that the first wait covers only them
+  const float* ps = part + min(tid, ns - 1) * sstride + p.rv;
+  const f4 ml0 = *reinterpret_cast<const f4*>(ps);
+  const f4 qb0 = *reinterpret_cast<const f4*>(ps + 4);
+  const float mv0 = tid < ns ? ml0[0] : -INFINITY;
+  const float lv0 = ml0[1];
+  const uint32_t fl0 = tid < ns ? __float_as_uint(ml0[2]) : 0u;
   const int D8 = Dc / 8;                 // 16, 8 or 4 column vectors
   const int groups = 256 / D8;           // row groups of the up-projection
   const int j8 = tid % D8, rg = tid / D8;
@@ -1578,8 +1594,8 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   // Value-latent partials: wave w takes splits w, w + 4, .., lane l channels
   // 4l..4l+3 of each 256-channel chunk, one 16-byte load per (split, chunk), so
   // a chunk of all splits is 64 loads of 1 KiB per workgroup.  A wave loads its
-  // splits in batches of 8 (splits w + 32h + 4k); the first batch of chunk 0 is
-  // loaded now (it does not depend on the merge weights).
+  // splits in batches of 8 (splits w + 32h + 4k); the two batches of chunk 0
+  // (splits below 64) are loaded now.
   constexpr int kSplitBatch = 8;
   const int n_chunk = (p.rv + 255) / 256;
   auto load_batch = [&](int ch, int h, f4 (&pv)[kSplitBatch]) {
@@ -1589,33 +1605,51 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
       pv[k] = *reinterpret_cast<const f4*>(
           pbase + o + (uint32_t)min(w + 32 * h + 4 * k, ns - 1) * sbytes);
   };
-  f4 pv0[kSplitBatch];
+  f4 pv0[kSplitBatch], pv1[kSplitBatch];
   load_batch(0, 0, pv0);
-  constexpr int kUpRows = 4;             // rows of U_V per thread per round of loads
+  load_batch(0, 1, pv1);   // (split indices are clamped: valid, unused below 33 splits)
+  constexpr int kUpRows = 8;             // rows of U_V per thread per round of loads
+  // rows past rv load row rv - 1 and are skipped by the product.  The loads are
+  // not in a branch, so that no wait before them covers more than it must: with
+  // latent output (no U_V) they read the first partials, unused.
+  const uint16_t* bvl = to_lat ? reinterpret_cast<const uint16_t*>(part) : bv;
+  const int64_t ldbl = to_lat ? 0 : ldb;
+  auto load_rows = [&](int r0, u4 (&w8)[kUpRows]) {
+#pragma unroll
+    for (int k = 0; k < kUpRows; ++k)
+      w8[k] = *reinterpret_cast<const u4*>(bvl + (int64_t)min(r0 + k * groups, p.rv - 1) * ldbl);
+  };
+  u4 w0[kUpRows];
+  load_rows(rg, w0);
   const int r_g = p.k_rank[g];
   {                               // split weights: one split per thread
-    const int s = min(tid, ns - 1);
-    // m_s and l_s wait in LDS (lat is free here) across the barrier
-    float* lsp = lat;
-    const float mv0 = tid < ns ? part[s * sstride + p.rv] : -INFINITY;
-    lsp[tid] = part[s * sstride + p.rv + 1];
-    wts[tid] = mv0;
     float m = mv0;
     for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
     if (lane == 0) wmax[w] = m;
     __syncthreads();
     m = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
-    const float mv = wts[tid], lv = lsp[tid];
-    const float wv = tid < ns ? __builtin_amdgcn_exp2f(mv - m) : 0.0f;
+    const float wv = tid < ns ? __builtin_amdgcn_exp2f(mv0 - m) : 0.0f;
     wts[tid] = wv;
-    float l = tid < ns ? wv * lv : 0.0f;
+    float l = tid < ns ? wv * lv0 : 0.0f;
     for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o);
     if (lane == 0) wsum[w] = l;
     __syncthreads();
-    if (tid == 0) { misc[0] = m; misc[1] = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3]; }
+    const float ls = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
+    // the candidate blocks of this split that may hold a token to rescore:
+    // written by the split and bounded by 2^(m_s - M) q / L >= tau / 2
+    uint32_t fl = 0;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      if (((fl0 >> (8 * t)) & 0xFFu) != 0u && wv * qb0[t] >= 0.5f * kRescoreTau * ls)
+        fl |= 1u << (8 * t);
+    sfl[tid] = fl;
+    const bool fw = __ballot(fl != 0u) != 0;
+    if (lane == 0) wfl[w] = fw ? 1 : 0;
+    if (tid == 0) { misc[0] = m; misc[1] = ls; }
     __syncthreads();
   }
   const float M = misc[0], Lsum = misc[1];
+  const bool any_cand = (wfl[0] | wfl[1] | wfl[2] | wfl[3]) != 0;
   // weighted sums of this wave's splits, per channel, into red4[w][r]
   auto add_batch = [&](int h, const f4 (&pv)[kSplitBatch], f4& acc) {
 #pragma unroll
@@ -1628,15 +1662,13 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
     f4 acc = (f4){0, 0, 0, 0};
     if (ch == 0) {
       add_batch(0, pv0, acc);
+      if (ns > 32) add_batch(1, pv1, acc);   // splits 32 .. 63
     } else {
-      f4 pv[kSplitBatch];
-      load_batch(ch, 0, pv);
-      add_batch(0, pv, acc);
-    }
-    if (ns > 32) {                        // splits 32 .. 63
-      f4 pv[kSplitBatch];
-      load_batch(ch, 1, pv);
-      add_batch(1, pv, acc);
+      f4 pa[kSplitBatch], pb[kSplitBatch];
+      load_batch(ch, 0, pa);
+      if (ns > 32) load_batch(ch, 1, pb);
+      add_batch(0, pa, acc);
+      if (ns > 32) add_batch(1, pb, acc);
     }
     const int r = 256 * ch + 4 * lane;
     if (r < p.rv) *reinterpret_cast<f4*>(red4 + w * p.rv + r) = acc;
@@ -1661,6 +1693,23 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   // beyond, one pass over the chunks counts the entries above each threshold
   // and a second compacts, reading the chunks again.
   constexpr int kLevels = 8;
+  // Candidate entries of the splits.  Thread tid takes slot `lane` of splits
+  // 64 c + 4 k + w of chunk c (entry order: split, then slot); a slot's block of
+  // 16 entries holds data only when the split set its flag byte, and the rest
+  // read as -inf scores (never selected).
+  static_assert(kCand == 64 && kCandPerThread == 16, "one slot per lane");
+  const float2* cand = p.cand + ((int64_t)first * p.n_q + i) * kCand;
+  auto load_cand = [&](int c, float2 (&ce)[kCandPerThread]) {
+    const float2* cl = cand + (int64_t)(64 * c + w) * p.n_q * kCand + lane;
+    const int64_t cstep = (int64_t)4 * p.n_q * kCand;
+#pragma unroll
+    for (int k = 0; k < kCandPerThread; ++k) {
+      const int s = 64 * c + 4 * k + w;
+      ce[k] = make_float2(-INFINITY, 0.0f);
+      if (s < ns && ((sfl[s] >> (8 * (lane >> 4))) & 0xFFu) != 0u) ce[k] = cl[k * cstep];
+    }
+  };
+  const int n_cchunk = (ns + 63) / 64;
   auto priorities = [&](const float2 (&ce)[kCandPerThread], float (&prio)[kCandPerThread]) {
 #pragma unroll
     for (int k = 0; k < kCandPerThread; ++k) {
@@ -1699,7 +1748,11 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   };
   float tau = kRescoreTau;
   int n_sel = 0;
-  if (n_cchunk == 1) {
+  if (!any_cand) {
+    // no split holds a candidate that could reach the threshold
+  } else if (n_cchunk == 1) {
+    float2 ce0[kCandPerThread];
+    load_cand(0, ce0);
     float prio[kCandPerThread];
     priorities(ce0, prio);
     for (int it = 0; it < kLevels; ++it) {
@@ -1842,17 +1895,6 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
     }
     a[r] = acc * inv_l;
   };
-  // the first rows of U_V, in flight while the rescored tokens' value latents load
-  u4 w0[kUpRows];
-  {
-    const uint16_t* bl = bv + (int64_t)rg * ldb;
-#pragma unroll
-    for (int k = 0; k < kUpRows; ++k) {
-      w0[k] = (u4){0, 0, 0, 0};
-      if (!to_lat && rg + k * groups < p.rv)
-        w0[k] = *reinterpret_cast<const u4*>(bl + (int64_t)k * groups * ldb);
-    }
-  }
   for (int r = tid; r < p.rv; r += 256) merge_channel(r);
   __syncthreads();
   if (to_lat) {                 // absorbed output: the latents go to the product pass
@@ -1882,12 +1924,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   up_rows(rg, w0);
   for (int r0 = rg + kUpRows * groups; r0 < p.rv; r0 += kUpRows * groups) {
     u4 w8[kUpRows];
-    const uint16_t* bl = bv + (int64_t)r0 * ldb;
-#pragma unroll
-    for (int k = 0; k < kUpRows; ++k) {
-      w8[k] = (u4){0, 0, 0, 0};
-      if (r0 + k * groups < p.rv) w8[k] = *reinterpret_cast<const u4*>(bl + (int64_t)k * groups * ldb);
-    }
+    load_rows(r0, w8);
     up_rows(r0, w8);
   }
 #pragma unroll

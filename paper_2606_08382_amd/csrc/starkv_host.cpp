@@ -452,7 +452,8 @@ starkv_status starkv_decode_describe(const starkv_plan* P, int32_t max_ctx,
   return STARKV_OK;
 }
 
-static int part_stride(const starkv_plan* P) { return P->cfg.value_rank + 4; }
+// value latent, then m, l, candidate flags, unused, four candidate bounds
+static int part_stride(const starkv_plan* P) { return P->cfg.value_rank + 8; }
 
 // Work items whose partials the workspace holds: the device plan's cap, or
 // every (sequence, split).

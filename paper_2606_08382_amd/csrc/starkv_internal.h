@@ -96,6 +96,9 @@ struct DecodeParams {
 
 constexpr int kCand = 64;      // rescoring candidates per (sequence, split, query head):
                                // the top two scores of each of 32 lane slots
+// a candidate is rescored when its share of the softmax times (1 + |score|)
+// reaches this
+constexpr float kRescoreTau = 1.0f / 64.0f;
 
 struct CombineParams {
   const float* part;
