@@ -68,15 +68,20 @@ __device__ __forceinline__ uint32_t group_code(const GroupQ& g, uint16_t x) {
   return (uint32_t)c;
 }
 
-// ------------------------------------------------------------------ pack kernel
-// One wave per (new token, quantization group); lane i holds channel c0 + i of
-// the group (at most 32 lanes are active).  The group's min and max come from
-// wave reductions, the scale and the codes from fp64 arithmetic per lane, and
-// the codes are packed into the cache words with shuffles.  Value 4-bit words
-// hold eight tokens of one channel, so a token updates its nibble with an
-// atomic AND/OR pair: tokens of one launch touch disjoint nibbles.
-// When the latents come from the down-projection, the lane first sums the
-// split-k partial products (fixed order) and stores the fp16 latent.
+// ------------------------------------------------------------------ pack kernels
+// Lanes 32h .. 32h + 31 of a wave hold the channels c0 .. c0 + 31 of one token
+// and one quantization group (lanes at or beyond the group's width are off).
+// The group's min and max come from reductions within those 32 lanes, the scale
+// and the codes from fp64 arithmetic per lane, and a token's key codes are
+// packed into its cache words with shuffles.
+//
+// Two kernels.  Decode-sized appends (one token per wave) first sum the
+// down-projection's split-k partials (fixed order) and store the fp16 latent;
+// a token then writes its value nibbles into words that hold eight tokens four
+// apart, with an atomic AND/OR pair unless each word has one writer.  Appends
+// given as fp16 latents take one wave per 32-row block of a sequence and
+// group, with lane (h, c) on channel c0 + c of the block's tokens 2i + h: every
+// value word of the block is then assembled in one lane and stored once.
 
 __device__ __forceinline__ float wave_min32(float v) {
   for (int o = 16; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o));
@@ -87,140 +92,11 @@ __device__ __forceinline__ float wave_max32(float v) {
   return v;
 }
 
-// PARTIAL: the latents are summed here from the down-projection's split-k
-// partials (decode-sized appends); otherwise they are read as fp16.  Two
-// instances, so that the large prefill pack keeps a small register footprint.
-// Quantize and store one token's values of one group (lane i: channel c0 + i).
 struct PackGroup {
   int bl, gi, c0, n, bits, ro, hb, lb, ngr, rb;
   bool is_v;
 };
 
-__device__ __forceinline__ void pack_token(const AppendParams& p, const PackGroup& G, int lane,
-                                           int b, int t, uint16_t xb) {
-  const int bl = G.bl, gi = G.gi, bits = G.bits, ro = G.ro, hb = G.hb, lb = G.lb;
-  const bool is_v = G.is_v;
-  const bool on = lane < G.n;
-  const int c = G.c0 + lane;
-  if (t < 0 || t >= p.capacity) return;     // rows outside the cache are dropped
-  if (p.rmap.table) {                        // and rows on pages outside the pool
-    const int pg = p.rmap.table[(int64_t)b * p.rmap.per_seq + (t >> p.rmap.shift)];
-    if (pg < 0 || pg >= p.rmap.n_pages) return;
-  }
-  uint8_t* code_plane = p.cache + p.code_off[bl];
-  uint8_t* meta_plane = p.cache + p.meta_off[bl];
-  const int rb = G.rb;
-  const int ngr = G.ngr;
-  const int64_t row = cache_row(p.rmap, b, t);
-  const int64_t kblk = row / 16;
-  const int tau = t % 16;
-  const int64_t vblk = row / 32;
-  const int u = t % 32, kq = u % 4, slot = 4 * (u / 16) + (u % 16) / 4;
-  if (bits == 16) {
-    if (on) {
-      if (!is_v)
-        *reinterpret_cast<uint16_t*>(code_plane + kblk * 16 * rb + (c / 8) * 256 + tau * 16 + (c % 8) * 2) = xb;
-      else
-        *reinterpret_cast<uint16_t*>(code_plane + vblk * 32 * rb + ((int64_t)c * 4 + kq) * 16 + slot * 2) = xb;
-    }
-    return;
-  }
-  // group parameters (the fp16 values compare exactly in fp32)
-  const float xf = (float)__builtin_bit_cast(_Float16, xb);
-  const float lo = wave_min32(on ? xf : INFINITY);
-  const float hi = wave_max32(on ? xf : -INFINITY);
-  const double levels = (double)((1 << bits) - 1);
-  const uint16_t s16 = (hi > lo) ? f16_ceil_pos(((double)hi - (double)lo) / levels) : (uint16_t)0;
-  const uint16_t z16 = __builtin_bit_cast(uint16_t, (_Float16)lo);
-  const double sv = h2d(s16);
-  uint32_t code = 0;
-  if (sv != 0.0) {
-    double q = rint(((double)xf - (double)lo) / sv);
-    q = q < 0.0 ? 0.0 : (q > levels ? levels : q);
-    code = (uint32_t)q;
-  }
-  if (!on) code = 0;
-  if (!is_v) {
-    uint8_t* kb = code_plane + kblk * 16 * rb;
-    const int nhi = ro / 8;              // outlier chunks (16 tokens x hb bytes each)
-    const int ch = c / 8;
-    uint8_t* chunk = ch < nhi ? kb + ch * 16 * hb : kb + nhi * 16 * hb + (ch - nhi) * 16 * lb;
-    if (bits == 8) {          // 4 codes per 32-bit word, lanes 4k..4k+3
-      uint32_t wv = code << (8 * (lane & 3));
-      wv |= __shfl_xor(wv, 1);
-      wv |= __shfl_xor(wv, 2);
-      if (on && (lane & 3) == 0)
-        *reinterpret_cast<uint32_t*>(chunk + tau * 8 + (c % 8)) = wv;
-    } else {                  // a token's 8 codes of a chunk, lanes 8k..8k+7: channel
-      // w at bits bits*w (4-bit: one 32-bit word; 3-bit: 3 bytes, stored bytewise
-      // since neighbouring tokens share 32-bit words)
-      uint32_t wv = code << (bits * (lane & 7));
-      wv |= __shfl_xor(wv, 1);
-      wv |= __shfl_xor(wv, 2);
-      wv |= __shfl_xor(wv, 4);
-      if (on && (lane & 7) == 0) {
-        if (bits == 4) {
-          *reinterpret_cast<uint32_t*>(chunk + tau * 4) = wv;
-        } else {
-          uint8_t* d = chunk + tau * 3;
-          d[0] = (uint8_t)wv;
-          d[1] = (uint8_t)(wv >> 8);
-          d[2] = (uint8_t)(wv >> 16);
-        }
-      }
-    }
-    if (lane == 0) {
-      uint16_t* m = reinterpret_cast<uint16_t*>(meta_plane + (kblk * ngr + gi) * 64 + tau * 4);
-      m[0] = s16;
-      m[1] = z16;
-    }
-  } else {
-    uint8_t* vb = code_plane + vblk * 32 * rb;
-    if (on) {
-      // (channel, chunk) words: the outlier region (4*ro*hb bytes) first
-      const bool hi = c < ro;
-      const int64_t word = hi ? ((int64_t)c * 4 + kq) * hb
-                              : 4LL * ro * hb + ((int64_t)(c - ro) * 4 + kq) * lb;
-      if (bits == 8) {
-        vb[word + slot] = (uint8_t)code;
-      } else {
-        // 4-bit: slot 2k -> bits 4k.., slot 2k+1 -> bits 16+4k.. of the 32-bit word;
-        // 3-bit: slot 2k -> bits 3k.., slot 2k+1 -> bits 12+3k.. of the 24-bit word.
-        // Tokens of one launch own disjoint fields, updated with atomic AND/OR on
-        // the aligned 32-bit word(s) holding them (a 3-bit field may straddle two).
-        const int sh = bits == 4 ? ((slot % 2 == 0) ? 4 * (slot / 2) : 16 + 4 * (slot / 2))
-                                 : ((slot % 2 == 0) ? 3 * (slot / 2) : 12 + 3 * (slot / 2));
-        const uint64_t abit = (uint64_t)((vb + word) - p.cache) * 8 + sh;   // bit address
-        unsigned int* wp = reinterpret_cast<unsigned int*>(p.cache) + abit / 32;
-        const int s0 = (int)(abit % 32);
-        const uint32_t fmask = (1u << bits) - 1;
-        if (p.single_writer && bits == 4) {
-          // at most four new tokens per sequence: every 4-bit word (eight tokens
-          // four apart) has one writer in this launch
-          *wp = (*wp & ~(fmask << s0)) | (code << s0);
-        } else {
-          atomicAnd(wp, ~(fmask << s0));
-          atomicOr(wp, code << s0);
-          if (s0 + bits > 32) {                // the field's high bits in the next word
-            atomicAnd(wp + 1, ~(fmask >> (32 - s0)));
-            atomicOr(wp + 1, code >> (32 - s0));
-          }
-        }
-      }
-    }
-    if (lane == 0) {
-      uint16_t* m = reinterpret_cast<uint16_t*>(meta_plane + (vblk * ngr + gi) * 128 + kq * 32 + slot * 2);
-      m[0] = s16;
-      m[8] = z16;
-    }
-  }
-}
-
-// PARTIAL: the latents are summed here from the down-projection's split-k
-// partials (decode-sized appends, one token per wave); otherwise they are read
-// as fp16 and a wave takes TPW tokens of one group, their loads issued together.
-// Two instances, so that the large prefill pack keeps a small register
-// footprint and several tokens' latency chains overlap.
 // The quantization group of work item `item`: its block (a key head or the
 // value latent), region, channels c0 .. c0 + n - 1 of the block and bit width.
 __device__ __forceinline__ PackGroup make_group(const AppendParams& p, int item) {
@@ -245,58 +121,296 @@ __device__ __forceinline__ PackGroup make_group(const AppendParams& p, int item)
   return G;
 }
 
-template <bool PARTIAL, int TPW>
+// Scale, zero and the lane's code for one token of a group (bits < 16); `on`
+// says whether the lane holds one of the group's channels.  The reductions run
+// over the 32 lanes of the lane's half.
+struct QCode {
+  uint16_t s16, z16;
+  uint32_t code;
+};
+
+__device__ __forceinline__ QCode quantize_lane(uint16_t xb, bool on, int bits) {
+  // the fp16 values compare exactly in fp32
+  const float xf = (float)__builtin_bit_cast(_Float16, xb);
+  const float lo = wave_min32(on ? xf : INFINITY);
+  const float hi = wave_max32(on ? xf : -INFINITY);
+  const double levels = (double)((1 << bits) - 1);
+  QCode q;
+  q.s16 = (hi > lo) ? f16_ceil_pos(((double)hi - (double)lo) / levels) : (uint16_t)0;
+  q.z16 = __builtin_bit_cast(uint16_t, (_Float16)lo);
+  const double sv = h2d(q.s16);
+  q.code = 0;
+  if (sv != 0.0) {
+    double c = rint(((double)xf - (double)lo) / sv);
+    c = c < 0.0 ? 0.0 : (c > levels ? levels : c);
+    q.code = (uint32_t)c;
+  }
+  if (!on) q.code = 0;
+  return q;
+}
+
+// A token's key codes and meta (rows in 16-token blocks: kblk, tau).  cl is
+// the lane's index in its 32-lane half; the writers are `on` lanes leading
+// groups of 4 (8-bit) or 8 (4-, 3-bit) channels, and the meta is written when
+// `meta` is set (by one lane).
+__device__ __forceinline__ void store_key_token(const AppendParams& p, const PackGroup& G, int cl,
+                                                int64_t kblk, int tau, const QCode& q, bool on,
+                                                bool meta) {
+  const int c = G.c0 + cl, bits = G.bits, hb = G.hb, lb = G.lb;
+  uint8_t* kb = p.cache + p.code_off[G.bl] + kblk * 16 * G.rb;
+  const int nhi = G.ro / 8;              // outlier chunks (16 tokens x hb bytes each)
+  const int ch = c / 8;
+  uint8_t* chunk = ch < nhi ? kb + ch * 16 * hb : kb + nhi * 16 * hb + (ch - nhi) * 16 * lb;
+  if (bits == 8) {          // 4 codes per 32-bit word, lanes 4k..4k+3
+    uint32_t wv = q.code << (8 * (cl & 3));
+    wv |= __shfl_xor(wv, 1);
+    wv |= __shfl_xor(wv, 2);
+    if (on && (cl & 3) == 0)
+      *reinterpret_cast<uint32_t*>(chunk + tau * 8 + (c % 8)) = wv;
+  } else {                  // a token's 8 codes of a chunk, lanes 8k..8k+7: channel
+    // w at bits bits*w (4-bit: one 32-bit word; 3-bit: 3 bytes, stored bytewise
+    // since neighbouring tokens share 32-bit words)
+    uint32_t wv = q.code << (bits * (cl & 7));
+    wv |= __shfl_xor(wv, 1);
+    wv |= __shfl_xor(wv, 2);
+    wv |= __shfl_xor(wv, 4);
+    if (on && (cl & 7) == 0) {
+      if (bits == 4) {
+        *reinterpret_cast<uint32_t*>(chunk + tau * 4) = wv;
+      } else {
+        uint8_t* d = chunk + tau * 3;
+        d[0] = (uint8_t)wv;
+        d[1] = (uint8_t)(wv >> 8);
+        d[2] = (uint8_t)(wv >> 16);
+      }
+    }
+  }
+  if (meta) {
+    uint16_t* m = reinterpret_cast<uint16_t*>(p.cache + p.meta_off[G.bl] +
+                                              (kblk * G.ngr + G.gi) * 64 + tau * 4);
+    m[0] = q.s16;
+    m[1] = q.z16;
+  }
+}
+
+// Value words of a 32-row block: the outlier region's (channel, chunk) words of
+// 8 bytes first, then the inlier region's of lb bytes; chunk kq holds the
+// block's tokens u = kq + 4 j in slots 4 (u / 16) + (u % 16) / 4.
+__device__ __forceinline__ int64_t value_word(const PackGroup& G, int c, int kq) {
+  return c < G.ro ? ((int64_t)c * 4 + kq) * G.hb
+                  : 4LL * G.ro * G.hb + ((int64_t)(c - G.ro) * 4 + kq) * G.lb;
+}
+// bit offset of slot `slot` in a 4-bit (32-bit word) or 3-bit (24-bit word)
+// value word: slot 2k at field k, slot 2k + 1 at field k + 4
+__device__ __forceinline__ int value_shift(int bits, int slot) {
+  return bits == 4 ? ((slot % 2 == 0) ? 4 * (slot / 2) : 16 + 4 * (slot / 2))
+                   : ((slot % 2 == 0) ? 3 * (slot / 2) : 12 + 3 * (slot / 2));
+}
+
+// One token of a decode-sized append (lane i: channel c0 + i, lanes 32..63 off).
+__device__ __forceinline__ void pack_token(const AppendParams& p, const PackGroup& G, int lane,
+                                           int b, int t, uint16_t xb) {
+  const int bits = G.bits;
+  const bool on = lane < G.n;
+  const int c = G.c0 + lane;
+  if (t < 0 || t >= p.capacity) return;     // rows outside the cache are dropped
+  if (p.rmap.table) {                        // and rows on pages outside the pool
+    const int pg = p.rmap.table[(int64_t)b * p.rmap.per_seq + (t >> p.rmap.shift)];
+    if (pg < 0 || pg >= p.rmap.n_pages) return;
+  }
+  uint8_t* code_plane = p.cache + p.code_off[G.bl];
+  uint8_t* meta_plane = p.cache + p.meta_off[G.bl];
+  const int64_t row = cache_row(p.rmap, b, t);
+  const int64_t kblk = row / 16;
+  const int tau = t % 16;
+  const int64_t vblk = row / 32;
+  const int u = t % 32, kq = u % 4, slot = 4 * (u / 16) + (u % 16) / 4;
+  if (bits == 16) {
+    if (on) {
+      if (!G.is_v)
+        *reinterpret_cast<uint16_t*>(code_plane + kblk * 16 * G.rb + (c / 8) * 256 + tau * 16 + (c % 8) * 2) = xb;
+      else
+        *reinterpret_cast<uint16_t*>(code_plane + vblk * 32 * G.rb + ((int64_t)c * 4 + kq) * 16 + slot * 2) = xb;
+    }
+    return;
+  }
+  const QCode q = quantize_lane(xb, on, bits);
+  if (!G.is_v) {
+    store_key_token(p, G, lane, kblk, tau, q, on, lane == 0);
+    return;
+  }
+  uint8_t* vb = code_plane + vblk * 32 * G.rb;
+  if (on) {
+    const int64_t word = value_word(G, c, kq);
+    if (bits == 8) {
+      vb[word + slot] = (uint8_t)q.code;
+    } else {
+      // tokens of one launch own disjoint fields, updated with atomic AND/OR on
+      // the aligned 32-bit word(s) holding them (a 3-bit field may straddle two)
+      const uint64_t abit = (uint64_t)((vb + word) - p.cache) * 8 + value_shift(bits, slot);
+      unsigned int* wp = reinterpret_cast<unsigned int*>(p.cache) + abit / 32;
+      const int s0 = (int)(abit % 32);
+      const uint32_t fmask = (1u << bits) - 1;
+      if (p.single_writer && bits == 4) {
+        // at most four new tokens per sequence: every 4-bit word (eight tokens
+        // four apart) has one writer in this launch
+        *wp = (*wp & ~(fmask << s0)) | (q.code << s0);
+      } else {
+        atomicAnd(wp, ~(fmask << s0));
+        atomicOr(wp, q.code << s0);
+        if (s0 + bits > 32) {                // the field's high bits in the next word
+          atomicAnd(wp + 1, ~(fmask >> (32 - s0)));
+          atomicOr(wp + 1, q.code >> (32 - s0));
+        }
+      }
+    }
+  }
+  if (lane == 0) {
+    uint16_t* m = reinterpret_cast<uint16_t*>(meta_plane + (vblk * G.ngr + G.gi) * 128 + kq * 32 + slot * 2);
+    m[0] = q.s16;
+    m[8] = q.z16;
+  }
+}
+
+// Decode-sized appends: one token per wave, its latents summed from the
+// down-projection's split-k partials in a fixed order (up to 64 loads in
+// flight) and stored as fp16 before the pack.
 __global__ __launch_bounds__(256) void pack_kernel(AppendParams p) {
   const int lane = threadIdx.x & 63;
   const int wid = blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
   const int n_tok = p.batch * p.n_new;
-  const int n_tb = (n_tok + TPW - 1) / TPW;
-  if (wid >= n_tb * p.n_items) return;
-  const int tb = wid / p.n_items, item = wid % p.n_items;
+  if (wid >= n_tok * p.n_items) return;
+  const int tok = wid / p.n_items, item = wid % p.n_items;
   const PackGroup G = make_group(p, item);
   const bool on = lane < G.n;
   const int c = G.c0 + lane;
-  uint16_t xb[TPW];
-  int pos[TPW];
-#pragma unroll
-  for (int i = 0; i < TPW; ++i) {
-    const int tok = tb * TPW + i;
-    xb[i] = 0;
-    pos[i] = tok < n_tok ? p.pos[tok / p.n_new] : 0;
-    if (!on || tok >= n_tok) continue;
+  const int pos = p.pos[tok / p.n_new];
+  uint16_t xb = 0;
+  if (on) {
     const int64_t li = (int64_t)tok * p.width + p.lat_off[G.bl] + c;
-    if (PARTIAL) {
-      // the split-k partial sums in a fixed order, up to 64 loads in flight
-      const int64_t mn = (int64_t)n_tok * p.width;
-      float acc = 0.0f;
-      int k = 0;
-      for (; k + 64 <= p.k_split; k += 64) {
-        float v[64];
+    const int64_t mn = (int64_t)n_tok * p.width;
+    float acc = 0.0f;
+    int k = 0;
+    for (; k + 64 <= p.k_split; k += 64) {
+      float v[64];
 #pragma unroll
-        for (int u = 0; u < 64; ++u) v[u] = p.partial[(k + u) * mn + li];
+      for (int u = 0; u < 64; ++u) v[u] = p.partial[(k + u) * mn + li];
 #pragma unroll
-        for (int u = 0; u < 64; ++u) acc += v[u];
+      for (int u = 0; u < 64; ++u) acc += v[u];
+    }
+    for (; k + 16 <= p.k_split; k += 16) {
+      float v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) v[u] = p.partial[(k + u) * mn + li];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) acc += v[u];
+    }
+    for (; k < p.k_split; ++k) acc += p.partial[k * mn + li];
+    xb = __builtin_bit_cast(uint16_t, (_Float16)acc);
+    p.lat_out[li] = xb;
+  }
+  const int b = tok / p.n_new, j = tok % p.n_new;
+  pack_token(p, G, lane, b, pos + j, xb);
+}
+
+// Appends given as fp16 latents: one wave per (sequence, 32-row block that the
+// rows pos .. pos + n_new - 1 touch, group).  A 3- or 4-bit value word of the
+// block (eight tokens of one channel, four apart) belongs to one lane, which
+// assembles the new fields and stores the word once, reading it first only
+// when the append covers part of it; no other wave of the launch writes it.
+__global__ __launch_bounds__(256) void pack_block_kernel(AppendParams p) {
+  const int lane = threadIdx.x & 63;
+  const int wid = blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
+  const int nblk = (p.n_new + 31) / 32 + 1;     // blocks a run of n_new rows can touch
+  const int per_seq = nblk * p.n_items;
+  if (wid >= p.batch * per_seq) return;
+  const int b = wid / per_seq, rem = wid % per_seq;
+  const int bi = rem / p.n_items, item = rem % p.n_items;
+  const int t0 = p.pos[b];
+  const int a = (t0 >> 5) + bi;                 // rows 32 a .. 32 a + 31 of the sequence
+  // rows outside the cache are dropped
+  const int t_lo = max(max(t0, 32 * a), 0);
+  const int t_hi = min(min(t0 + p.n_new, 32 * a + 32), p.capacity);
+  if (t_lo >= t_hi) return;
+  if (p.rmap.table) {                           // and rows on pages outside the pool
+    const int pg = p.rmap.table[(int64_t)b * p.rmap.per_seq + ((32 * a) >> p.rmap.shift)];
+    if (pg < 0 || pg >= p.rmap.n_pages) return;
+  }
+  const PackGroup G = make_group(p, item);
+  const int h = lane >> 5, cl = lane & 31;
+  const bool on = cl < G.n;
+  const int c = G.c0 + cl;
+  const int bits = G.bits;
+  const int64_t row0 = cache_row(p.rmap, b, 32 * a);   // 32-aligned: pages hold >= 128 rows
+  // the lane's 16 latents (tokens u = 2 i + h of the block), loaded together
+  uint16_t xb[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int t = 32 * a + 2 * i + h;
+    xb[i] = 0;
+    if (on && t >= t_lo && t < t_hi)
+      xb[i] = p.lat[((int64_t)b * p.n_new + (t - t0)) * p.width + p.lat_off[G.bl] + c];
+  }
+  uint8_t* code_plane = p.cache + p.code_off[G.bl];
+  uint8_t* meta_plane = p.cache + p.meta_off[G.bl];
+  uint8_t* vb = code_plane + (row0 / 32) * 32 * G.rb;
+  // value words of chunks kq = h and kq = h + 2 (3- and 4-bit): new fields, and
+  // the bits they cover
+  uint32_t acc[2] = {0u, 0u}, cov[2] = {0u, 0u};
+  const uint32_t fmask = bits < 16 ? (1u << bits) - 1 : 0u;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int u = 2 * i + h, t = 32 * a + u;
+    const bool live = t >= t_lo && t < t_hi;    // uniform in the lane's half
+    const int64_t kblk = (row0 + u) / 16;
+    const int tau = u % 16, kq = u % 4, slot = 4 * (u / 16) + (u % 16) / 4;
+    if (bits == 16) {
+      if (on && live) {
+        if (!G.is_v)
+          *reinterpret_cast<uint16_t*>(code_plane + kblk * 16 * G.rb + (c / 8) * 256 + tau * 16 + (c % 8) * 2) = xb[i];
+        else
+          *reinterpret_cast<uint16_t*>(vb + ((int64_t)c * 4 + kq) * 16 + slot * 2) = xb[i];
       }
-      for (; k + 16 <= p.k_split; k += 16) {
-        float v[16];
-#pragma unroll
-        for (int u = 0; u < 16; ++u) v[u] = p.partial[(k + u) * mn + li];
-#pragma unroll
-        for (int u = 0; u < 16; ++u) acc += v[u];
+      continue;
+    }
+    const QCode q = quantize_lane(xb[i], on, bits);
+    if (!G.is_v) {
+      store_key_token(p, G, cl, kblk, tau, q, on && live, live && cl == 0);
+      continue;
+    }
+    if (on && live) {
+      if (bits == 8) {
+        vb[value_word(G, c, kq) + slot] = (uint8_t)q.code;
+      } else {
+        const int sh = value_shift(bits, slot);
+        acc[i & 1] |= q.code << sh;
+        cov[i & 1] |= fmask << sh;
       }
-      for (; k < p.k_split; ++k) acc += p.partial[k * mn + li];
-      xb[i] = __builtin_bit_cast(uint16_t, (_Float16)acc);
-      p.lat_out[li] = xb[i];
-    } else {
-      xb[i] = p.lat[li];
+    }
+    if (live && cl == 0) {
+      uint16_t* m = reinterpret_cast<uint16_t*>(meta_plane + ((row0 / 32) * G.ngr + G.gi) * 128 +
+                                                kq * 32 + slot * 2);
+      m[0] = q.s16;
+      m[8] = q.z16;
     }
   }
+  if (G.is_v && on && (bits == 4 || bits == 3)) {
 #pragma unroll
-  for (int i = 0; i < TPW; ++i) {
-    const int tok = tb * TPW + i;
-    if (tok >= n_tok) break;
-    const int b = tok / p.n_new, j = tok % p.n_new;
-    pack_token(p, G, lane, b, pos[i] + j, xb[i]);
+    for (int k = 0; k < 2; ++k) {               // chunk kq = 2 k + h
+      if (cov[k] == 0u) continue;
+      uint8_t* wd = vb + value_word(G, c, 2 * k + h);
+      if (bits == 4) {
+        uint32_t* w32 = reinterpret_cast<uint32_t*>(wd);
+        *w32 = cov[k] == 0xFFFFFFFFu ? acc[k] : ((*w32 & ~cov[k]) | acc[k]);
+      } else {                                  // 24-bit word, bytewise (not aligned)
+        uint32_t old = 0u;
+        if (cov[k] != 0xFFFFFFu) old = (uint32_t)wd[0] | ((uint32_t)wd[1] << 8) | ((uint32_t)wd[2] << 16);
+        const uint32_t v = (old & ~cov[k]) | acc[k];
+        wd[0] = (uint8_t)v;
+        wd[1] = (uint8_t)(v >> 8);
+        wd[2] = (uint8_t)(v >> 16);
+      }
+    }
   }
 }
 
@@ -576,14 +690,15 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_bf16_nt_kernel(DownprojPa
 
 // ------------------------------------------------------------------ launchers
 int launch_append_pack(const AppendParams& p, void* stream) {
-  constexpr int kTpw = 4;            // tokens per wave without partials
-  const int64_t n_tok = (int64_t)p.batch * p.n_new;
-  const int64_t waves = (p.partial ? n_tok : (n_tok + kTpw - 1) / kTpw) * p.n_items;
-  dim3 grid((unsigned)((waves + 3) / 4));
-  if (p.partial)
-    hipLaunchKernelGGL((pack_kernel<true, 1>), grid, dim3(256), 0, static_cast<hipStream_t>(stream), p);
-  else
-    hipLaunchKernelGGL((pack_kernel<false, kTpw>), grid, dim3(256), 0, static_cast<hipStream_t>(stream), p);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int64_t waves;
+  if (p.partial) {
+    waves = (int64_t)p.batch * p.n_new * p.n_items;
+    hipLaunchKernelGGL(pack_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, st, p);
+  } else {
+    waves = (int64_t)p.batch * ((p.n_new + 31) / 32 + 1) * p.n_items;
+    hipLaunchKernelGGL(pack_block_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, st, p);
+  }
   return (int)hipGetLastError();
 }
 
