@@ -677,17 +677,22 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   extern __shared__ __align__(16) uint8_t smem[];
   constexpr int CTH = (CT + 1) / 2;
   constexpr int NKBS = D / 32;   // score k-blocks (head dimension / 32)
+  // The pipelined key routine (key_head_q) for the 4-bit and 8-bit/4-bit caches
+  // when the value accumulators are small (NTW <= 2): with more, its state
+  // across heads no longer fits in registers and key_head is faster.
+  constexpr bool kPipeKeys = (QM == STARKV_Q_INT4 || QM == STARKV_Q_MIX8_4) && NTW <= 2;
   constexpr int HALF = D / 2;
   constexpr int QS = D + 8;
   constexpr int NQV = (16 * CT * (D / 8) + kThreads - 1) / kThreads;   // query vectors per thread
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  // Waves w and w + 4 share a SIMD; they take the same half of the heads (and
-  // so the same work) on different tokens, so that neither runs alone on its
-  // SIMD at the end of the key phase.
-  const int hh = w & 1;                    // half of the group's KV heads
-  const int tg = w >> 1;                   // token group: tokens 32*tg.. of each step
+  // Waves w and w + 4 share a SIMD and take the two halves of the heads on the
+  // same tokens, so every SIMD carries the whole key work of one token group
+  // (the halves cannot always be balanced: ranks 80, 32, 128, 128 split 9 : 11
+  // in k-block cost).
+  const int tg = w & (kTokenGroups - 1);   // token group: tokens 32*tg.. of each step
+  const int hh = w / kTokenGroups;         // half of the group's KV heads
   const int col = lane & 15, quad = lane >> 4;
   // Token order of the score tiles: row 4*quad + e of a 16-token subtile is
   // token 4*e + quad, so a lane's rows are tokens quad, quad+4, quad+8,
@@ -1121,7 +1126,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     for (int k = 1; k <= NKBS; ++k) {
       for (int i = cls_end[k - 1]; i < cls_end[k]; ++i) {
         const HeadRt kh = head_rt(i);
-        if constexpr (QM == STARKV_Q_INT4 || QM == STARKV_Q_MIX8_4) {
+        if constexpr (kPipeKeys) {
           if (k == 1) key_head_q<D, QM, CTH, 1>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, lc4, lc8, cs, acc_s, pend);
           if (k == 2) key_head_q<D, QM, CTH, 2>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, lc4, lc8, cs, acc_s, pend);
           if (NKBS > 2 && k == 3) key_head_q<D, QM, CTH, (NKBS > 2 ? 3 : 1)>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, lc4, lc8, cs, acc_s, pend);
@@ -1137,7 +1142,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
         if (step + 1 < n_steps) copy_head(kh, kblk_next);
       }
     }
-    if constexpr (QM == STARKV_Q_INT4 || QM == STARKV_Q_MIX8_4) key_drain<D, CTH>(pend, cs, acc_s);
+    if constexpr (kPipeKeys) key_drain<D, CTH>(pend, cs, acc_s);
 
     // ------------------------------------------ online softmax (log2 domain)
     // scores are already in log2 units (the query carries log2(e)/sqrt(d))
