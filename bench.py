@@ -29,6 +29,7 @@ HBM_PEAK_GBS = 8000.0
 MFMA_F16_PEAK_TFLOPS = 2500.0   # dense fp16 matrix peak
 COPY_BYTES = 256 << 20           # the plain device-to-device copy timed beside the path
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_split_c3_traffic.json")
+SQ_SUMMARY = os.path.join(ROOT, "profiles", "decode_split_c3_sq_counters.json")
 SPLIT_SOURCE = os.path.join(ROOT, "paper_2606_08382_amd", "csrc", "decode.hip")
 
 
@@ -63,20 +64,27 @@ def cpu_baseline(w, inp, sample_ctx: int, n_seq: int = 4):
                        f"over {span} took {dt:.2f} s")}
 
 
-def measured_traffic(workload_name):
-    """HBM bytes per split launch from the committed rocprofv3 counter summary (FETCH_SIZE and
-    WRITE_SIZE, each scaled by the same counter's reading for a copy of known size), or None
-    when the summary is missing, covers another workload, or the kernel source has changed
-    since the counters were taken."""
+def _counter_summary(path, workload_name):
+    """A committed rocprofv3 counter summary of the split kernel, or None when it is missing,
+    covers another workload, or the kernel source has changed since the counters were taken."""
     import hashlib
     try:
-        with open(TRAFFIC_SUMMARY) as f:
+        with open(path) as f:
             t = json.load(f)
         with open(SPLIT_SOURCE, "rb") as f:
             sha = hashlib.sha256(f.read()).hexdigest()
     except (OSError, ValueError):
-        return None, None
+        return None
     if t.get("source_sha256") != sha or t.get("workload") != workload_name:
+        return None
+    return t
+
+
+def measured_traffic(workload_name):
+    """HBM bytes per split launch from the committed counter summary (FETCH_SIZE and
+    WRITE_SIZE, each scaled by the same counter's reading for a copy of known size), or None."""
+    t = _counter_summary(TRAFFIC_SUMMARY, workload_name)
+    if t is None:
         return None, None
     return float(t["traffic_bytes_per_launch"]), t
 
@@ -302,6 +310,13 @@ def main():
         result["absorbed_output"] = absorbed
     if prefill is not None:
         result["prefill"] = prefill
+    sq = _counter_summary(SQ_SUMMARY, w.name)
+    if sq is not None:       # what the matrix cores and vector ALUs did, from the SQ counters
+        result["roofline_mfma"]["measured"] = {
+            "mfma_busy": sq["simd_fraction"]["mfma_busy"],
+            "valu_active": sq["simd_fraction"]["valu_active"],
+            "mfma_valu_coexec": sq["simd_fraction"]["mfma_valu_coexec"],
+            "source": "profiles/decode_split_c3_sq_counters.json (fractions of SIMD cycles)"}
     if tsum is not None:
         result["roofline"]["traffic_detail"] = {
             k: tsum[k] for k in ("fetch_bytes_per_launch", "write_bytes_per_launch",
