@@ -1516,7 +1516,14 @@ __host__ __device__ constexpr int combine_head_floats(int rv) {
   return (rv + 2 * kCombineMaxSplits + 3 * kRescoreMax + 16 + 3) / 4 * 4;
 }
 
-__global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
+// DEEP (grids of at most one workgroup per compute unit): both partial batches
+// of the first 64 splits and the thread's U_V rows are loaded at entry.
+// Otherwise (several workgroups per compute unit) the second batch is loaded
+// when needed and U_V just before the merge, which keeps the kernel at 128
+// VGPRs (four workgroups per compute unit).
+template <bool DEEP>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(DEEP ? 1 : 4)))
+void decode_combine_kernel(CombineParams p) {
   extern __shared__ __align__(16) float sm[];
   const int D = p.head_dim;
   float* a = sm;                         // [rv] merged value latent
@@ -1612,8 +1619,10 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
   };
   f4 pv0[kSplitBatch], pv1[kSplitBatch];
   load_batch(0, 0, pv0);
-  load_batch(0, 1, pv1);   // (split indices are clamped: valid, unused below 33 splits)
-  constexpr int kUpRows = 8;             // rows of U_V per thread per round of loads
+  if constexpr (DEEP) load_batch(0, 1, pv1);   // (clamped split indices: valid, unused below 33 splits)
+  // rows of U_V per thread per round of loads: 8 when they are loaded at entry,
+  // 16 when loaded before the merge (then the partials' registers are free)
+  constexpr int kUpRows = DEEP ? 8 : 16;
   // rows past rv load row rv - 1 and are skipped by the product.  The loads are
   // not in a branch, so that no wait before them covers more than it must: with
   // latent output (no U_V) they read the first partials, unused.
@@ -1625,7 +1634,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
       w8[k] = *reinterpret_cast<const u4*>(bvl + (int64_t)min(r0 + k * groups, p.rv - 1) * ldbl);
   };
   u4 w0[kUpRows];
-  load_rows(rg, w0);
+  if constexpr (DEEP) load_rows(rg, w0);
   const int r_g = p.k_rank[g];
   {                               // split weights: one split per thread
     float m = mv0;
@@ -1667,7 +1676,14 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
     f4 acc = (f4){0, 0, 0, 0};
     if (ch == 0) {
       add_batch(0, pv0, acc);
-      if (ns > 32) add_batch(1, pv1, acc);   // splits 32 .. 63
+      if (ns > 32) {                           // splits 32 .. 63
+        if constexpr (DEEP) {
+          add_batch(1, pv1, acc);
+        } else {
+          load_batch(0, 1, pv1);
+          add_batch(1, pv1, acc);
+        }
+      }
     } else {
       f4 pa[kSplitBatch], pb[kSplitBatch];
       load_batch(ch, 0, pa);
@@ -1900,6 +1916,9 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(CombineParams p) {
     }
     a[r] = acc * inv_l;
   };
+  // (shallow form: the first rows of U_V, in flight while the rescored tokens'
+  // value latents load)
+  if constexpr (!DEEP) load_rows(rg, w0);
   for (int r = tid; r < p.rv; r += 256) merge_channel(r);
   __syncthreads();
   if (to_lat) {                 // absorbed output: the latents go to the product pass
@@ -2076,11 +2095,17 @@ int launch_decode_combine(const CombineParams& p, void* stream) {
   const size_t upproj = (size_t)256 / (dc / 8) * dc;
   const size_t lds = ((size_t)combine_head_floats(p.rv) + (merge > upproj ? merge : upproj)) *
                      sizeof(float);
-  static std::atomic<uint64_t> attr{0};
-  if (const int e = allow_lds(reinterpret_cast<const void*>(decode_combine_kernel), attr)) return e;
   dim3 grid(p.n_q, p.batch, p.col_split);
-  hipLaunchKernelGGL(decode_combine_kernel, grid, dim3(256), lds,
-                     static_cast<hipStream_t>(stream), p);
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  if ((int64_t)p.n_q * p.batch * p.col_split <= 256) {
+    static std::atomic<uint64_t> attr{0};
+    if (const int e = allow_lds(reinterpret_cast<const void*>(decode_combine_kernel<true>), attr)) return e;
+    hipLaunchKernelGGL(decode_combine_kernel<true>, grid, dim3(256), lds, st, p);
+  } else {
+    static std::atomic<uint64_t> attr{0};
+    if (const int e = allow_lds(reinterpret_cast<const void*>(decode_combine_kernel<false>), attr)) return e;
+    hipLaunchKernelGGL(decode_combine_kernel<false>, grid, dim3(256), lds, st, p);
+  }
   return (int)hipGetLastError();
 }
 #endif
