@@ -611,9 +611,16 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_bf16_nt_kernel(DownprojPa
   __shared__ __align__(16) uint16_t xs[2][GM * GKP];
   __shared__ __align__(16) uint16_t bs[2][GN * GKP];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int n0 = blockIdx.x * GN, m0 = blockIdx.y * GM;
-  const int wm = (w / WNW) * 64, wn = (w % WNW) * TN;
   const int M = p.m, N = p.n, K = p.k;            // K is a multiple of GK (checked by the host)
+  // workgroups are dealt to the eight XCDs in turn (workgroup i on XCD i % 8):
+  // tiles are numbered row-major and XCD x takes a contiguous run of them, so
+  // the column tiles of a row of X share that XCD's L2
+  const int n_ct = (N + GN - 1) / GN, n_t = n_ct * ((M + GM - 1) / GM);
+  const int per_xcd = (n_t + 7) / 8;
+  const int t = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (t >= n_t) return;
+  const int n0 = (t % n_ct) * GN, m0 = (t / n_ct) * GM;
+  const int wm = (w / WNW) * 64, wn = (w % WNW) * TN;
   // global -> register staging: chunk c = tid + NTH i of a (rows x 64) tile is
   // row c / 8, k chunk c % 8 (16 bytes); rows past M or N read the last row
   u4 rx[NA], rb[NB];
@@ -712,10 +719,11 @@ int launch_downproj(const DownprojParams& p, void* stream) {
     // else 128 x 96 tiles (then at most 4 x 96 of them: a single round at two
     // workgroups per CU)
     if (((p.m + 255) / 256) * ((p.n + 191) / 192) >= 96)
-      hipLaunchKernelGGL((gemm_bf16_nt_kernel<4, 2, 96>), dim3((p.n + 191) / 192, (p.m + 255) / 256),
-                         dim3(512), 0, st, p);
+      hipLaunchKernelGGL((gemm_bf16_nt_kernel<4, 2, 96>),
+                         dim3(8 * ((((p.n + 191) / 192) * ((p.m + 255) / 256) + 7) / 8)), dim3(512), 0, st, p);
     else
-      hipLaunchKernelGGL((gemm_bf16_nt_kernel<2, 2, 48>), dim3((p.n + 95) / 96, (p.m + 127) / 128),
+      hipLaunchKernelGGL((gemm_bf16_nt_kernel<2, 2, 48>),
+                         dim3(8 * ((((p.n + 95) / 96) * ((p.m + 127) / 128) + 7) / 8)),
                          dim3(256), 0, st, p);
     return (int)hipGetLastError();
   }
