@@ -763,6 +763,17 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   if (p.dyn) {
     int cnt;
     S = wave_split_plan(L, p.batch, p.k_lo, p.cap, lane, &cnt) * kStepTokens;
+    if (blockIdx.x == 0 && blockIdx.z == 0 && w == 0) {
+      // the plan of every sequence for the merge pass: its first item (an
+      // exclusive prefix sum of the split counts), split count and length
+      int incl = lane < p.batch ? cnt : 0;
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o);
+        if (lane >= o) incl += y;
+      }
+      if (lane < p.batch)
+        *reinterpret_cast<int4*>(p.plan + 4 * lane) = make_int4(incl - cnt, cnt, L, 0);
+    }
     pitem = blockIdx.x;
     // the item's sequence: a scalar walk over the sequences' split counts
     b = -1;
@@ -1551,17 +1562,16 @@ void decode_combine_kernel(CombineParams p) {
   const int lane = tid & 63, w = tid >> 6;
   const int g = (int)(((int64_t)i * p.n_kv) / p.n_q);
   // this sequence's splits: under the work plan, items first .. first + ns - 1
-  int L = p.dyn ? (lane < p.batch ? p.ctx_len[lane] : 0) : p.ctx_len[b];
-  L = L < 0 ? 0 : (L > p.max_ctx ? p.max_ctx : L);
-  int ns, first;
+  // (the split pass wrote the plan), else the fixed split grid
+  int L, ns, first;
   if (p.dyn) {
-    int cnt;
-    wave_split_plan(L, p.batch, p.k_lo, p.cap, lane, &cnt);
-    first = 0;
-    for (int j = 0; j < b; ++j) first += __builtin_amdgcn_readlane(cnt, j);
-    ns = __builtin_amdgcn_readlane(cnt, b);
-    L = __builtin_amdgcn_readlane(L, b);
+    const int4 e = *reinterpret_cast<const int4*>(p.plan + 4 * b);
+    first = e.x;
+    ns = e.y;
+    L = e.z;
   } else {
+    L = p.ctx_len[b];
+    L = L < 0 ? 0 : (L > p.max_ctx ? p.max_ctx : L);
     ns = (L + p.split_len - 1) / p.split_len;
     first = b * p.n_split;
   }

@@ -475,10 +475,16 @@ static int64_t lat_offset(const starkv_plan* P, int32_t max_ctx) {
          align256(part_slots(P, max_ctx) * P->cfg.n_q_heads * kCand * 8);
 }
 
+// Then the per-sequence work plan the split pass writes for the merge pass
+// [B] (first item, splits, length, 0).
+static int64_t plan_offset(const starkv_plan* P, int32_t max_ctx) {
+  return lat_offset(P, max_ctx) +
+         align256((int64_t)2 * P->cfg.batch * P->cfg.n_q_heads * P->cfg.value_rank * 2);
+}
+
 size_t starkv_decode_workspace_bytes(const starkv_plan* P, int32_t max_ctx) {
   if (!P || max_ctx < 1) return 0;
-  return (size_t)(lat_offset(P, max_ctx) +
-                  align256((int64_t)2 * P->cfg.batch * P->cfg.n_q_heads * P->cfg.value_rank * 2));
+  return (size_t)(plan_offset(P, max_ctx) + align256((int64_t)16 * P->cfg.batch));
 }
 
 static starkv_status check_common(const starkv_plan* P, int32_t max_ctx, size_t ws_bytes,
@@ -537,6 +543,7 @@ starkv_status starkv_decode_split(const starkv_plan* P, const void* cache, const
   p.ctx_len = ctx_len_dev;
   p.part = static_cast<float*>(ws);
   p.cand = reinterpret_cast<float2*>(static_cast<uint8_t*>(ws) + cand_offset(P, max_ctx));
+  p.plan = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(ws) + plan_offset(P, max_ctx));
   p.batch = c.batch;
   p.n_q = c.n_q_heads;
   p.n_kv = c.n_kv_heads;
@@ -603,6 +610,7 @@ static void combine_params(const starkv_plan* P, const void* cache, const void* 
   std::memset(&p, 0, sizeof(p));
   p.part = static_cast<const float*>(ws);
   p.cand = reinterpret_cast<const float2*>(static_cast<const uint8_t*>(ws) + cand_offset(P, max_ctx));
+  p.plan = reinterpret_cast<const int32_t*>(static_cast<const uint8_t*>(ws) + plan_offset(P, max_ctx));
   p.bv = static_cast<const uint16_t*>(B_v);
   p.bk = static_cast<const uint16_t*>(B_k);
   p.cache = static_cast<const uint8_t*>(cache);

@@ -57,6 +57,9 @@ struct DecodeParams {
   const int32_t* ctx_len;
   float* part;                 // split partials
   float2* cand;                // per (b, split, query head): kCand (score, token) candidates
+  // work plan over ragged lengths: per sequence (first item, splits, length, 0),
+  // written once (by the first wave of workgroup (0, 0)) for the merge pass
+  int32_t* plan;
   int32_t batch, n_q, n_kv, group_q;   // group_q = H_q / H_kv
   RowMap rmap;
   int32_t max_ctx, split_len, n_split;
@@ -116,6 +119,7 @@ struct CombineParams {
   int32_t batch, n_q, n_kv, head_dim, rv;
   int32_t max_ctx, split_len, n_split, part_stride;
   int32_t dyn, k_lo, cap;      // as in DecodeParams
+  const int32_t* plan;         // dyn: the split pass's per-sequence plan (DecodeParams::plan)
   int32_t out_dtype, q_bf16, qmode;
   int32_t rmax;                // largest key rank (sizes the rescoring buffers)
   int32_t col_split;           // workgroups per (sequence, query head), each taking
