@@ -186,8 +186,10 @@ starkv_status starkv_cache_layout(const starkv_plan* plan, starkv_layout* out);
  * d_model > 0, the down-projection's fp32 partial sums (or, for 512 and more new
  * rows B*n_new with d_model a multiple of 64, A_all transposed for the prefill
  * GEMM).  Decode: the split
- * partials for contexts up to max_ctx, and the normalized value latents that
- * the absorbed output reads (the same size serves both decode entry points). */
+ * partials and rescoring candidates for contexts up to max_ctx, the normalized
+ * value latents that the absorbed output reads (the same size serves both
+ * decode entry points), and the per-sequence work plan the split pass leaves
+ * for the combine pass. */
 size_t        starkv_append_workspace_bytes(const starkv_plan* plan, int32_t n_new);
 size_t        starkv_decode_workspace_bytes(const starkv_plan* plan, int32_t max_ctx);
 
@@ -251,8 +253,8 @@ starkv_status starkv_decode_attn(const starkv_plan* plan, const void* cache, con
  * it: calls that overlap on one device (other streams, other threads) race and
  * must be ordered by the caller.
  * Errors: as starkv_decode_attn; WORKSPACE when starkv_decode_workspace_bytes(plan,
- * max_ctx) exceeds 32 MiB (the C3 layer shape needs 10.3 MiB at 4 x 131072 tokens
- * and 42.5 MiB at 64 x 131072). */
+ * max_ctx) exceeds 32 MiB (the C3 layer shape needs 12.4 MiB at 4 x 131072 tokens
+ * and 51.0 MiB at 64 x 131072). */
 starkv_status starkv_decode_attn_noalloc(const starkv_plan* plan, const void* cache,
                                          const void* q, const void* B_k, const void* B_v,
                                          const int32_t* ctx_len_dev, int32_t max_ctx, void* out,
@@ -260,8 +262,10 @@ starkv_status starkv_decode_attn_noalloc(const starkv_plan* plan, const void* ca
 
 /* The two launches of starkv_decode_attn, exposed separately so that each can be
  * timed on its own, with the same arguments and errors:
- *   split    keys, scores, softmax state and value latents per context split, and
- *            the largest approximate scores of each split, written to ws;
+ *   split    keys, scores, softmax state and value latents per context split, the
+ *            largest approximate scores of each split that may need rescoring,
+ *            and (for batches of up to 64 sequences) each sequence's work plan,
+ *            written to ws;
  *   combine  merge of the splits (log-sum-exp weights), exact fp32 rescoring of
  *            the tokens that dominate the softmax (re-read from the cache), and
  *            the value up-projection into out.
