@@ -695,6 +695,92 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_bf16_nt_kernel(DownprojPa
       }
 }
 
+// The large-problem tile (256 x 192, eight waves of 64 x 96) with its operands
+// copied from global memory straight into LDS (global_load_lds, 16 bytes per
+// lane) instead of through registers: unpadded 128-byte rows of 64 k whose
+// 16-byte chunk c sits in slot c ^ (row % 8), each lane of a copy fetching the
+// chunk that lands where the swizzle wants it, so that a fragment read (one
+// chunk of 16 rows) covers eight distinct slots per eight lanes.  Two stages;
+// the next step's copies are issued at the start of a step.
+constexpr int GDM = 256, GDN = 192;
+constexpr int GDA = GDM / 8, GDB = GDN / 8;       // 1 KiB copies per k step (A, B)
+constexpr int GDSTAGE = (GDM + GDN) * 128;
+
+__global__ __launch_bounds__(512) void gemm_bf16_nt_dma_kernel(DownprojParams p) {
+  __shared__ __align__(16) uint8_t sm[2 * GDSTAGE];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int M = p.m, N = p.n, K = p.k;            // K is a multiple of GK (checked by the host)
+  // tiles row-major, a contiguous run per XCD (workgroup i on XCD i % 8)
+  const int n_ct = (N + GDN - 1) / GDN, n_t = n_ct * ((M + GDM - 1) / GDM);
+  const int per_xcd = (n_t + 7) / 8;
+  const int t = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (t >= n_t) return;
+  const int n0 = (t % n_ct) * GDN, m0 = (t / n_ct) * GDM;
+  const int wm = (w / 2) * 64, wn = (w % 2) * 96;
+  // copy j of a k step: rows 8 j' .. 8 j' + 7 of the A tile (j < GDA) or of the
+  // B tile (j' = j - GDA); lane l fills slot l % 8 of row l / 8 with the global
+  // chunk (l % 8) ^ (l / 8)
+  const int crow = lane >> 3, cchunk = (lane & 7) ^ crow;
+  auto issue = [&](int k0, int buf) {
+    uint8_t* st = sm + buf * GDSTAGE;
+    for (int j = w; j < GDA + GDB; j += 8) {
+      const uint16_t* src;
+      if (j < GDA) src = p.x + (int64_t)min(m0 + 8 * j + crow, M - 1) * K;
+      else src = p.at + (int64_t)min(n0 + 8 * (j - GDA) + crow, N - 1) * K;
+      __builtin_amdgcn_global_load_lds(src + k0 + 8 * cchunk, st + j * 1024, 16, 0, 0);
+    }
+  };
+  const int fr = lane & 15, kq = lane >> 4;
+  f4 acc[4][6];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 6; ++j) acc[i][j] = (f4){0, 0, 0, 0};
+  const int nk = K / GK;
+  issue(0, 0);
+  __builtin_amdgcn_s_waitcnt(0x0F70);               // vmcnt(0)
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) issue((kt + 1) * GK, buf ^ 1);
+    const uint8_t* sa = sm + buf * GDSTAGE;
+    const uint8_t* sb = sa + GDM * 128;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {                 // 32 k each: chunks 4 kk + kq
+      const int c = 4 * kk + kq;
+      b8 af[4], bf[6];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = wm + 16 * i + fr;
+        af[i] = *reinterpret_cast<const b8*>(sa + r * 128 + ((c ^ (r & 7)) << 4));
+      }
+#pragma unroll
+      for (int j = 0; j < 6; ++j) {
+        const int r = wn + 16 * j + fr;
+        bf[j] = *reinterpret_cast<const b8*>(sb + r * 128 + ((c ^ (r & 7)) << 4));
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 6; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+    }
+    __builtin_amdgcn_s_waitcnt(0x0F70);             // this wave's copies of the next step
+    __syncthreads();                                 // every wave's; buf is free
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 6; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int m = m0 + wm + 16 * i + 4 * kq + e;
+        const int n = n0 + wn + 16 * j + fr;
+        if (m < M && n < N)
+          p.lat[(int64_t)m * N + n] = __builtin_bit_cast(uint16_t, (_Float16)acc[i][j][e]);
+      }
+}
+
 // ------------------------------------------------------------------ launchers
 int launch_append_pack(const AppendParams& p, void* stream) {
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -719,7 +805,7 @@ int launch_downproj(const DownprojParams& p, void* stream) {
     // else 128 x 96 tiles (then at most 4 x 96 of them: a single round at two
     // workgroups per CU)
     if (((p.m + 255) / 256) * ((p.n + 191) / 192) >= 96)
-      hipLaunchKernelGGL((gemm_bf16_nt_kernel<4, 2, 96>),
+      hipLaunchKernelGGL(gemm_bf16_nt_dma_kernel,
                          dim3(8 * ((((p.n + 191) / 192) * ((p.m + 255) / 256) + 7) / 8)), dim3(512), 0, st, p);
     else
       hipLaunchKernelGGL((gemm_bf16_nt_kernel<2, 2, 48>),
