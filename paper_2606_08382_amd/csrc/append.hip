@@ -695,18 +695,24 @@ __global__ __launch_bounds__(64 * WMW * WNW) void gemm_bf16_nt_kernel(DownprojPa
       }
 }
 
-// The large-problem tile (256 x 192, eight waves of 64 x 96) with its operands
-// copied from global memory straight into LDS (global_load_lds, 16 bytes per
-// lane) instead of through registers: unpadded 128-byte rows of 64 k whose
+// The large-problem tile (256 x 192) with its operands copied from global
+// memory straight into LDS (global_load_lds, 16 bytes per lane) instead of
+// through registers, which leaves registers for sixteen waves of 64 x 48 (four
+// per SIMD: the other waves hide each one's fragment reads and the step's
+// barrier, worth a third of the GEMM time against two per SIMD): unpadded
+// 128-byte rows of 64 k whose
 // 16-byte chunk c sits in slot c ^ (row % 8), each lane of a copy fetching the
 // chunk that lands where the swizzle wants it, so that a fragment read (one
 // chunk of 16 rows) covers eight distinct slots per eight lanes.  Two stages;
 // the next step's copies are issued at the start of a step.
-constexpr int GDM = 256, GDN = 192;
+constexpr int GDM = 256, GDN = 192, GDWN = 4;   // 16 waves of 64 x 48: four per SIMD
 constexpr int GDA = GDM / 8, GDB = GDN / 8;       // 1 KiB copies per k step (A, B)
 constexpr int GDSTAGE = (GDM + GDN) * 128;
 
-__global__ __launch_bounds__(512) void gemm_bf16_nt_dma_kernel(DownprojParams p) {
+// WN waves across the 192 columns (tiles of 192 / WN), four across the rows.
+template <int WN>
+__global__ __launch_bounds__(256 * WN) void gemm_bf16_nt_dma_kernel(DownprojParams p) {
+  constexpr int NW = 4 * WN, TN = GDN / WN, NT = TN / 16;
   __shared__ __align__(16) uint8_t sm[2 * GDSTAGE];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int M = p.m, N = p.n, K = p.k;            // K is a multiple of GK (checked by the host)
@@ -716,14 +722,14 @@ __global__ __launch_bounds__(512) void gemm_bf16_nt_dma_kernel(DownprojParams p)
   const int t = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
   if (t >= n_t) return;
   const int n0 = (t % n_ct) * GDN, m0 = (t / n_ct) * GDM;
-  const int wm = (w / 2) * 64, wn = (w % 2) * 96;
+  const int wm = (w / WN) * 64, wn = (w % WN) * TN;
   // copy j of a k step: rows 8 j' .. 8 j' + 7 of the A tile (j < GDA) or of the
   // B tile (j' = j - GDA); lane l fills slot l % 8 of row l / 8 with the global
   // chunk (l % 8) ^ (l / 8)
   const int crow = lane >> 3, cchunk = (lane & 7) ^ crow;
   auto issue = [&](int k0, int buf) {
     uint8_t* st = sm + buf * GDSTAGE;
-    for (int j = w; j < GDA + GDB; j += 8) {
+    for (int j = w; j < GDA + GDB; j += NW) {
       const uint16_t* src;
       if (j < GDA) src = p.x + (int64_t)min(m0 + 8 * j + crow, M - 1) * K;
       else src = p.at + (int64_t)min(n0 + 8 * (j - GDA) + crow, N - 1) * K;
@@ -731,11 +737,11 @@ __global__ __launch_bounds__(512) void gemm_bf16_nt_dma_kernel(DownprojParams p)
     }
   };
   const int fr = lane & 15, kq = lane >> 4;
-  f4 acc[4][6];
+  f4 acc[4][NT];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 6; ++j) acc[i][j] = (f4){0, 0, 0, 0};
+    for (int j = 0; j < NT; ++j) acc[i][j] = (f4){0, 0, 0, 0};
   const int nk = K / GK;
   issue(0, 0);
   __builtin_amdgcn_s_waitcnt(0x0F70);               // vmcnt(0)
@@ -748,21 +754,21 @@ __global__ __launch_bounds__(512) void gemm_bf16_nt_dma_kernel(DownprojParams p)
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {                 // 32 k each: chunks 4 kk + kq
       const int c = 4 * kk + kq;
-      b8 af[4], bf[6];
+      b8 af[4], bf[NT];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int r = wm + 16 * i + fr;
         af[i] = *reinterpret_cast<const b8*>(sa + r * 128 + ((c ^ (r & 7)) << 4));
       }
 #pragma unroll
-      for (int j = 0; j < 6; ++j) {
+      for (int j = 0; j < NT; ++j) {
         const int r = wn + 16 * j + fr;
         bf[j] = *reinterpret_cast<const b8*>(sb + r * 128 + ((c ^ (r & 7)) << 4));
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 6; ++j)
+        for (int j = 0; j < NT; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
     }
     __builtin_amdgcn_s_waitcnt(0x0F70);             // this wave's copies of the next step
@@ -771,7 +777,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_nt_dma_kernel(DownprojParams p)
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 6; ++j)
+    for (int j = 0; j < NT; ++j)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int m = m0 + wm + 16 * i + 4 * kq + e;
@@ -805,8 +811,8 @@ int launch_downproj(const DownprojParams& p, void* stream) {
     // else 128 x 96 tiles (then at most 4 x 96 of them: a single round at two
     // workgroups per CU)
     if (((p.m + 255) / 256) * ((p.n + 191) / 192) >= 96)
-      hipLaunchKernelGGL(gemm_bf16_nt_dma_kernel,
-                         dim3(8 * ((((p.n + 191) / 192) * ((p.m + 255) / 256) + 7) / 8)), dim3(512), 0, st, p);
+      hipLaunchKernelGGL((gemm_bf16_nt_dma_kernel<GDWN>),
+                         dim3(8 * ((((p.n + 191) / 192) * ((p.m + 255) / 256) + 7) / 8)), dim3(256 * GDWN), 0, st, p);
     else
       hipLaunchKernelGGL((gemm_bf16_nt_kernel<2, 2, 48>),
                          dim3(8 * ((((p.n + 95) / 96) * ((p.m + 127) / 128) + 7) / 8)),
