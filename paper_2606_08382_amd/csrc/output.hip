@@ -105,12 +105,123 @@ __global__ __launch_bounds__(kOutWaves * 64) void absorbed_out_kernel(AbsorbPara
   }
 }
 
+// Up to 16 sequences with K a multiple of 4 kStageK.  A load of the kernel
+// above covers 64 bytes in each of 16 rows of W_abs that lie K * 2 bytes
+// apart; here the workgroup's 16 rows go through LDS in stages of kStageK
+// channels, every row copied as contiguous 1 KiB runs (global_load_lds, 16
+// bytes per lane), and the MFMA B operands are read from LDS.  Rows are padded
+// to kStageK * 2 + 16 bytes, so that the 16 lanes of a fragment read start in
+// 16 distinct groups of four banks.  Four buffers, three stages in flight (96
+// KiB per workgroup, one workgroup per CU).  A stage's group of loads is the
+// wave's two copies and its four latent fragments (k blocks w and w + 16 of
+// the stage, hi and lo), so that waiting for a stage is a vmcnt of six per
+// later stage.  The barrier is a bare s_barrier after the LDS reads have
+// landed: the waits for the copies are the explicit vmcnts, and a
+// __syncthreads() would also wait for the stages still in flight.
+constexpr int kStageK = 1024;
+constexpr int kStageRow = kStageK * 2 + 16;       // bytes per staged row
+constexpr int kStageBytes = kOutCols * kStageRow;
+constexpr int kStageBufs = 4;
+
+__global__ __launch_bounds__(kOutWaves * 64) void absorbed_out_lds_kernel(AbsorbParams p) {
+  static_assert(kOutWaves == 16 && kOutCols == 16 && kStageK == 64 * kOutWaves,
+                "two copies and two k blocks per wave and stage");
+  __shared__ __align__(16) uint8_t osm[kStageBufs * kStageBytes];
+  __shared__ float red[kOutWaves][256];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int n0 = blockIdx.x * kOutCols;
+  const int K = p.k, nst = K / kStageK;           // a multiple of kStageBufs
+  const int ksub = 8 * (lane >> 4);
+  // copies of a stage: rows (w >> 1) and (w >> 1) + 8, 1 KiB run w & 1 (rows
+  // past d_out copy the last row; never stored)
+  const uint16_t* ws0 = p.w + (int64_t)min(n0 + (w >> 1), p.n_out - 1) * K + 512 * (w & 1) + 8 * lane;
+  const uint16_t* ws1 = p.w + (int64_t)min(n0 + (w >> 1) + 8, p.n_out - 1) * K + 512 * (w & 1) + 8 * lane;
+  const int wd = (w >> 1) * kStageRow + 1024 * (w & 1);
+  // A operand: sequence lane & 15 (rows past the batch repeat the last
+  // sequence; their outputs are never stored)
+  const int brow = min(lane & 15, p.batch - 1);
+  const uint16_t* hi = p.lat + (int64_t)brow * K + ksub + 32 * w;
+  const uint16_t* lo = hi + (int64_t)p.batch * K;
+  // the fragment reads are written out: the compiler would put a wait for every
+  // copy in flight (vmcnt(0)) in front of an LDS read it sees
+  typedef __attribute__((address_space(3))) uint8_t lds_u8;
+  const uint32_t sw_lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u8*)osm)) +
+                          (lane & 15) * kStageRow + 2 * ksub + 64 * w;
+  u4 lat[kStageBufs][4];
+  f4 acc = (f4){0, 0, 0, 0};
+  auto issue = [&](int st, u4(&l)[4]) {
+    uint8_t* dst = osm + (st % kStageBufs) * kStageBytes + wd;
+    const int64_t c = (int64_t)st * kStageK;
+    __builtin_amdgcn_global_load_lds(ws0 + c, dst, 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(ws1 + c, dst + 8 * kStageRow, 16, 0, 0);
+    l[0] = *reinterpret_cast<const u4*>(hi + c);
+    l[1] = *reinterpret_cast<const u4*>(lo + c);
+    l[2] = *reinterpret_cast<const u4*>(hi + c + 512);
+    l[3] = *reinterpret_cast<const u4*>(lo + c + 512);
+  };
+  // stage st (buffer u = st % 4) with `later` stages still in flight after it;
+  // the fragments are read before the next copies go out, which then take
+  // buffer (u + 3) % 4, the one that held stage st - 1
+  auto step = [&](int u, int st, int later, bool more) {
+    if (later == 2) __builtin_amdgcn_s_waitcnt(0x0F7C);        // vmcnt(12)
+    else if (later == 1) __builtin_amdgcn_s_waitcnt(0x0F76);   // vmcnt(6)
+    else __builtin_amdgcn_s_waitcnt(0x0F70);                   // vmcnt(0)
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    u4 b0, b1;
+    asm volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %2 offset:1024"
+                 : "=v"(b0), "=v"(b1) : "v"(sw_lds + u * kStageBytes) : "memory");
+    if (more) issue(st + 3, lat[(u + 3) % kStageBufs]);
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(b0), "+v"(b1) :: "memory");
+    acc = mfma16(lat[u][0], b0, acc);
+    acc = mfma16(lat[u][1], b0, acc);
+    acc = mfma16(lat[u][2], b1, acc);
+    acc = mfma16(lat[u][3], b1, acc);
+  };
+  issue(0, lat[0]);
+  issue(1, lat[1]);
+  issue(2, lat[2]);
+  int s0 = 0;
+  for (; s0 < nst - kStageBufs; s0 += kStageBufs) {
+#pragma unroll
+    for (int u = 0; u < kStageBufs; ++u) step(u, s0 + u, 2, true);
+  }
+  step(0, s0, 2, true);
+  step(1, s0 + 1, 2, false);
+  step(2, s0 + 2, 1, false);
+  step(3, s0 + 3, 0, false);
+  // lane holds rows 4*(lane/16)+e (sequences) of column lane%16 (outputs)
+#pragma unroll
+  for (int e = 0; e < 4; ++e) red[w][e * 64 + lane] = acc[e];
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < 256; idx += kOutWaves * 64) {
+    float s = 0.0f;
+#pragma unroll
+    for (int ww = 0; ww < kOutWaves; ++ww) s += red[ww][idx];
+    const int e = (idx >> 6) & 3, l = idx & 63;
+    const int b = 4 * (l >> 4) + e, n = n0 + (l & 15);
+    if (b >= p.batch || n >= p.n_out) continue;
+    const int64_t o = (int64_t)b * p.n_out + n;
+    if (p.out_dtype == STARKV_DT_F32) {
+      static_cast<float*>(p.out)[o] = s;
+    } else if (p.out_dtype == STARKV_DT_BF16) {
+      const uint32_t u = __float_as_uint(s);
+      uint16_t bits = (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+      if ((u & 0x7F800000u) == 0x7F800000u) bits = (uint16_t)(u >> 16) | ((u & 0xFFFFu) ? 0x40 : 0);
+      static_cast<uint16_t*>(p.out)[o] = bits;
+    } else {
+      static_cast<uint16_t*>(p.out)[o] = __builtin_bit_cast(uint16_t, (_Float16)s);
+    }
+  }
+}
+
 int launch_absorbed_out(const AbsorbParams& p, void* stream) {
   if (p.n_out < 1 || p.k < 8 || p.k % 8 || p.batch < 1) return (int)hipErrorInvalidValue;
   dim3 grid((p.n_out + kOutCols - 1) / kOutCols, (p.batch + kOutRows - 1) / kOutRows);
   dim3 block(kOutWaves * 64);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (p.batch <= 16) hipLaunchKernelGGL(absorbed_out_kernel<1>, grid, block, 0, st, p);
+  if (p.batch <= 16 && p.k % (kStageBufs * kStageK) == 0)
+    hipLaunchKernelGGL(absorbed_out_lds_kernel, dim3(grid.x), block, 0, st, p);
+  else if (p.batch <= 16) hipLaunchKernelGGL(absorbed_out_kernel<1>, grid, block, 0, st, p);
   else if (p.batch <= 32) hipLaunchKernelGGL(absorbed_out_kernel<2>, grid, block, 0, st, p);
   else hipLaunchKernelGGL(absorbed_out_kernel<4>, grid, block, 0, st, p);
   return (int)hipGetLastError();

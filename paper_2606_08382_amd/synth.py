@@ -170,8 +170,9 @@ def generate(w: Workload, seed: Optional[int] = None, peaked: int = 0,
             latents[b] = np.ascontiguousarray(z.astype(np.float16)).view(np.uint16)
     needles = None
     if peaked and with_latents:
-        needles = np.stack([rng.choice(int(ctx[b]), size=min(4, int(ctx[b])), replace=False)
-                            for b in range(w.batch)])
+        # up to four per sequence (fewer in a context shorter than four tokens)
+        needles = [rng.choice(int(ctx[b]), size=min(4, int(ctx[b])), replace=False)
+                   for b in range(w.batch)]
         ksum = sum(ranks)
         for b in range(w.batch):
             for t in needles[b]:

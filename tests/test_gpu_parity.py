@@ -300,7 +300,7 @@ def _absorbed_case(w, inp, d_out, ctx_len=None, max_ctx=None, capacity=None):
 @pytest.mark.parametrize("name,ctx,batch,d_out,ragged", [
     ("c1", 1024, None, 64, None), ("c3", 1100, 2, 4096, None), ("c3q", 700, 2, 1000, None),
     ("c5", 600, 2, 2048, None), ("c4", 600, 20, 200, (1, 600)), ("c2", 300, 40, 72, None),
-    ("c1", 200, 70, 40, (5, 200))])
+    ("c1", 200, 70, 40, (5, 200)), ("c3", 300, 16, 272, (1, 300))])
 @pytest.mark.parametrize("peaked", [0, 2])
 def test_absorbed_output_matches_oracle(name, ctx, batch, d_out, ragged, peaked):
     """Weight-absorbed output (Sec. 3.3): y_b = sum_i W'_out,i a_i / l_i over all query
