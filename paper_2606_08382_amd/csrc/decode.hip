@@ -1133,9 +1133,19 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     pend.q = (h8){0, 0, 0, 0, 0, 0, 0, 0};
     pend.ct = 0;
 
+    // The two waves sharing a SIMD (w and w + 4, one per head half) would
+    // split its issue slots unevenly: at equal priority the older wave wins,
+    // finishes its heads first and leaves the younger to run its last heads
+    // alone, with no second wave to cover its latencies.  With the pipelined
+    // key routine they take the higher issue priority on alternate heads
+    // instead, so that both halves advance together.
 #pragma unroll
     for (int k = 1; k <= NKBS; ++k) {
       for (int i = cls_end[k - 1]; i < cls_end[k]; ++i) {
+        if constexpr (kPipeKeys) {
+          if (((i + hh) & 1) != 0) __builtin_amdgcn_s_setprio(1);
+          else __builtin_amdgcn_s_setprio(0);
+        }
         const HeadRt kh = head_rt(i);
         if constexpr (kPipeKeys) {
           if (k == 1) key_head_q<D, QM, CTH, 1>(kh, raw, frag, qc, qzero, kh.gl, ct0, G, lane, col, tcol, quad, lc4, lc8, cs, acc_s, pend);
@@ -1153,7 +1163,10 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
         if (step + 1 < n_steps) copy_head(kh, kblk_next);
       }
     }
-    if constexpr (kPipeKeys) key_drain<D, CTH>(pend, cs, acc_s);
+    if constexpr (kPipeKeys) {
+      key_drain<D, CTH>(pend, cs, acc_s);
+      __builtin_amdgcn_s_setprio(0);
+    }
 
     // ------------------------------------------ online softmax (log2 domain)
     // scores are already in log2 units (the query carries log2(e)/sqrt(d))
