@@ -144,7 +144,7 @@ __device__ __forceinline__ u4 deq_int4m(uint32_t w, uint32_t mask, h2 s0, h2 z0,
 
 // LDS layout of the split kernel (byte offsets); identical on the host.
 struct SplitLds {
-  int frag, qc, red, alpha, flag, prog, rot, qmap, loop, raw, vcode, vmeta, pbuf, rope, total;
+  int frag, qc, red, alpha, flag, prog, rot, qmap, loop, raw, vcode, vmeta, pbuf, xch, rope, total;
 };
 
 // vcode_bytes: value codes of one step (kStepTokens tokens), a multiple of 16.
@@ -164,7 +164,10 @@ __host__ __device__ inline SplitLds split_lds(int frags, int nql, int head_dim, 
   L.vcode = L.raw + kWaves * raw_bytes;
   L.vmeta = L.vcode + vcode_bytes;
   L.pbuf = L.vmeta + 4 * v_ng * 128;
-  int loop_end = L.pbuf + kTokenGroups * ct * 1024;
+  // single-tile groups of a kernel with one accumulator per half: the second
+  // half's partial scores, [token group][lane][8]
+  L.xch = L.pbuf + kTokenGroups * ct * 1024;
+  int loop_end = L.xch + (ct <= 2 && nql <= 16 ? kTokenGroups * 64 * 32 : 0);
   L.rope = L.vcode;   // RoPE tables (prologue only) alias the value staging
   int rope_end = L.rope + (16 * 65 + 8 * 64) * 8;
   L.total = loop_end > rope_end ? loop_end : rope_end;
@@ -204,6 +207,15 @@ __device__ __forceinline__ void wait_vm(int n) {
     case 15: __builtin_amdgcn_s_waitcnt(0x0F7F); break;
     default: __builtin_amdgcn_s_waitcnt(0x0F70); break;   // vmcnt(0)
   }
+}
+
+// Workgroup barrier over LDS traffic only: this wave's LDS operations have
+// completed (lgkmcnt(0)), then s_barrier.  The fence of __syncthreads() also
+// waits for every global load and LDS copy still in flight (vmcnt(0)); this
+// barrier leaves them in flight, and the copies it must cover are waited for
+// explicitly (wait_vm) before it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 // The same by one wave: n_bytes (a multiple of 16) at src into lds, one copy
@@ -708,6 +720,10 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   const int G = p.group_q;
   const int nql = (g1 - g0) * G;
   const int ct_half = ((gm - g0) * G + 15) / 16;          // score tiles of the first half
+  // A single-tile group (one accumulator per half: CT <= 2) splits its heads
+  // between the halves by key cost; the first half owns the tile and adds the
+  // second half's partial scores to its own before the softmax.
+  const bool merge = CTH == 1 && nql <= 16 && g1 > gm;
   const int ct0 = hh ? ct_half : 0;                        // first score tile of this half
   const int ctn = hh ? (nql + 15) / 16 - ct_half : ct_half; // its tile count
 
@@ -1167,6 +1183,23 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
       key_drain<D, CTH>(pend, cs, acc_s);
       __builtin_amdgcn_s_setprio(0);
     }
+    if constexpr (CTH == 1) {
+      // Each half's partial tile holds its own heads' columns and exact zeros
+      // in the others (their query operand is zero), so the sum is the tile a
+      // single wave would have accumulated over all the heads.
+      if (merge) {
+        f4* xs = reinterpret_cast<f4*>(smem + LL.xch) + (tg * 64 + lane) * 2;
+        if (hh) {
+          xs[0] = acc_s[0][0];
+          xs[1] = acc_s[1][0];
+        }
+        lds_barrier();
+        if (!hh) {
+          acc_s[0][0] += xs[0];
+          acc_s[1][0] += xs[1];
+        }
+      }
+    }
 
     // ------------------------------------------ online softmax (log2 domain)
     // scores are already in log2 units (the query carries log2(e)/sqrt(d))
@@ -1233,7 +1266,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     // this wave's value copies landed (the next step's key copies, issued after
     // them, may still be in flight)
     wait_vm(step + 1 < n_steps ? n_kw : 0);
-    __syncthreads();   // (1) probabilities, maxima, flags and the step's values visible
+    lds_barrier();   // (1) probabilities, maxima, flags and the step's values visible
     if (step + 1 < n_steps) {   // every wave is done with the queries: rotate them
       const int j0 = 4 * (tid % (D / 8));
 #pragma unroll
@@ -1266,7 +1299,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
         pbuf[(tg * CT + ct) * 64 + lane] = __builtin_bit_cast(h8, pk);
         if (tg == 0 && quad == 0) alpha_s[ct * 16 + col] = al;
       }
-      __syncthreads();   // new probabilities and rescale factors visible
+      lds_barrier();   // new probabilities and rescale factors visible
 #pragma unroll
       for (int c = 0; c < CT; ++c) {
         const f4 al = *reinterpret_cast<const f4*>(alpha_s + c * 16 + 4 * quad);
@@ -1359,7 +1392,7 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     else if (vmode == kValues4) values(std::integral_constant<int, kValues4>{}, Full{});
     else values(std::integral_constant<int, kValuesMixed>{}, Full{});
     if (step + 1 < n_steps) {
-      __syncthreads();   // every wave is done reading this step's values
+      lds_barrier();   // every wave is done reading this step's values
       load_v(step + 1);
     }
   }

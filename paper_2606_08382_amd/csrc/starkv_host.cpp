@@ -230,10 +230,13 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
   }
   // A group of KV heads [a, b) is processed by one workgroup whose waves split
   // the heads into two halves; each half owns whole score tiles (16 query
-  // heads).  The heads are assigned to the halves to balance their key work
-  // (about 2 + k-blocks units per head: the rotation is per head, the
-  // reconstruction per k-block); slots list half 0's heads, then half 1's.
-  auto assign = [&](int a, int b, int* slots, int* n_first) {
+  // heads), except in a single-tile group of a kernel with at most two tiles
+  // (one accumulator per half), whose second half hands its partial scores to
+  // the first.  The heads are assigned to the halves to
+  // balance their key work (about 2 + k-blocks units per head: the rotation is
+  // per head, the reconstruction per k-block); slots list half 0's heads, then
+  // half 1's.
+  auto assign = [&](int a, int b, int ct, int* slots, int* n_first) {
     const int n = b - a;
     const int tiles = (n * G + 15) / 16;
     const int cap0 = tiles < 2 ? n : std::min(n, ((tiles + 1) / 2) * 16 / G);
@@ -244,7 +247,8 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
     int h0[STARKV_MAX_KV_HEADS], h1[STARKV_MAX_KV_HEADS], n0 = 0, n1 = 0, w0 = 0, w1 = 0;
     for (int i = 0; i < n; ++i) {
       const int g = order_idx[i], cost = 2 + info[g].nkb;
-      const bool to0 = n0 < cap0 && (n1 >= n - cap0 || w0 <= w1);
+      const bool to0 = (tiles < 2 && ct <= 2) ? w0 <= w1
+                                              : n0 < cap0 && (n1 >= n - cap0 || w0 <= w1);
       if (to0) { h0[n0++] = g; w0 += cost; } else { h1[n1++] = g; w1 += cost; }
     }
     std::sort(h0, h0 + n0);
@@ -262,7 +266,7 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
     int frags = 0;
     for (int g = g_first; g < g_last; ++g) frags += (D / 16) * info[g].nkb;
     int slots[STARKV_MAX_KV_HEADS], n0;
-    assign(g_first, g_last, slots, &n0);
+    assign(g_first, g_last, ct, slots, &n0);
     const int raw = std::max(raw_of(slots, n0), raw_of(slots + n0, g_last - g_first - n0));
     *frags_out = frags;
     *raw_out = raw;
@@ -307,7 +311,7 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
     P->hg_frags[h] = fr;
     P->hg_raw[h] = rw;
     int slots[STARKV_MAX_KV_HEADS], n0;
-    assign(a, b, slots, &n0);
+    assign(a, b, P->ct, slots, &n0);
     const int mid = a + n0;          // first slot of half 1
     P->hg_mid[h] = mid;
     int fb = 0;
