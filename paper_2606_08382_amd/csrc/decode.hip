@@ -144,7 +144,7 @@ __device__ __forceinline__ u4 deq_int4m(uint32_t w, uint32_t mask, h2 s0, h2 z0,
 
 // LDS layout of the split kernel (byte offsets); identical on the host.
 struct SplitLds {
-  int frag, qc, red, alpha, flag, prog, rot, qmap, loop, raw, vcode, vmeta, pbuf, xch, rope, total;
+  int frag, qc, red, alpha, flag, rot, qmap, loop, raw, vcode, vmeta, pbuf, xch, rope, total;
 };
 
 // vcode_bytes: value codes of one step (kStepTokens tokens), a multiple of 16.
@@ -156,8 +156,7 @@ __host__ __device__ inline SplitLds split_lds(int frags, int nql, int head_dim, 
   L.red = L.qc + ((nql * (head_dim + 8) * 2 + 256 + 15) / 16) * 16;
   L.alpha = L.red + kTokenGroups * ct * 16 * 4;
   L.flag = L.alpha + ct * 16 * 4;
-  L.prog = L.flag + kWaves * 4;
-  L.rot = L.prog + kWaves * 4;
+  L.rot = L.flag + kWaves * 4;
   L.qmap = L.rot + 64 * 8;
   L.loop = L.qmap + 64 * 4;
   L.raw = L.loop;
@@ -693,6 +692,9 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
   // when the value accumulators are small (NTW <= 2): with more, its state
   // across heads no longer fits in registers and key_head is faster.
   constexpr bool kPipeKeys = (QM == STARKV_Q_INT4 || QM == STARKV_Q_MIX8_4) && NTW <= 2;
+  // alternate issue priority between the two waves of a SIMD (key phase);
+  // measured faster with up to two value tiles per wave, slower with four
+  constexpr bool kAltPrio = NTW <= 2;
   constexpr int HALF = D / 2;
   constexpr int QS = D + 8;
   constexpr int NQV = (16 * CT * (D / 8) + kThreads - 1) / kThreads;   // query vectors per thread
@@ -1152,13 +1154,13 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
     // The two waves sharing a SIMD (w and w + 4, one per head half) would
     // split its issue slots unevenly: at equal priority the older wave wins,
     // finishes its heads first and leaves the younger to run its last heads
-    // alone, with no second wave to cover its latencies.  With the pipelined
-    // key routine they take the higher issue priority on alternate heads
-    // instead, so that both halves advance together.
+    // alone, with no second wave to cover its latencies.  With up to two
+    // value tiles per wave they take the higher issue priority on alternate
+    // heads instead, so that both halves advance together.
 #pragma unroll
     for (int k = 1; k <= NKBS; ++k) {
       for (int i = cls_end[k - 1]; i < cls_end[k]; ++i) {
-        if constexpr (kPipeKeys) {
+        if constexpr (kAltPrio) {
           if (((i + hh) & 1) != 0) __builtin_amdgcn_s_setprio(1);
           else __builtin_amdgcn_s_setprio(0);
         }
@@ -1179,10 +1181,8 @@ __global__ __launch_bounds__(kThreads, 1) void decode_split_kernel(DecodeParams 
         if (step + 1 < n_steps) copy_head(kh, kblk_next);
       }
     }
-    if constexpr (kPipeKeys) {
-      key_drain<D, CTH>(pend, cs, acc_s);
-      __builtin_amdgcn_s_setprio(0);
-    }
+    if constexpr (kPipeKeys) key_drain<D, CTH>(pend, cs, acc_s);
+    if constexpr (kAltPrio) __builtin_amdgcn_s_setprio(0);
     if constexpr (CTH == 1) {
       // Each half's partial tile holds its own heads' columns and exact zeros
       // in the others (their query operand is zero), so the sum is the tile a
