@@ -236,12 +236,11 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
   // balance their key work (about 2 + k-blocks units per head: the rotation is
   // per head, the reconstruction per k-block); slots list half 0's heads, then
   // half 1's.
-  auto assign = [&](int a, int b, int ct, int* slots, int* n_first) {
-    const int n = b - a;
+  auto assign = [&](const int* heads, int n, int ct, int* slots, int* n_first) {
     const int tiles = (n * G + 15) / 16;
     const int cap0 = tiles < 2 ? n : std::min(n, ((tiles + 1) / 2) * 16 / G);
     int order_idx[STARKV_MAX_KV_HEADS];
-    for (int i = 0; i < n; ++i) order_idx[i] = a + i;
+    for (int i = 0; i < n; ++i) order_idx[i] = heads[i];
     std::stable_sort(order_idx, order_idx + n,
                      [&](int x, int y) { return info[x].nkb > info[y].nkb; });
     int h0[STARKV_MAX_KV_HEADS], h1[STARKV_MAX_KV_HEADS], n0 = 0, n1 = 0, w0 = 0, w1 = 0;
@@ -262,18 +261,21 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
     for (int i = 0; i < n; ++i) raw += 32 * info[heads[i]].row_bytes + 2 * info[heads[i]].ngroups * 64;
     return raw;
   };
-  auto group_fits = [&](int g_first, int g_last, int ct, int* frags_out, int* raw_out) {
+  auto group_fits = [&](const int* heads, int n, int ct, int* frags_out, int* raw_out) {
     int frags = 0;
-    for (int g = g_first; g < g_last; ++g) frags += (D / 16) * info[g].nkb;
+    for (int i = 0; i < n; ++i) frags += (D / 16) * info[heads[i]].nkb;
     int slots[STARKV_MAX_KV_HEADS], n0;
-    assign(g_first, g_last, ct, slots, &n0);
-    const int raw = std::max(raw_of(slots, n0), raw_of(slots + n0, g_last - g_first - n0));
+    assign(heads, n, ct, slots, &n0);
+    const int raw = std::max(raw_of(slots, n0), raw_of(slots + n0, n - n0));
     *frags_out = frags;
     *raw_out = raw;
-    const int nql = (g_last - g_first) * G;
+    const int nql = n * G;
     if (nql > 16 * ct) return false;
     return split_lds_bytes(frags, nql, D, ct, raw, L.value_groups, L.value_row_bytes) <= kLdsLimit;
   };
+  // heads of the groups, group after group (order[first[h] ..  first[h+1]))
+  int order[STARKV_MAX_KV_HEADS];
+  for (int g = 0; g < c->n_kv_heads; ++g) order[g] = g;
   int best_ct = -1;
   for (int ct : {1, 2, 4}) {
     if (ct * ntw > 16) continue;
@@ -283,8 +285,8 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
     int first[STARKV_MAX_KV_HEADS + 1];
     while (g < c->n_kv_heads) {
       int e = g + 1, fr, rw;
-      if (!group_fits(g, e, ct, &fr, &rw)) { ok = false; break; }
-      while (e < c->n_kv_heads && group_fits(g, e + 1, ct, &fr, &rw)) ++e;
+      if (!group_fits(order + g, e - g, ct, &fr, &rw)) { ok = false; break; }
+      while (e < c->n_kv_heads && group_fits(order + g, e + 1 - g, ct, &fr, &rw)) ++e;
       first[n_hg++] = g;
       g = e;
     }
@@ -302,16 +304,62 @@ starkv_status starkv_plan_create(const starkv_config* c, starkv_plan** out) {
     return fail(STARKV_ERR_UNSUPPORTED, "no workgroup shape fits the ranks in LDS");
   }
   P->ct = best_ct;
+  // All head groups run side by side for the whole split, so the split takes
+  // as long as its costliest group.  With the group count fixed, the heads
+  // are redistributed by cost (largest first, each into the cheapest group
+  // that still fits the LDS and the tile count); the result replaces the
+  // contiguous grouping when its costliest group is cheaper.
+  if (P->n_hg > 1) {
+    const int n_hg = P->n_hg;
+    auto cost_of = [&](int g) { return 2 + info[g].nkb; };
+    int worst = 0;
+    for (int h = 0; h < n_hg; ++h) {
+      int w = 0;
+      for (int i = P->hg_first[h]; i < P->hg_first[h + 1]; ++i) w += cost_of(order[i]);
+      worst = std::max(worst, w);
+    }
+    int by_cost[STARKV_MAX_KV_HEADS];
+    for (int g = 0; g < c->n_kv_heads; ++g) by_cost[g] = g;
+    std::stable_sort(by_cost, by_cost + c->n_kv_heads,
+                     [&](int x, int y) { return cost_of(x) > cost_of(y); });
+    int members[STARKV_MAX_KV_HEADS][STARKV_MAX_KV_HEADS], count[STARKV_MAX_KV_HEADS] = {0};
+    int load[STARKV_MAX_KV_HEADS] = {0};
+    bool placed_all = true;
+    for (int i = 0; i < c->n_kv_heads && placed_all; ++i) {
+      const int g = by_cost[i];
+      int best = -1;
+      for (int h = 0; h < n_hg; ++h) {
+        if (best >= 0 && load[h] >= load[best]) continue;
+        members[h][count[h]] = g;
+        int fr, rw;
+        if (group_fits(members[h], count[h] + 1, P->ct, &fr, &rw)) best = h;
+      }
+      if (best < 0) { placed_all = false; break; }
+      members[best][count[best]++] = g;
+      load[best] += cost_of(g);
+    }
+    int worst_lpt = 0;
+    for (int h = 0; h < n_hg; ++h) worst_lpt = std::max(worst_lpt, load[h]);
+    if (placed_all && worst_lpt < worst) {
+      int o = 0;
+      for (int h = 0; h < n_hg; ++h) {
+        std::sort(members[h], members[h] + count[h]);
+        P->hg_first[h] = o;
+        for (int i = 0; i < count[h]; ++i) order[o++] = members[h][i];
+      }
+      P->hg_first[n_hg] = o;
+    }
+  }
   P->lds_bytes = 0;
   int pos = 0;
   for (int h = 0; h < P->n_hg; ++h) {
     const int a = P->hg_first[h], b = P->hg_first[h + 1];
     int fr, rw;
-    group_fits(a, b, P->ct, &fr, &rw);
+    group_fits(order + a, b - a, P->ct, &fr, &rw);
     P->hg_frags[h] = fr;
     P->hg_raw[h] = rw;
     int slots[STARKV_MAX_KV_HEADS], n0;
-    assign(a, b, P->ct, slots, &n0);
+    assign(order + a, b - a, P->ct, slots, &n0);
     const int mid = a + n0;          // first slot of half 1
     P->hg_mid[h] = mid;
     int fb = 0;
