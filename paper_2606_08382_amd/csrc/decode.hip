@@ -1832,7 +1832,7 @@ void decode_combine_kernel(CombineParams p) {
     load_cand(0, ce0);
     float prio[kCandPerThread];
     priorities(ce0, prio);
-    for (int it = 0; it < kLevels; ++it) {
+    {
       int c = 0;
 #pragma unroll
       for (int k = 0; k < kCandPerThread; ++k) c += prio[k] >= tau;
@@ -1841,8 +1841,34 @@ void decode_combine_kernel(CombineParams p) {
       __syncthreads();
       n_sel = kcnt[0] + kcnt[1] + kcnt[2] + kcnt[3];
       __syncthreads();
-      if (n_sel <= kRescoreMax || it == kLevels - 1) break;
-      tau *= 4.0f;
+    }
+    if (n_sel > kRescoreMax) {
+      // the higher thresholds counted in one pass (16-bit fields, as for
+      // several chunks below), then the first that leaves at most kRescoreMax
+      uint32_t lv[kLevels / 2];
+#pragma unroll
+      for (int j = 0; j < kLevels / 2; ++j) lv[j] = 0;
+#pragma unroll
+      for (int k = 0; k < kCandPerThread; ++k) {
+        float t = kRescoreTau;
+#pragma unroll
+        for (int j = 0; j < kLevels; ++j, t *= 4.0f)
+          lv[j / 2] += prio[k] >= t ? 1u << (16 * (j % 2)) : 0u;
+      }
+#pragma unroll
+      for (int j = 0; j < kLevels / 2; ++j) {
+        uint32_t v = lv[j];
+        for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+        if (lane == 0) kcnt[4 * j + w] = (int)v;
+      }
+      __syncthreads();
+      for (int j = 1; j < kLevels; ++j) {
+        tau *= 4.0f;
+        n_sel = 0;
+        for (int ww = 0; ww < 4; ++ww) n_sel += ((uint32_t)kcnt[4 * (j / 2) + ww] >> (16 * (j % 2))) & 0xFFFFu;
+        if (n_sel <= kRescoreMax) break;
+      }
+      __syncthreads();                   // the counts are read before kcnt is rewritten
     }
     // past the cap at every threshold tried (at least kRescoreMax tokens each
     // holding that much): the first kRescoreMax of the last one, in entry order
