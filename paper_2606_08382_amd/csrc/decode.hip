@@ -1806,19 +1806,26 @@ void decode_combine_kernel(CombineParams p) {
       if (lane == 0) kcnt[4 * k + w] = __builtin_popcountll(bal[k]);
     }
     __syncthreads();
+    // the wave counts of four entries at a time, read together
 #pragma unroll
-    for (int k = 0; k < kCandPerThread; ++k) {
-      int off = base;
-      for (int ww = 0; ww < w; ++ww) off += kcnt[4 * k + ww];
-      if (prio[k] >= tau) {
-        const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal[k] >> 32),
-                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)bal[k], 0));
-        if (off + rank < kRescoreMax) {
-          c_x[off + rank] = ce[k].x;
-          c_t[off + rank] = __float_as_int(ce[k].y);
+    for (int k0 = 0; k0 < kCandPerThread; k0 += 4) {
+      int4 kc[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) kc[j] = *reinterpret_cast<const int4*>(kcnt + 4 * (k0 + j));
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int k = k0 + j;
+        const int off = base + (w > 0 ? kc[j].x : 0) + (w > 1 ? kc[j].y : 0) + (w > 2 ? kc[j].z : 0);
+        if (prio[k] >= tau) {
+          const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal[k] >> 32),
+                                                     __builtin_amdgcn_mbcnt_lo((uint32_t)bal[k], 0));
+          if (off + rank < kRescoreMax) {
+            c_x[off + rank] = ce[k].x;
+            c_t[off + rank] = __float_as_int(ce[k].y);
+          }
         }
+        base += kc[j].x + kc[j].y + kc[j].z + kc[j].w;
       }
-      base += kcnt[4 * k] + kcnt[4 * k + 1] + kcnt[4 * k + 2] + kcnt[4 * k + 3];
     }
     __syncthreads();                     // kcnt is rewritten by the next chunk
     return base;
