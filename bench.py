@@ -109,7 +109,7 @@ def copy_stream(torch, stream, reps=5):
 
 def read_stream(torch, stream, n_bytes=1 << 30, reps=7):
     """Bandwidth of the plain HBM read stream (the library's hand-written read kernel:
-    16-byte loads, four in flight per lane, one word written per wave) over n_bytes, at a
+    16-byte loads, sixteen in flight per lane, one word written per wave) over n_bytes, at a
     few grid sizes; the best median is the measured read ceiling."""
     from paper_2606_08382_amd import starkv as S
     x = torch.ones(n_bytes // 4, dtype=torch.float32, device="cuda")

@@ -340,7 +340,7 @@ starkv_status starkv_decode_describe(const starkv_plan* plan, int32_t max_ctx,
                                      starkv_decode_info* out);
 
 /* starkv_read_stream -- a measurement aid, not part of the method: reads `bytes`
- * at src once with 16-byte loads (every lane keeps four in flight, grid-stride
+ * at src once with 16-byte loads (every lane keeps sixteen in flight, grid-stride
  * over `workgroups` workgroups of 256 threads) and folds them into one word per
  * wave, written to sink.  Timing it gives the plain HBM read ceiling that the
  * split pass's latent stream is compared with.
