@@ -19,6 +19,11 @@
 
 namespace starkv {
 
+#ifndef ABS_SK
+#define ABS_SK 512
+#define ABS_NB 8
+#endif
+
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
@@ -105,38 +110,51 @@ __global__ __launch_bounds__(kOutWaves * 64) void absorbed_out_kernel(AbsorbPara
   }
 }
 
-// Up to 16 sequences with K a multiple of 4 kStageK.  A load of the kernel
+// Up to 16 sequences with K a multiple of NB * SK.  A load of the kernel
 // above covers 64 bytes in each of 16 rows of W_abs that lie K * 2 bytes
-// apart; here the workgroup's 16 rows go through LDS in stages of kStageK
+// apart; here the workgroup's 16 rows go through LDS in stages of SK
 // channels, every row copied as contiguous 1 KiB runs (global_load_lds, 16
 // bytes per lane), and the MFMA B operands are read from LDS.  Rows are padded
-// to kStageK * 2 + 16 bytes, so that the 16 lanes of a fragment read start in
-// 16 distinct groups of four banks.  Four buffers, three stages in flight (96
-// KiB per workgroup, one workgroup per CU).  A stage's group of loads is the
-// wave's two copies and its four latent fragments (k blocks w and w + 16 of
-// the stage, hi and lo), so that waiting for a stage is a vmcnt of six per
-// later stage.  The barrier is a bare s_barrier after the LDS reads have
-// landed: the waits for the copies are the explicit vmcnts, and a
-// __syncthreads() would also wait for the stages still in flight.
-constexpr int kStageK = 1024;
-constexpr int kStageRow = kStageK * 2 + 16;       // bytes per staged row
-constexpr int kStageBytes = kOutCols * kStageRow;
-constexpr int kStageBufs = 4;
+// to SK * 2 + 16 bytes, so that the 16 lanes of a fragment read start in 16
+// distinct groups of four banks.  NB buffers, NB - 1 stages in flight (one
+// workgroup per CU).  A stage's group of loads is the wave's SK / 512 copies
+// and its latent fragments (k blocks w + 16 i of the stage, hi and lo), so
+// that waiting for a stage is a vmcnt of 3 SK / 512 per later stage.  The
+// barrier is a bare s_barrier after the LDS reads have landed: the waits for
+// the copies are the explicit vmcnts, and a __syncthreads() would also wait
+// for the stages still in flight.
+template <int V>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(V >= 0 && V < 64, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (V & 15) | ((V >> 4) << 14));
+}
+
+constexpr int SK = ABS_SK, NB = ABS_NB;   // stage channels, LDS buffers
 
 __global__ __launch_bounds__(kOutWaves * 64) void absorbed_out_lds_kernel(AbsorbParams p) {
-  static_assert(kOutWaves == 16 && kOutCols == 16 && kStageK == 64 * kOutWaves,
-                "two copies and two k blocks per wave and stage");
-  __shared__ __align__(16) uint8_t osm[kStageBufs * kStageBytes];
+  static_assert(kOutWaves == 16 && kOutCols == 16 && SK % 512 == 0 && SK <= 1024,
+                "one or two 1 KiB copies and k blocks per wave and stage");
+  constexpr int CPW = SK / 512;              // copies and k blocks per wave and stage
+  constexpr int OPS = 3 * CPW;               // loads per wave and stage
+  constexpr int ROW = SK * 2 + 16;           // bytes per staged row
+  constexpr int SB = kOutCols * ROW;         // bytes per stage
+  constexpr int AHEAD = NB - 1;              // stages in flight
+  __shared__ __align__(16) uint8_t osm[NB * SB];
   __shared__ float red[kOutWaves][256];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int n0 = blockIdx.x * kOutCols;
-  const int K = p.k, nst = K / kStageK;           // a multiple of kStageBufs
+  const int K = p.k, nst = K / SK;           // a multiple of NB
   const int ksub = 8 * (lane >> 4);
-  // copies of a stage: rows (w >> 1) and (w >> 1) + 8, 1 KiB run w & 1 (rows
-  // past d_out copy the last row; never stored)
-  const uint16_t* ws0 = p.w + (int64_t)min(n0 + (w >> 1), p.n_out - 1) * K + 512 * (w & 1) + 8 * lane;
-  const uint16_t* ws1 = p.w + (int64_t)min(n0 + (w >> 1) + 8, p.n_out - 1) * K + 512 * (w & 1) + 8 * lane;
-  const int wd = (w >> 1) * kStageRow + 1024 * (w & 1);
+  // copy i of a stage: j = w + 16 i, row j / CPW, 1 KiB run j % CPW (rows past
+  // d_out copy the last row; never stored)
+  const uint16_t* wsrc[CPW];
+  int wd[CPW];
+#pragma unroll
+  for (int i = 0; i < CPW; ++i) {
+    const int j = w + 16 * i, r = j / CPW, run = j % CPW;
+    wsrc[i] = p.w + (int64_t)min(n0 + r, p.n_out - 1) * K + 512 * run + 8 * lane;
+    wd[i] = r * ROW + 1024 * run;
+  }
   // A operand: sequence lane & 15 (rows past the batch repeat the last
   // sequence; their outputs are never stored)
   const int brow = min(lane & 15, p.batch - 1);
@@ -146,49 +164,67 @@ __global__ __launch_bounds__(kOutWaves * 64) void absorbed_out_lds_kernel(Absorb
   // copy in flight (vmcnt(0)) in front of an LDS read it sees
   typedef __attribute__((address_space(3))) uint8_t lds_u8;
   const uint32_t sw_lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u8*)osm)) +
-                          (lane & 15) * kStageRow + 2 * ksub + 64 * w;
-  u4 lat[kStageBufs][4];
+                          (lane & 15) * ROW + 2 * ksub + 64 * w;
+  u4 lat[NB][2 * CPW];
   f4 acc = (f4){0, 0, 0, 0};
-  auto issue = [&](int st, u4(&l)[4]) {
-    uint8_t* dst = osm + (st % kStageBufs) * kStageBytes + wd;
-    const int64_t c = (int64_t)st * kStageK;
-    __builtin_amdgcn_global_load_lds(ws0 + c, dst, 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(ws1 + c, dst + 8 * kStageRow, 16, 0, 0);
-    l[0] = *reinterpret_cast<const u4*>(hi + c);
-    l[1] = *reinterpret_cast<const u4*>(lo + c);
-    l[2] = *reinterpret_cast<const u4*>(hi + c + 512);
-    l[3] = *reinterpret_cast<const u4*>(lo + c + 512);
-  };
-  // stage st (buffer u = st % 4) with `later` stages still in flight after it;
-  // the fragments are read before the next copies go out, which then take
-  // buffer (u + 3) % 4, the one that held stage st - 1
-  auto step = [&](int u, int st, int later, bool more) {
-    if (later == 2) __builtin_amdgcn_s_waitcnt(0x0F7C);        // vmcnt(12)
-    else if (later == 1) __builtin_amdgcn_s_waitcnt(0x0F76);   // vmcnt(6)
-    else __builtin_amdgcn_s_waitcnt(0x0F70);                   // vmcnt(0)
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    u4 b0, b1;
-    asm volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %2 offset:1024"
-                 : "=v"(b0), "=v"(b1) : "v"(sw_lds + u * kStageBytes) : "memory");
-    if (more) issue(st + 3, lat[(u + 3) % kStageBufs]);
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(b0), "+v"(b1) :: "memory");
-    acc = mfma16(lat[u][0], b0, acc);
-    acc = mfma16(lat[u][1], b0, acc);
-    acc = mfma16(lat[u][2], b1, acc);
-    acc = mfma16(lat[u][3], b1, acc);
-  };
-  issue(0, lat[0]);
-  issue(1, lat[1]);
-  issue(2, lat[2]);
-  int s0 = 0;
-  for (; s0 < nst - kStageBufs; s0 += kStageBufs) {
+  auto issue = [&](int st, u4(&l)[2 * CPW]) {
+    uint8_t* dst = osm + (st % NB) * SB;
+    const int64_t c = (int64_t)st * SK;
 #pragma unroll
-    for (int u = 0; u < kStageBufs; ++u) step(u, s0 + u, 2, true);
+    for (int i = 0; i < CPW; ++i) __builtin_amdgcn_global_load_lds(wsrc[i] + c, dst + wd[i], 16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < CPW; ++i) {
+      l[2 * i] = *reinterpret_cast<const u4*>(hi + c + 512 * i);
+      l[2 * i + 1] = *reinterpret_cast<const u4*>(lo + c + 512 * i);
+    }
+  };
+  // stage st (buffer u = st % NB) with `later` stages still in flight after
+  // it; the fragments are read before the next copies go out, which then take
+  // buffer (u + AHEAD) % NB, the one that held stage st - 1
+  // `later` is a constant once the loops below are unrolled: the switch folds
+  auto wait_later = [](int later) {
+    static_assert(AHEAD <= 8, "cases below");
+    switch (later) {
+      case 0: wait_vmcnt<0>(); break;
+      case 1: wait_vmcnt<OPS>(); break;
+      case 2: wait_vmcnt<2 * OPS>(); break;
+      case 3: wait_vmcnt<3 * OPS>(); break;
+      case 4: wait_vmcnt<4 * OPS>(); break;
+      case 5: wait_vmcnt<5 * OPS>(); break;
+      case 6: wait_vmcnt<6 * OPS>(); break;
+      default: wait_vmcnt<7 * OPS>(); break;
+    }
+  };
+  auto step = [&](int later, int u, int st, bool more) {
+    wait_later(later);
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    u4 bf[CPW];
+    if constexpr (CPW == 2) {
+      asm volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %2 offset:1024"
+                   : "=v"(bf[0]), "=v"(bf[1]) : "v"(sw_lds + u * SB) : "memory");
+    } else {
+      asm volatile("ds_read_b128 %0, %1" : "=v"(bf[0]) : "v"(sw_lds + u * SB) : "memory");
+    }
+    if (more) issue(st + AHEAD, lat[(u + AHEAD) % NB]);
+    if constexpr (CPW == 2) asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(bf[0]), "+v"(bf[1]) :: "memory");
+    else asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(bf[0]) :: "memory");
+#pragma unroll
+    for (int i = 0; i < CPW; ++i) {
+      acc = mfma16(lat[u][2 * i], bf[i], acc);
+      acc = mfma16(lat[u][2 * i + 1], bf[i], acc);
+    }
+  };
+#pragma unroll
+  for (int st = 0; st < AHEAD; ++st) issue(st, lat[st]);
+  int s0 = 0;
+  for (; s0 < nst - NB; s0 += NB) {
+#pragma unroll
+    for (int u = 0; u < NB; ++u) step(AHEAD - 1, u, s0 + u, true);
   }
-  step(0, s0, 2, true);
-  step(1, s0 + 1, 2, false);
-  step(2, s0 + 2, 1, false);
-  step(3, s0 + 3, 0, false);
+  // the last NB stages: stage s0 + u has min(AHEAD - 1, NB - 1 - u) later
+  // stages in flight, and only the first still issues one
+#pragma unroll
+  for (int u = 0; u < NB; ++u) step(min(AHEAD - 1, NB - 1 - u), u, s0 + u, u == 0);
   // lane holds rows 4*(lane/16)+e (sequences) of column lane%16 (outputs)
 #pragma unroll
   for (int e = 0; e < 4; ++e) red[w][e * 64 + lane] = acc[e];
@@ -219,7 +255,7 @@ int launch_absorbed_out(const AbsorbParams& p, void* stream) {
   dim3 grid((p.n_out + kOutCols - 1) / kOutCols, (p.batch + kOutRows - 1) / kOutRows);
   dim3 block(kOutWaves * 64);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (p.batch <= 16 && p.k % (kStageBufs * kStageK) == 0)
+  if (p.batch <= 16 && p.k % (ABS_NB * ABS_SK) == 0)
     hipLaunchKernelGGL(absorbed_out_lds_kernel, dim3(grid.x), block, 0, st, p);
   else if (p.batch <= 16) hipLaunchKernelGGL(absorbed_out_kernel<1>, grid, block, 0, st, p);
   else if (p.batch <= 32) hipLaunchKernelGGL(absorbed_out_kernel<2>, grid, block, 0, st, p);
