@@ -311,6 +311,16 @@ def test_absorbed_output_matches_oracle(name, ctx, batch, d_out, ragged, peaked)
     _absorbed_case(w, inp, d_out)
 
 
+def test_absorbed_output_single_block_of_stages_fp32():
+    """H_q * r_v = 4096 (32 heads x value rank 128): the staged product's smallest K, where
+    its whole pipeline is the closing block of stages (fill, no steady state, drain), at 1, 5
+    and 16 sequences and an output width that is not a multiple of 16."""
+    for batch, d_out in ((1, 40), (5, 4096), (16, 200)):
+        w = small("c3", ctx=300, batch=batch).with_(value_rank=128, out_dtype=synth.DT_F32)
+        inp = synth.generate(w)
+        _absorbed_case(w, inp, d_out)
+
+
 def test_absorbed_output_empty_and_clamped_contexts_fp32():
     w = small("c3", ctx=600, batch=3).with_(out_dtype=synth.DT_F32)
     inp = synth.generate(w)
